@@ -1,0 +1,65 @@
+"""Builds libcosta_mi355x.so (the C-ABI library) in place with hipcc for gfx950.
+
+Also builds the seeded-input fill library used by tests and benchmarks
+(synth/libcosta_synth.so); the CPU oracle is built separately by oracle.build().
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+LIB = os.path.join(PKG, "libcosta_mi355x.so")
+SYNTH_SRC = os.path.join(ROOT, "synth", "fill.hip")
+SYNTH_LIB = os.path.join(ROOT, "synth", "libcosta_synth.so")
+BUILD_DIR = os.path.join(ROOT, "_build")
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+# -ffp-contract=off: no FMA contraction, so a*b + c is rounded twice exactly as written.
+# packed-fp32-ops disabled: no packed fp32 instructions are generated.
+COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off",
+          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-Wall", "-Wno-unused-function"]
+SOURCES = ["layout.cpp", "lap.cpp", "plan.cpp", "api.cpp", "kernels.hip"]
+
+
+def _run(cmd):
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    out = "\n".join(l for l in r.stdout.splitlines() if "packed-fp32-ops" not in l)
+    if r.returncode != 0:
+        raise RuntimeError("build failed: " + " ".join(cmd) + "\n" + out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    objs = []
+    jobs = []
+    for src in SOURCES:
+        path = os.path.join(CSRC, src)
+        obj = os.path.join(BUILD_DIR, src + ".o")
+        objs.append(obj)
+        lang = ["-x", "hip"]
+        jobs.append([HIPCC, f"--offload-arch={ARCH}", *COMMON, *lang, "-c", path, "-o", obj])
+    with ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
+        outs = list(ex.map(_run, jobs))
+    if verbose:
+        for o in outs:
+            if o.strip():
+                print(o)
+    tmp = LIB + ".tmp"
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    os.replace(tmp, LIB)
+    tmp = SYNTH_LIB + ".tmp"
+    _run([HIPCC, f"--offload-arch={ARCH}", *COMMON, "-shared", "-o", tmp, SYNTH_SRC])
+    os.replace(tmp, SYNTH_LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

@@ -1,0 +1,645 @@
+// C ABI entry points: volume matrix, transform, batched transform, plan
+// statistics, workspace control and kernel timing.  Plans are cached per
+// (device, element size, layouts, ops, relabeling, workspace cap).
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <new>
+#include <string>
+
+#include "plan.hpp"
+
+namespace costa {
+namespace {
+
+constexpr int64_t kMaxPieceElems = 1 << 16;
+constexpr int64_t kMinGroupElems = 1 << 14;
+constexpr int32_t kMaxGroupPieces = 64;
+
+int elem_size(costa_dtype d) {
+  switch (d) {
+    case COSTA_R64: return 8;
+    case COSTA_C128: return 16;
+    case COSTA_R32: return 4;
+    case COSTA_C64: return 8;
+  }
+  return 0;
+}
+bool is_complex(costa_dtype d) { return d == COSTA_C128 || d == COSTA_C64; }
+
+#define HIP_OR_FAIL(expr)                                                                      \
+  do {                                                                                         \
+    hipError_t e_ = (expr);                                                                    \
+    if (e_ != hipSuccess)                                                                      \
+      return fail(COSTA_ERROR_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_));      \
+  } while (0)
+
+struct DevicePlan {
+  HostPlan host;
+  int device = -1;
+  Piece* d_pieces = nullptr;
+  int32_t* d_groups = nullptr;
+  // per-call table: buffer pointers then pair parameters
+  void* d_table = nullptr;
+  void* h_staging = nullptr;  // pinned
+  size_t table_bytes = 0;
+  size_t nbufs = 0;
+  std::vector<unsigned char> last_table;
+  hipEvent_t table_event = nullptr;
+  bool table_pending = false;
+  ~DevicePlan() {
+    if (d_pieces) (void)hipFree(d_pieces);
+    if (d_groups) (void)hipFree(d_groups);
+    if (d_table) (void)hipFree(d_table);
+    if (h_staging) (void)hipHostFree(h_staging);
+    if (table_event) (void)hipEventDestroy(table_event);
+  }
+};
+
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+  hipEvent_t last_use = nullptr;
+  hipStream_t last_stream = nullptr;
+  bool used = false;
+};
+
+struct TimingRec {
+  costa_kernel_kind kind;
+  hipEvent_t start, stop;
+  int64_t bytes;
+};
+
+struct State {
+  std::mutex mu;
+  size_t workspace_limit = 0;
+  std::map<std::string, std::unique_ptr<DevicePlan>> plans;
+  std::map<std::string, std::unique_ptr<HostPlan>> host_plans;  // plan statistics without a device
+  std::map<int, Workspace> ws;
+  bool timing = false;
+  std::vector<TimingRec> pending;
+  std::vector<hipEvent_t> event_pool;
+  costa_timing totals{};
+};
+
+State& state() {
+  static State* s = new State();
+  return *s;
+}
+
+std::string plan_key(int device, int es, const std::vector<ItemDesc>& items, const std::vector<int32_t>& sigma,
+                     size_t cap) {
+  std::string k;
+  auto put = [&](const void* p, size_t n) { k.append(reinterpret_cast<const char*>(p), n); };
+  put(&device, sizeof device);
+  put(&es, sizeof es);
+  put(&cap, sizeof cap);
+  size_t n = items.size();
+  put(&n, sizeof n);
+  for (const ItemDesc& d : items) {
+    put(&d.A->id, sizeof d.A->id);
+    put(&d.B->id, sizeof d.B->id);
+    int32_t t = d.op == COSTA_OP_N ? 0 : 1;  // T and C move the same data
+    put(&t, sizeof t);
+  }
+  size_t ns = sigma.size();
+  put(&ns, sizeof ns);
+  if (ns) put(sigma.data(), ns * sizeof(int32_t));
+  return k;
+}
+
+PlanConfig make_config(int es) {
+  PlanConfig c;
+  c.elem_size = es;
+  c.workspace_cap = INT64_MAX;
+  c.max_piece_elems = kMaxPieceElems;
+  c.min_group_elems = kMinGroupElems;
+  c.max_group_pieces = kMaxGroupPieces;
+  return c;
+}
+
+// Validates a batch; fills `items` and `sig`.  No device calls.
+costa_status validate(costa_dtype dtype, int32_t n, const costa_transform_desc* desc, const int32_t* sigma,
+                      bool need_buffers, std::vector<ItemDesc>& items, std::vector<int32_t>& sig) {
+  if (elem_size(dtype) == 0) return fail(COSTA_ERROR_INVALID_VALUE, "unknown dtype");
+  if (n < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative batch size");
+  if (n > 0 && !desc) return fail(COSTA_ERROR_INVALID_VALUE, "null descriptor array");
+  if (n > 0xFFFF) return fail(COSTA_ERROR_NOT_SUPPORTED, "batch larger than 65535 pairs");
+  items.clear();
+  int32_t P = -1;
+  for (int32_t k = 0; k < n; ++k) {
+    const costa_transform_desc& d = desc[k];
+    const Layout* A = layout_of(d.A);
+    const Layout* B = layout_of(d.B);
+    if (!A || !B) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
+    if (d.op != COSTA_OP_N && d.op != COSTA_OP_T && d.op != COSTA_OP_C)
+      return fail(COSTA_ERROR_INVALID_VALUE, "unknown op");
+    const bool tr = d.op != COSTA_OP_N;
+    if (A->nrows != (tr ? B->ncols : B->nrows) || A->ncols != (tr ? B->nrows : B->ncols))
+      return fail(COSTA_ERROR_SHAPE_MISMATCH, "A is not the shape of op(B)");
+    if (A->nranks != B->nranks) return fail(COSTA_ERROR_SHAPE_MISMATCH, "layouts of A and B have different P");
+    if (P >= 0 && A->nranks != P) return fail(COSTA_ERROR_SHAPE_MISMATCH, "pairs of a batch have different P");
+    P = A->nranks;
+    if (A->nrows > INT32_MAX || A->ncols > INT32_MAX)
+      return fail(COSTA_ERROR_NOT_SUPPORTED, "matrix dimension above 2^31-1");
+    if (need_buffers) {
+      if (!d.alpha || !d.beta) return fail(COSTA_ERROR_INVALID_VALUE, "null alpha or beta");
+      if (!d.A_local || !d.B_local) return fail(COSTA_ERROR_INVALID_VALUE, "null buffer array");
+    }
+    items.push_back(ItemDesc{A, B, d.op});
+  }
+  sig.clear();
+  if (sigma && P > 0) {
+    std::vector<char> seen(P, 0);
+    for (int32_t t = 0; t < P; ++t) {
+      if (sigma[t] < 0 || sigma[t] >= P || seen[sigma[t]])
+        return fail(COSTA_ERROR_INVALID_VALUE, "sigma is not a permutation of 0..P-1");
+      seen[sigma[t]] = 1;
+    }
+    bool ident = true;
+    for (int32_t t = 0; t < P; ++t) ident = ident && sigma[t] == t;
+    if (!ident) sig.assign(sigma, sigma + P);
+  }
+  if (need_buffers) {
+    for (int32_t k = 0; k < n; ++k) {
+      const Layout* A = items[k].A;
+      const Layout* B = items[k].B;
+      for (int32_t t = 0; t < P; ++t) {
+        int32_t r = sig.empty() ? t : sig[t];
+        if (A->local_elems[t] > 0 && !desc[k].A_local[r])
+          return fail(COSTA_ERROR_INVALID_VALUE, "null A buffer for a rank that holds data");
+        if (B->local_elems[t] > 0 && !desc[k].B_local[t])
+          return fail(COSTA_ERROR_INVALID_VALUE, "null B buffer for a rank that holds data");
+      }
+    }
+  }
+  return COSTA_SUCCESS;
+}
+
+bool is_zero(costa_dtype dt, const void* p) {
+  if (dt == COSTA_R64) return *(const double*)p == 0.0;
+  if (dt == COSTA_C128) return ((const double*)p)[0] == 0.0 && ((const double*)p)[1] == 0.0;
+  if (dt == COSTA_R32) return *(const float*)p == 0.0f;
+  return ((const float*)p)[0] == 0.0f && ((const float*)p)[1] == 0.0f;
+}
+bool is_one(costa_dtype dt, const void* p) {
+  if (dt == COSTA_R64) return *(const double*)p == 1.0;
+  if (dt == COSTA_C128) return ((const double*)p)[0] == 1.0 && ((const double*)p)[1] == 0.0;
+  if (dt == COSTA_R32) return *(const float*)p == 1.0f;
+  return ((const float*)p)[0] == 1.0f && ((const float*)p)[1] == 0.0f;
+}
+void to_pair(costa_dtype dt, const void* p, double out[2]) {
+  out[0] = out[1] = 0.0;
+  if (dt == COSTA_R64) out[0] = *(const double*)p;
+  else if (dt == COSTA_C128) { out[0] = ((const double*)p)[0]; out[1] = ((const double*)p)[1]; }
+  else if (dt == COSTA_R32) out[0] = *(const float*)p;
+  else { out[0] = ((const float*)p)[0]; out[1] = ((const float*)p)[1]; }
+}
+
+hipEvent_t get_event(State& S) {
+  if (!S.event_pool.empty()) {
+    hipEvent_t e = S.event_pool.back();
+    S.event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+costa_status collect_timing(State& S) {
+  for (TimingRec& r : S.pending) {
+    HIP_OR_FAIL(hipEventSynchronize(r.stop));
+    float ms = 0.f;
+    HIP_OR_FAIL(hipEventElapsedTime(&ms, r.start, r.stop));
+    S.totals.ms[r.kind] += ms;
+    S.totals.launches[r.kind] += 1;
+    S.totals.bytes[r.kind] += r.bytes;
+    S.event_pool.push_back(r.start);
+    S.event_pool.push_back(r.stop);
+  }
+  S.pending.clear();
+  return COSTA_SUCCESS;
+}
+
+// Launches one mover range, bracketed by timing events when enabled.
+costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePlan& dp, const LaunchRange& lr,
+                       void* const* d_bufs, const ItemParam* d_items, int32_t allow_wide, int64_t bytes,
+                       hipStream_t stream) {
+  if (lr.ngroups == 0) return COSTA_SUCCESS;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (S.timing) {
+    if (S.pending.size() > 4096) {
+      costa_status st = collect_timing(S);
+      if (st != COSTA_SUCCESS) return st;
+    }
+    e0 = get_event(S);
+    e1 = get_event(S);
+    if (!e0 || !e1) return fail(COSTA_ERROR_DEVICE, "hipEventCreate failed");
+    HIP_OR_FAIL(hipEventRecord(e0, stream));
+  }
+  HIP_OR_FAIL(launch_mover(kind, dt, dp.d_pieces, dp.d_groups + lr.group_begin, lr.ngroups, d_bufs, d_items,
+                           allow_wide, stream));
+  if (S.timing) {
+    HIP_OR_FAIL(hipEventRecord(e1, stream));
+    costa_kernel_kind kk = kind == KIND_PACK ? COSTA_KERNEL_PACK
+                           : kind == KIND_UNPACK ? COSTA_KERNEL_UNPACK
+                                                 : COSTA_KERNEL_DIRECT;
+    S.pending.push_back(TimingRec{kk, e0, e1, bytes});
+  }
+  return COSTA_SUCCESS;
+}
+
+int64_t range_bytes(const LaunchRange& lr, int es, const std::vector<char>& reads_a) {
+  int64_t b = 0;
+  for (size_t k = 0; k < lr.item_elems.size(); ++k) b += lr.item_elems[k] * es * (2 + (reads_a[k] ? 1 : 0));
+  return b;
+}
+
+// Message workspace of the current device, at least `bytes` large.
+costa_status ensure_workspace(State& S, int device, size_t bytes, Workspace*& out) {
+  Workspace& w = S.ws[device];
+  out = &w;
+  if (w.bytes >= bytes) return COSTA_SUCCESS;
+  if (w.ptr) {
+    HIP_OR_FAIL(hipDeviceSynchronize());
+    HIP_OR_FAIL(hipFree(w.ptr));
+    w.ptr = nullptr;
+    w.bytes = 0;
+  }
+  if (bytes == 0) return COSTA_SUCCESS;
+  hipError_t e = hipMalloc(&w.ptr, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    w.ptr = nullptr;
+    return fail(COSTA_ERROR_OUT_OF_MEMORY, "cannot allocate " + std::to_string(bytes) + " bytes of message workspace");
+  }
+  w.bytes = bytes;
+  if (!w.last_use) HIP_OR_FAIL(hipEventCreateWithFlags(&w.last_use, hipEventDisableTiming));
+  return COSTA_SUCCESS;
+}
+
+int64_t auto_cap(State& S, int device, int64_t needed) {
+  if (S.workspace_limit) return std::min<int64_t>(needed, (int64_t)S.workspace_limit);
+  size_t free_b = 0, total_b = 0;
+  if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) {
+    (void)hipGetLastError();
+    return needed;
+  }
+  int64_t have = (int64_t)S.ws[device].bytes + (int64_t)free_b;  // the current workspace can be reused
+  int64_t cap = (int64_t)(0.6 * (double)have);
+  cap = std::max<int64_t>(cap, 64ll << 20);
+  return std::min(needed, cap);
+}
+
+costa_status get_plan(State& S, costa_dtype dt, const std::vector<ItemDesc>& items, const std::vector<int32_t>& sig,
+                      DevicePlan*& out) {
+  int device = 0;
+  HIP_OR_FAIL(hipGetDevice(&device));
+  const int es = elem_size(dt);
+  std::string key = plan_key(device, es, items, sig, S.workspace_limit);
+  auto it = S.plans.find(key);
+  if (it != S.plans.end()) {
+    out = it->second.get();
+    return COSTA_SUCCESS;
+  }
+  if (S.plans.size() >= 32) {  // bounded cache: drop everything (plans are cheap to rebuild)
+    HIP_OR_FAIL(hipDeviceSynchronize());
+    S.plans.clear();
+  }
+  std::unique_ptr<DevicePlan> dp(new (std::nothrow) DevicePlan());
+  if (!dp) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
+  dp->device = device;
+  PlanConfig cfg = make_config(es);
+  try {
+    build_plan(items, sig, cfg, [&](int64_t need) { return auto_cap(S, device, need); }, dp->host);
+  } catch (const std::bad_alloc&) {
+    return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed while planning");
+  }
+  const HostPlan& hp = dp->host;
+  if (!hp.pieces.empty()) {
+    HIP_OR_FAIL(hipMalloc(&dp->d_pieces, hp.pieces.size() * sizeof(Piece)));
+    HIP_OR_FAIL(hipMemcpy(dp->d_pieces, hp.pieces.data(), hp.pieces.size() * sizeof(Piece), hipMemcpyHostToDevice));
+    HIP_OR_FAIL(hipMalloc(&dp->d_groups, hp.groups.size() * sizeof(int32_t)));
+    HIP_OR_FAIL(hipMemcpy(dp->d_groups, hp.groups.data(), hp.groups.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+  }
+  const int32_t P = items.empty() ? 0 : items[0].A->nranks;
+  dp->nbufs = (size_t)2 * items.size() * P + 1;
+  size_t ptr_bytes = (dp->nbufs * sizeof(void*) + 63) / 64 * 64;
+  dp->table_bytes = ptr_bytes + items.size() * sizeof(ItemParam);
+  HIP_OR_FAIL(hipMalloc(&dp->d_table, dp->table_bytes));
+  HIP_OR_FAIL(hipHostMalloc(&dp->h_staging, dp->table_bytes, hipHostMallocDefault));
+  HIP_OR_FAIL(hipEventCreateWithFlags(&dp->table_event, hipEventDisableTiming));
+  out = dp.get();
+  S.plans.emplace(key, std::move(dp));
+  return COSTA_SUCCESS;
+}
+
+costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_desc* desc, const int32_t* sigma,
+                            hipStream_t stream) {
+  State& S = state();
+  std::vector<ItemDesc> items;
+  std::vector<int32_t> sig;
+  costa_status st = validate(dt, n, desc, sigma, true, items, sig);
+  if (st != COSTA_SUCCESS) return st;
+  std::lock_guard<std::mutex> lock(S.mu);
+  int64_t total = 0;
+  for (const ItemDesc& d : items) total += d.A->nrows * d.A->ncols;
+  if (total == 0) return COSTA_SUCCESS;
+  DevicePlan* dp = nullptr;
+  st = get_plan(S, dt, items, sig, dp);
+  if (st != COSTA_SUCCESS) return st;
+  const HostPlan& hp = dp->host;
+  const int es = elem_size(dt);
+  const int32_t P = items[0].A->nranks;
+
+  Workspace* ws = nullptr;
+  st = ensure_workspace(S, dp->device, (size_t)hp.workspace_bytes, ws);
+  if (st != COSTA_SUCCESS) return st;
+
+  // call table: buffer pointers, then pair parameters
+  std::vector<unsigned char> table(dp->table_bytes, 0);
+  void** bp = reinterpret_cast<void**>(table.data());
+  bool aligned = true;
+  auto note = [&](const void* p) { aligned = aligned && ((uintptr_t)p % 16 == 0); };
+  for (int32_t k = 0; k < n; ++k)
+    for (int32_t r = 0; r < P; ++r) {
+      bp[(size_t)k * P + r] = desc[k].A_local[r];
+      bp[(size_t)n * P + (size_t)k * P + r] = const_cast<void*>(desc[k].B_local[r]);
+      note(desc[k].A_local[r]);
+      note(desc[k].B_local[r]);
+    }
+  bp[(size_t)2 * n * P] = ws->ptr;
+  size_t ptr_bytes = (dp->nbufs * sizeof(void*) + 63) / 64 * 64;
+  ItemParam* ipar = reinterpret_cast<ItemParam*>(table.data() + ptr_bytes);
+  std::vector<char> reads_a(n, 0);
+  for (int32_t k = 0; k < n; ++k) {
+    ItemParam& q = ipar[k];
+    to_pair(dt, desc[k].alpha, q.alpha);
+    to_pair(dt, desc[k].beta, q.beta);
+    const bool bz = is_zero(dt, desc[k].beta);
+    q.mode = bz ? (is_one(dt, desc[k].alpha) ? MODE_COPY : MODE_SCALE) : MODE_AXPBY;
+    q.conj = (desc[k].op == COSTA_OP_C && is_complex(dt)) ? 1 : 0;
+    reads_a[k] = !bz;
+  }
+  if (table != dp->last_table) {
+    if (dp->table_pending) HIP_OR_FAIL(hipEventSynchronize(dp->table_event));
+    std::memcpy(dp->h_staging, table.data(), table.size());
+    HIP_OR_FAIL(hipMemcpyAsync(dp->d_table, dp->h_staging, table.size(), hipMemcpyHostToDevice, stream));
+    HIP_OR_FAIL(hipEventRecord(dp->table_event, stream));
+    dp->table_pending = true;
+    dp->last_table.swap(table);
+  }
+  // message buffers are shared by every call on this device: order after the last user
+  if (ws->used && ws->last_stream != stream) HIP_OR_FAIL(hipStreamWaitEvent(stream, ws->last_use, 0));
+
+  void* const* d_bufs = reinterpret_cast<void* const*>(dp->d_table);
+  const ItemParam* d_items = reinterpret_cast<const ItemParam*>((unsigned char*)dp->d_table + ptr_bytes);
+  const int32_t wide = aligned ? 1 : 0;
+  st = run_range(S, KIND_DIRECT, dt, *dp, hp.direct, d_bufs, d_items, wide, range_bytes(hp.direct, es, reads_a),
+                 stream);
+  if (st != COSTA_SUCCESS) return st;
+  std::vector<char> no_read(n, 0);
+  for (const Wave& w : hp.waves) {
+    st = run_range(S, KIND_PACK, dt, *dp, w.pack, d_bufs, d_items, wide, range_bytes(w.pack, es, no_read), stream);
+    if (st != COSTA_SUCCESS) return st;
+    st = run_range(S, KIND_UNPACK, dt, *dp, w.unpack, d_bufs, d_items, wide, range_bytes(w.unpack, es, reads_a),
+                   stream);
+    if (st != COSTA_SUCCESS) return st;
+  }
+  if (ws->last_use) {
+    HIP_OR_FAIL(hipEventRecord(ws->last_use, stream));
+    ws->last_stream = stream;
+    ws->used = true;
+  }
+  return COSTA_SUCCESS;
+}
+
+}  // namespace
+}  // namespace costa
+
+using namespace costa;
+
+extern "C" costa_status costa_transform(costa_dtype dtype, costa_op op, const void* alpha, const void* beta,
+                                        costa_layout A, void* const* A_local, costa_layout B,
+                                        const void* const* B_local, const int32_t* sigma, hipStream_t stream) {
+  costa_transform_desc d{op, alpha, beta, A, A_local, B, B_local};
+  return transform_impl(dtype, 1, &d, sigma, stream);
+}
+
+extern "C" costa_status costa_transform_batched(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
+                                                const int32_t* sigma, hipStream_t stream) {
+  return transform_impl(dtype, n, desc, sigma, stream);
+}
+
+extern "C" costa_status costa_set_workspace_limit(size_t bytes) {
+  State& S = state();
+  std::lock_guard<std::mutex> lock(S.mu);
+  S.workspace_limit = bytes;
+  return COSTA_SUCCESS;
+}
+
+// Host-only plan (no device): the workspace cap is the user limit, else unlimited.
+costa_status host_plan(costa_dtype dtype, int32_t n, const costa_transform_desc* desc, const int32_t* sigma,
+                       const HostPlan*& out) {
+  std::vector<ItemDesc> items;
+  std::vector<int32_t> sig;
+  costa_status st = validate(dtype, n, desc, sigma, false, items, sig);
+  if (st != COSTA_SUCCESS) return st;
+  State& S = state();
+  const int es = elem_size(dtype);
+  std::string key = plan_key(-1, es, items, sig, S.workspace_limit);
+  auto it = S.host_plans.find(key);
+  if (it == S.host_plans.end()) {
+    if (S.host_plans.size() >= 32) S.host_plans.clear();
+    std::unique_ptr<HostPlan> hp(new (std::nothrow) HostPlan());
+    if (!hp) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
+    PlanConfig cfg = make_config(es);
+    size_t lim = S.workspace_limit;
+    try {
+      build_plan(items, sig, cfg, [lim](int64_t need) { return lim ? std::min<int64_t>(need, (int64_t)lim) : need; },
+                 *hp);
+    } catch (const std::bad_alloc&) {
+      return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed while planning");
+    }
+    it = S.host_plans.emplace(key, std::move(hp)).first;
+  }
+  out = it->second.get();
+  return COSTA_SUCCESS;
+}
+
+extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
+                                          const int32_t* sigma, costa_piece_info* out, int64_t capacity,
+                                          int64_t* count) {
+  if (!count || capacity < 0 || (capacity > 0 && !out)) return fail(COSTA_ERROR_INVALID_VALUE, "bad output array");
+  State& S = state();
+  std::lock_guard<std::mutex> lock(S.mu);
+  const HostPlan* hp = nullptr;
+  costa_status st = host_plan(dtype, n, desc, sigma, hp);
+  if (st != COSTA_SUCCESS) return st;
+  int64_t k = 0;
+  auto emit = [&](const LaunchRange& lr, costa_kernel_kind kind, int32_t wave) {
+    for (int64_t g = 0; g < lr.ngroups; ++g)
+      for (int32_t p = hp->groups[lr.group_begin + g]; p < hp->groups[lr.group_begin + g + 1]; ++p, ++k) {
+        if (k >= capacity) continue;
+        const Piece& q = hp->pieces[p];
+        costa_piece_info& o = out[k];
+        o.kind = kind;
+        o.wave = wave;
+        o.group = g;
+        o.src_off = q.src_off;
+        o.dst_off = q.dst_off;
+        o.src_ld = q.src_ld;
+        o.dst_ld = q.dst_ld;
+        o.src_buf = q.src_buf;
+        o.dst_buf = q.dst_buf;
+        o.nx = q.nx;
+        o.ny = q.ny;
+        o.item = q.item;
+        o.flags = q.flags;
+      }
+  };
+  emit(hp->direct, COSTA_KERNEL_DIRECT, 0);
+  for (size_t w = 0; w < hp->waves.size(); ++w) {
+    emit(hp->waves[w].pack, COSTA_KERNEL_PACK, (int32_t)w);
+    emit(hp->waves[w].unpack, COSTA_KERNEL_UNPACK, (int32_t)w);
+  }
+  *count = k;
+  return COSTA_SUCCESS;
+}
+
+extern "C" costa_status costa_plan_stats(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
+                                         const int32_t* sigma, costa_stats* out) {
+  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output");
+  State& S = state();
+  std::lock_guard<std::mutex> lock(S.mu);
+  const HostPlan* hpp = nullptr;
+  costa_status st = host_plan(dtype, n, desc, sigma, hpp);
+  if (st != COSTA_SUCCESS) return st;
+  const HostPlan& hp = *hpp;
+  const int es = elem_size(dtype);
+  costa_stats s{};
+  s.overlay_blocks = hp.overlay_blocks;
+  for (int32_t k = 0; k < n; ++k) {
+    bool reads_a = !(desc[k].beta && is_zero(dtype, desc[k].beta));
+    s.total_elems += hp.item_total[k];
+    s.local_elems += hp.item_local[k];
+    s.remote_elems += hp.item_remote[k];
+    s.model_bytes += (int64_t)es * (hp.item_total[k] * (2 + (reads_a ? 1 : 0)) + 2 * hp.item_remote[k]);
+    s.pack_bytes += (int64_t)es * 2 * hp.item_remote[k];
+    s.unpack_bytes += (int64_t)es * hp.item_remote[k] * (2 + (reads_a ? 1 : 0));
+    s.direct_bytes += (int64_t)es * hp.item_local[k] * (2 + (reads_a ? 1 : 0));
+  }
+  s.message_bytes = (int64_t)es * s.remote_elems;
+  s.workspace_bytes = hp.workspace_bytes;
+  s.waves = (int32_t)hp.waves.size();
+  s.pieces_pack = hp.pieces_pack;
+  s.pieces_unpack = hp.pieces_unpack;
+  s.pieces_direct = hp.pieces_direct;
+  s.plan_ms = hp.plan_ms;
+  *out = s;
+  return COSTA_SUCCESS;
+}
+
+extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, costa_op op, int64_t* V_host,
+                                            hipStream_t stream) {
+  const Layout* A = layout_of(A_h);
+  const Layout* B = layout_of(B_h);
+  if (!A || !B || !V_host) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
+  if (op != COSTA_OP_N && op != COSTA_OP_T && op != COSTA_OP_C) return fail(COSTA_ERROR_INVALID_VALUE, "unknown op");
+  const bool tr = op != COSTA_OP_N;
+  if (A->nrows != (tr ? B->ncols : B->nrows) || A->ncols != (tr ? B->nrows : B->ncols))
+    return fail(COSTA_ERROR_SHAPE_MISMATCH, "A is not the shape of op(B)");
+  if (A->nranks != B->nranks) return fail(COSTA_ERROR_SHAPE_MISMATCH, "layouts of A and B have different P");
+  const int32_t P = A->nranks;
+  std::memset(V_host, 0, sizeof(int64_t) * (size_t)P * P);
+  std::vector<Interval> rows = overlay(A->rsplit, tr ? B->csplit : B->rsplit);
+  std::vector<Interval> cols = overlay(A->csplit, tr ? B->rsplit : B->csplit);
+  if (rows.empty() || cols.empty()) return COSTA_SUCCESS;
+  State& S = state();
+  std::lock_guard<std::mutex> lock(S.mu);
+  Interval *d_rows = nullptr, *d_cols = nullptr;
+  int32_t *d_oa = nullptr, *d_ob = nullptr;
+  unsigned long long* d_v = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  costa_status st = COSTA_SUCCESS;
+  auto check = [&](hipError_t e, const char* what) {
+    if (e != hipSuccess && st == COSTA_SUCCESS) st = fail(COSTA_ERROR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+    return st == COSTA_SUCCESS;
+  };
+  if (check(hipMalloc(&d_rows, rows.size() * sizeof(Interval)), "hipMalloc") &&
+      check(hipMalloc(&d_cols, cols.size() * sizeof(Interval)), "hipMalloc") &&
+      check(hipMalloc(&d_oa, A->owner.size() * sizeof(int32_t)), "hipMalloc") &&
+      check(hipMalloc(&d_ob, B->owner.size() * sizeof(int32_t)), "hipMalloc") &&
+      check(hipMalloc(&d_v, sizeof(unsigned long long) * (size_t)P * P), "hipMalloc") &&
+      check(hipMemcpyAsync(d_rows, rows.data(), rows.size() * sizeof(Interval), hipMemcpyHostToDevice, stream), "copy") &&
+      check(hipMemcpyAsync(d_cols, cols.data(), cols.size() * sizeof(Interval), hipMemcpyHostToDevice, stream), "copy") &&
+      check(hipMemcpyAsync(d_oa, A->owner.data(), A->owner.size() * sizeof(int32_t), hipMemcpyHostToDevice, stream), "copy") &&
+      check(hipMemcpyAsync(d_ob, B->owner.data(), B->owner.size() * sizeof(int32_t), hipMemcpyHostToDevice, stream), "copy") &&
+      check(hipMemcpyAsync(d_v, V_host, sizeof(int64_t) * (size_t)P * P, hipMemcpyHostToDevice, stream), "copy")) {
+    VolumeArgs a{d_rows, (int32_t)rows.size(), d_cols, (int32_t)cols.size(), d_oa, A->nbc, d_ob, B->nbc,
+                 tr ? 1 : 0, P, d_v};
+    if (S.timing) {
+      e0 = get_event(S);
+      e1 = get_event(S);
+      if (e0 && e1) check(hipEventRecord(e0, stream), "event");
+    }
+    if (check(launch_volume(a, stream), "volume kernel")) {
+      if (S.timing && e0 && e1 && check(hipEventRecord(e1, stream), "event")) {
+        S.pending.push_back(TimingRec{COSTA_KERNEL_VOLUME, e0, e1, (int64_t)(rows.size() + cols.size()) * 24});
+        e0 = e1 = nullptr;
+      }
+      if (check(hipMemcpyAsync(V_host, d_v, sizeof(int64_t) * (size_t)P * P, hipMemcpyDeviceToHost, stream), "copy"))
+        check(hipStreamSynchronize(stream), "sync");
+    }
+  }
+  (void)hipStreamSynchronize(stream);
+  if (e0) S.event_pool.push_back(e0);
+  if (e1) S.event_pool.push_back(e1);
+  if (d_rows) (void)hipFree(d_rows);
+  if (d_cols) (void)hipFree(d_cols);
+  if (d_oa) (void)hipFree(d_oa);
+  if (d_ob) (void)hipFree(d_ob);
+  if (d_v) (void)hipFree(d_v);
+  return st;
+}
+
+extern "C" costa_status costa_timing_enable(int on) {
+  State& S = state();
+  std::lock_guard<std::mutex> lock(S.mu);
+  costa_status st = collect_timing(S);
+  S.timing = on != 0;
+  S.totals = costa_timing{};
+  return st;
+}
+
+extern "C" costa_status costa_timing_read(costa_timing* out) {
+  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output");
+  State& S = state();
+  std::lock_guard<std::mutex> lock(S.mu);
+  costa_status st = collect_timing(S);
+  *out = S.totals;
+  return st;
+}
+
+extern "C" costa_status costa_finalize(void) {
+  State& S = state();
+  std::lock_guard<std::mutex> lock(S.mu);
+  if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty()) HIP_OR_FAIL(hipDeviceSynchronize());
+  S.pending.clear();
+  S.plans.clear();
+  S.host_plans.clear();
+  for (auto& kv : S.ws) {
+    if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+    if (kv.second.last_use) (void)hipEventDestroy(kv.second.last_use);
+  }
+  S.ws.clear();
+  for (hipEvent_t e : S.event_pool) (void)hipEventDestroy(e);
+  S.event_pool.clear();
+  S.timing = false;
+  S.totals = costa_timing{};
+  return COSTA_SUCCESS;
+}

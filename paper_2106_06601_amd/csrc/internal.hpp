@@ -1,0 +1,117 @@
+// Internal declarations shared by the host code and the kernels of the
+// layout-transform library.  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/costa.h"
+
+namespace costa {
+
+// ---- error reporting -------------------------------------------------------
+void set_error(const std::string& msg);
+costa_status fail(costa_status st, const std::string& msg);
+
+// ---- layouts (Section 5 "Matrix Layout", Figure 1) -------------------------
+struct Layout {
+  uint64_t id = 0;
+  int64_t nrows = 0, ncols = 0;
+  int32_t nbr = 0, nbc = 0;
+  int32_t nranks = 0;
+  costa_order order = COSTA_COL_MAJOR;
+  std::vector<int64_t> rsplit, csplit;  // nbr+1, nbc+1
+  std::vector<int32_t> owner;           // nbr*nbc row-major
+  std::vector<int64_t> boff, bld;       // nbr*nbc
+  std::vector<int64_t> local_elems;     // per rank
+  int64_t block(int32_t bi, int32_t bj) const { return (int64_t)bi * nbc + bj; }
+};
+
+// ---- grid overlay (Section 5 "Grid Overlay") -------------------------------
+// One interval of the union of two split lists, with the index of the
+// interval of each list that covers it.
+struct Interval {
+  int64_t start;
+  int64_t len;
+  int32_t a;  // covering block index in A's splits
+  int32_t b;  // covering block index in op(B)'s splits
+};
+std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<int64_t>& sb);
+
+// ---- work rectangles -------------------------------------------------------
+// A rectangle of elements moved with one addressing rule.  Coordinates are in
+// the destination's orientation: x runs along the destination's contiguous
+// direction.  dst(x, y) = dst_off + y*dst_ld + x.  The source is
+//   src_off + y*src_ld + x   (flag TRANSPOSE clear: contiguous along x), or
+//   src_off + x*src_ld + y   (flag TRANSPOSE set: contiguous along y).
+enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2 };
+
+struct alignas(16) Piece {
+  int64_t src_off;
+  int64_t dst_off;
+  int64_t src_ld;
+  int64_t dst_ld;
+  int32_t src_buf;  // index into the call's buffer table
+  int32_t dst_buf;
+  int32_t nx;
+  int32_t ny;
+  int32_t item;     // pair of a batched call (selects alpha, beta, mode)
+  int32_t flags;
+  float inv_nx;     // 1/nx (in the units the kernel walks: see PIECE_WIDE)
+  int32_t pad;
+};
+static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
+
+// Per-pair parameters of a call, read by the kernels.
+enum : int32_t { MODE_COPY = 0, MODE_SCALE = 1, MODE_AXPBY = 2 };
+struct alignas(16) ItemParam {
+  double alpha[2];
+  double beta[2];
+  int32_t mode;
+  int32_t conj;
+  int32_t pad[2];
+};
+static_assert(sizeof(ItemParam) == 48, "ItemParam must be 48 bytes");
+
+// One kernel launch of a plan: a range of pieces split into workgroup groups.
+struct LaunchRange {
+  int64_t group_begin = 0;  // index into Plan::groups (each group: [groups[g], groups[g+1]) of pieces)
+  int64_t ngroups = 0;
+  int64_t elems = 0;
+  std::vector<int64_t> item_elems;  // elements of each pair in this launch
+};
+
+struct Wave {
+  LaunchRange pack, unpack;
+  int64_t msg_bytes = 0;
+};
+
+// ---- kernels (kernels.hip) -------------------------------------------------
+enum MoverKind : int32_t { KIND_PACK = 0, KIND_UNPACK = 1, KIND_DIRECT = 2 };
+hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const Piece* pieces, const int32_t* groups,
+                        int64_t ngroups, void* const* bufs, const ItemParam* items, int32_t allow_wide,
+                        hipStream_t stream);
+
+struct VolumeArgs {
+  const Interval* rows;
+  int32_t K;
+  const Interval* cols;
+  int32_t L;
+  const int32_t* ownerA;
+  int32_t nbcA;
+  const int32_t* ownerB;
+  int32_t nbcB;
+  int32_t transposed;
+  int32_t P;
+  unsigned long long* V;
+};
+hipError_t launch_volume(const VolumeArgs& a, hipStream_t stream);
+
+// ---- relabeling (lap.cpp) --------------------------------------------------
+// Lexicographically smallest sigma maximising sum_t V[sigma[t]][t].
+void solve_relabel(int32_t P, const int64_t* V, int32_t* sigma);
+
+}  // namespace costa

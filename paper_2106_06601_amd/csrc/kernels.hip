@@ -1,0 +1,318 @@
+// HIP kernels for gfx950 (CDNA4): the rectangle mover used by the pack,
+// unpack-transform and direct paths, and the grid-overlay volume kernel.
+//
+// All of them are bound by HBM bandwidth: per element they read at most two
+// values and write one, with at most a few flops (Section 5 eq:costa).  The
+// design goals are therefore coalesced 64-lane accesses, 16-byte vectors
+// where the rectangle allows them, many independent loads in flight per lane,
+// an LDS tile for the rectangles whose source and destination run in
+// different directions, and a workgroup order that keeps neighbouring work on
+// one XCD (one L2).
+#include <hip/hip_runtime.h>
+
+#include "internal.hpp"
+
+// Products and sums are rounded one by one, never fused into an FMA, so the
+// results are reproducible bit for bit.
+#pragma clang fp contract(off)
+
+namespace costa {
+namespace {
+
+constexpr int kThreads = 256;
+
+// Workgroup b of n (dispatched round-robin over the 8 XCDs) gets the b-th
+// slot of a contiguous range per XCD, so consecutive groups share an L2.
+__device__ __forceinline__ int32_t xcd_remap(int32_t b, int32_t n) {
+  constexpr int32_t X = 8;
+  const int32_t q = n / X, r = n % X;
+  const int32_t xcd = b % X, idx = b / X;
+  const int32_t start = xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q;
+  return start + idx;
+}
+
+template <typename S, int N>
+struct alignas(sizeof(S) * N) Vec {
+  S v[N];
+};
+
+// Element arithmetic for a vector of NU scalars (pairs of them for complex).
+template <typename S, int NU, bool CPLX, int MODE, bool CONJ>
+__device__ __forceinline__ Vec<S, NU> combine(const Vec<S, NU>& b, const Vec<S, NU>& a, S ar, S ai, S br, S bi) {
+  Vec<S, NU> o;
+  if constexpr (CPLX) {
+#pragma unroll
+    for (int k = 0; k < NU; k += 2) {
+      const S xr = b.v[k];
+      const S xi = CONJ ? -b.v[k + 1] : b.v[k + 1];
+      if constexpr (MODE == MODE_COPY) {
+        o.v[k] = xr;
+        o.v[k + 1] = xi;
+      } else {
+        const S p1 = ar * xr, p2 = ai * xi, p3 = ar * xi, p4 = ai * xr;
+        S t1r = p1 - p2, t1i = p3 + p4;
+        if constexpr (MODE == MODE_AXPBY) {
+          const S q1 = br * a.v[k], q2 = bi * a.v[k + 1], q3 = br * a.v[k + 1], q4 = bi * a.v[k];
+          const S t2r = q1 - q2, t2i = q3 + q4;
+          t1r = t1r + t2r;
+          t1i = t1i + t2i;
+        }
+        o.v[k] = t1r;
+        o.v[k + 1] = t1i;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      if constexpr (MODE == MODE_COPY) {
+        o.v[k] = b.v[k];
+      } else if constexpr (MODE == MODE_SCALE) {
+        o.v[k] = ar * b.v[k];
+      } else {
+        const S t1 = ar * b.v[k];
+        const S t2 = br * a.v[k];
+        o.v[k] = t1 + t2;
+      }
+    }
+  }
+  return o;
+}
+
+// Rectangle whose source and destination both run along x:
+// dst[y*dst_ld + x] = f(src[y*src_ld + x]).  Units of NU scalars (one element,
+// or several when the rectangle is 16-byte aligned); lanes walk the flattened
+// (y, x) index so short rows still fill a wavefront.
+template <typename S, int NU, int NEL, bool CPLX, int MODE, bool CONJ, int UNROLL>
+__device__ __forceinline__ void move_rows(const S* __restrict__ src, S* __restrict__ dst, const Piece& p, S ar,
+                                          S ai, S br, S bi) {
+  using U = Vec<S, NU>;
+  const U* __restrict__ su = reinterpret_cast<const U*>(src) + p.src_off / NEL;
+  U* __restrict__ du = reinterpret_cast<U*>(dst) + p.dst_off / NEL;
+  const int64_t sld = p.src_ld / NEL, dld = p.dst_ld / NEL;
+  const int32_t nxu = p.nx / NEL;
+  const int32_t n = nxu * p.ny;
+  const float inv = p.inv_nx;
+  const int32_t tid = threadIdx.x;
+  for (int32_t base = 0; base < n; base += kThreads * UNROLL) {
+    U bv[UNROLL], av[UNROLL];
+    int64_t doff[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const int32_t e = base + u * kThreads + tid;
+      doff[u] = -1;
+      if (e < n) {
+        int32_t y = (int32_t)((float)e * inv);
+        int32_t x = e - y * nxu;
+        if (x < 0) {
+          --y;
+          x += nxu;
+        } else if (x >= nxu) {
+          ++y;
+          x -= nxu;
+        }
+        bv[u] = su[y * sld + x];
+        doff[u] = y * dld + x;
+        if constexpr (MODE == MODE_AXPBY) av[u] = du[doff[u]];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+      if (doff[u] >= 0) du[doff[u]] = combine<S, NU, CPLX, MODE, CONJ>(bv[u], av[u], ar, ai, br, bi);
+  }
+}
+
+// Rectangle whose source runs along y while the destination runs along x:
+// staged through an LDS tile of TS x TS elements (one padding column against
+// bank conflicts).  Loads are coalesced along the source, stores along the
+// destination.
+template <typename S, bool CPLX, int MODE, bool CONJ, int TS>
+__device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __restrict__ dst, const Piece& p,
+                                                Vec<S, CPLX ? 2 : 1> (*tile)[TS + 1], S ar, S ai, S br, S bi) {
+  constexpr int NS = CPLX ? 2 : 1;
+  using E = Vec<S, NS>;
+  constexpr int ROWS = kThreads / TS;  // tile rows per pass
+  const E* __restrict__ se = reinterpret_cast<const E*>(src) + p.src_off;
+  E* __restrict__ de = reinterpret_cast<E*>(dst) + p.dst_off;
+  const int32_t tid = threadIdx.x;
+  const int32_t lane = tid % TS, row = tid / TS;
+  for (int32_t ty = 0; ty < p.ny; ty += TS) {
+    for (int32_t tx = 0; tx < p.nx; tx += TS) {
+      // load: source contiguous along y
+      const int32_t y = ty + lane;
+#pragma unroll
+      for (int k = 0; k < TS / ROWS; ++k) {
+        const int32_t lx = row + k * ROWS;
+        const int32_t x = tx + lx;
+        if (x < p.nx && y < p.ny) tile[lx][lane] = se[(int64_t)x * p.src_ld + y];
+      }
+      __syncthreads();
+      // store: destination contiguous along x
+      const int32_t x = tx + lane;
+#pragma unroll
+      for (int k = 0; k < TS / ROWS; ++k) {
+        const int32_t ly = row + k * ROWS;
+        const int32_t yy = ty + ly;
+        if (x < p.nx && yy < p.ny) {
+          const int64_t o = (int64_t)yy * p.dst_ld + x;
+          E a;
+          if constexpr (MODE == MODE_AXPBY) a = de[o];
+          de[o] = combine<S, NS, CPLX, MODE, CONJ>(tile[lane][ly], a, ar, ai, br, bi);
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+template <typename S, bool CPLX>
+struct TypeTraits {
+  static constexpr int NS = CPLX ? 2 : 1;                      // scalars per element
+  static constexpr int ES = (int)sizeof(S) * NS;               // bytes per element
+  static constexpr int WIDE_NEL = ES >= 16 ? 1 : 16 / ES;      // elements per 16-byte unit
+  static constexpr int TS = ES >= 16 ? 32 : 64;                // transpose tile
+  static constexpr int UNROLL_NARROW = ES >= 16 ? 4 : 8;
+};
+
+template <typename S, bool CPLX, int MODE, bool CONJ>
+__device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p, bool wide,
+                                           Vec<S, CPLX ? 2 : 1> (*tile)[TypeTraits<S, CPLX>::TS + 1], S ar, S ai,
+                                           S br, S bi) {
+  using TT = TypeTraits<S, CPLX>;
+  if (p.flags & PIECE_TRANSPOSE) {
+    move_transposed<S, CPLX, MODE, CONJ, TT::TS>(src, dst, p, tile, ar, ai, br, bi);
+  } else if (wide && TT::WIDE_NEL > 1) {
+    move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, 4>(src, dst, p, ar, ai, br, bi);
+  } else {
+    move_rows<S, TT::NS, 1, CPLX, MODE, CONJ, TT::UNROLL_NARROW>(src, dst, p, ar, ai, br, bi);
+  }
+}
+
+// KIND: 0 pack (bitwise copy, never transposed), 1 unpack-transform, 2 direct.
+template <typename S, bool CPLX, int KIND>
+__global__ void __launch_bounds__(kThreads) costa_mover(const Piece* __restrict__ pieces,
+                                                        const int32_t* __restrict__ groups, int32_t ngroups,
+                                                        void* const* __restrict__ bufs,
+                                                        const ItemParam* __restrict__ items, int32_t allow_wide) {
+  using TT = TypeTraits<S, CPLX>;
+  using E = Vec<S, TT::NS>;
+  const int32_t g = xcd_remap((int32_t)blockIdx.x, ngroups);
+  const int32_t p0 = groups[g], p1 = groups[g + 1];
+  if constexpr (KIND == KIND_PACK) {
+    for (int32_t pi = p0; pi < p1; ++pi) {
+      const Piece p = pieces[pi];
+      const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
+      S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
+      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
+      if (wide && TT::WIDE_NEL > 1)
+        move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE_COPY, false, 4>(src, dst, p, S(0), S(0), S(0),
+                                                                                      S(0));
+      else
+        move_rows<S, TT::NS, 1, CPLX, MODE_COPY, false, TT::UNROLL_NARROW>(src, dst, p, S(0), S(0), S(0), S(0));
+    }
+  } else {
+    __shared__ E tile[TT::TS][TT::TS + 1];
+    for (int32_t pi = p0; pi < p1; ++pi) {
+      const Piece p = pieces[pi];
+      const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
+      S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
+      const ItemParam ip = items[p.item];
+      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
+      const S ar = (S)ip.alpha[0], ai = (S)ip.alpha[1], br = (S)ip.beta[0], bi = (S)ip.beta[1];
+      const bool conj = CPLX && ip.conj;
+      switch (ip.mode) {
+        case MODE_COPY:
+          if (conj) move_piece<S, CPLX, MODE_COPY, true>(src, dst, p, wide, tile, ar, ai, br, bi);
+          else move_piece<S, CPLX, MODE_COPY, false>(src, dst, p, wide, tile, ar, ai, br, bi);
+          break;
+        case MODE_SCALE:
+          if (conj) move_piece<S, CPLX, MODE_SCALE, true>(src, dst, p, wide, tile, ar, ai, br, bi);
+          else move_piece<S, CPLX, MODE_SCALE, false>(src, dst, p, wide, tile, ar, ai, br, bi);
+          break;
+        default:
+          if (conj) move_piece<S, CPLX, MODE_AXPBY, true>(src, dst, p, wide, tile, ar, ai, br, bi);
+          else move_piece<S, CPLX, MODE_AXPBY, false>(src, dst, p, wide, tile, ar, ai, br, bi);
+          break;
+      }
+    }
+  }
+}
+
+// Volume of the grid overlay: every overlay block (k, l) adds its element
+// count to V[s][t] (s: owner of its cover in L(B), t: owner of its cover in
+// L(A)).  Histogram in LDS when P*P fits, flushed with 64-bit atomics.
+__global__ void __launch_bounds__(kThreads) costa_volume(VolumeArgs a, int32_t use_lds) {
+  extern __shared__ unsigned long long hist[];
+  const int32_t PP = a.P * a.P;
+  if (use_lds) {
+    for (int32_t i = threadIdx.x; i < PP; i += kThreads) hist[i] = 0ull;
+    __syncthreads();
+  }
+  const int64_t total = (int64_t)a.K * a.L;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total; idx += stride) {
+    const int32_t k = (int32_t)(idx / a.L), l = (int32_t)(idx % a.L);
+    const Interval ri = a.rows[k], ci = a.cols[l];
+    const int32_t t = a.ownerA[(int64_t)ri.a * a.nbcA + ci.a];
+    const int32_t bi = a.transposed ? ci.b : ri.b, bj = a.transposed ? ri.b : ci.b;
+    const int32_t s = a.ownerB[(int64_t)bi * a.nbcB + bj];
+    const unsigned long long vol = (unsigned long long)(ri.len * ci.len);
+    if (use_lds) atomicAdd(&hist[s * a.P + t], vol);
+    else atomicAdd(&a.V[(int64_t)s * a.P + t], vol);
+  }
+  if (use_lds) {
+    __syncthreads();
+    for (int32_t i = threadIdx.x; i < PP; i += kThreads)
+      if (hist[i]) atomicAdd(&a.V[i], hist[i]);
+  }
+}
+
+template <typename S, bool CPLX>
+hipError_t launch_typed(MoverKind kind, const Piece* pieces, const int32_t* groups, int64_t ngroups,
+                        void* const* bufs, const ItemParam* items, int32_t allow_wide, hipStream_t stream) {
+  dim3 grid((unsigned)ngroups), block(kThreads);
+  const int32_t ng = (int32_t)ngroups;
+  switch (kind) {
+    case KIND_PACK:
+      hipLaunchKernelGGL((costa_mover<S, CPLX, KIND_PACK>), grid, block, 0, stream, pieces, groups, ng, bufs, items,
+                         allow_wide);
+      break;
+    case KIND_UNPACK:
+      hipLaunchKernelGGL((costa_mover<S, CPLX, KIND_UNPACK>), grid, block, 0, stream, pieces, groups, ng, bufs,
+                         items, allow_wide);
+      break;
+    default:
+      hipLaunchKernelGGL((costa_mover<S, CPLX, KIND_DIRECT>), grid, block, 0, stream, pieces, groups, ng, bufs,
+                         items, allow_wide);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const Piece* pieces, const int32_t* groups,
+                        int64_t ngroups, void* const* bufs, const ItemParam* items, int32_t allow_wide,
+                        hipStream_t stream) {
+  if (ngroups <= 0) return hipSuccess;
+  if (ngroups > INT32_MAX) return hipErrorInvalidValue;
+  switch (dtype) {
+    case COSTA_R64: return launch_typed<double, false>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
+    case COSTA_C128: return launch_typed<double, true>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
+    case COSTA_R32: return launch_typed<float, false>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
+    case COSTA_C64: return launch_typed<float, true>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_volume(const VolumeArgs& a, hipStream_t stream) {
+  const int64_t total = (int64_t)a.K * a.L;
+  if (total == 0) return hipSuccess;
+  int64_t blocks = (total + kThreads - 1) / kThreads;
+  if (blocks > 2048) blocks = 2048;
+  const size_t lds = (size_t)a.P * a.P * sizeof(unsigned long long);
+  const int32_t use_lds = lds <= 64 * 1024 ? 1 : 0;
+  hipLaunchKernelGGL(costa_volume, dim3((unsigned)blocks), dim3(kThreads), use_lds ? lds : 0, stream, a, use_lds);
+  return hipGetLastError();
+}
+
+}  // namespace costa

@@ -1,0 +1,333 @@
+// Planning of a transform (Section 5, Algorithm 2 and "Grid Overlay";
+// Section 6 "Implementation" and "Batched Transformation").
+//
+// Every block of the grid overlay of L(A) and L(op(B)) lies inside exactly one
+// block of each grid, so it has one sender s (owner in L(B)) and one receiver
+// label t (owner in L(A)), i.e. it belongs to package S_st.  Under the
+// relabeling sigma the label t lives on physical rank sigma[t]; the block is
+// local when s == sigma[t] and goes straight from B to A, otherwise it is
+// packed into the message of (s -> sigma[t]) and unpacked from there.
+//
+// Adjacent overlay blocks that are also adjacent in both the source and the
+// destination storage (for instance the blocks of one process row of a 1 x P
+// grid) are merged into one rectangle, large rectangles are split for load
+// balance, and runs of small rectangles are grouped per workgroup.
+#include <algorithm>
+#include <chrono>
+#include <numeric>
+
+#include "plan.hpp"
+
+namespace costa {
+
+std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<int64_t>& sb) {
+  // Both lists start at 0 and end at the same n.  The union of their points
+  // cuts [0, n) into intervals; each lies inside one interval of each list.
+  std::vector<Interval> out;
+  size_t na = sa.size() - 1, nb = sb.size() - 1;
+  if (na == 0 || nb == 0) return out;
+  out.reserve(na + nb);
+  size_t ia = 0, ib = 0;
+  int64_t pos = 0;
+  while (ia < na && ib < nb) {
+    int64_t end = std::min(sa[ia + 1], sb[ib + 1]);
+    out.push_back(Interval{pos, end - pos, (int32_t)ia, (int32_t)ib});
+    pos = end;
+    if (sa[ia + 1] == end) ++ia;
+    if (sb[ib + 1] == end) ++ib;
+  }
+  return out;
+}
+
+namespace {
+
+struct Cand {
+  Piece p;
+  int32_t kx0, kx1;  // x-interval range [kx0, kx1)
+  int32_t ly_end;    // y-interval index following the last strip merged
+  int32_t s, r;      // sender rank, receiving physical rank
+};
+
+inline bool same_kind(const Piece& a, const Piece& b) {
+  return a.src_buf == b.src_buf && a.dst_buf == b.dst_buf && a.flags == b.flags && a.src_ld == b.src_ld &&
+         a.dst_ld == b.dst_ld;
+}
+
+// All overlay rectangles of one pair, merged; appended to `local` / `remote`.
+void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vector<int32_t>& sigma,
+               std::vector<Cand>& local, std::vector<Cand>& remote, int64_t& overlay_blocks, int64_t& n_local,
+               int64_t& n_remote) {
+  const Layout& A = *d.A;
+  const Layout& B = *d.B;
+  const bool tr = d.op != COSTA_OP_N;
+  const int32_t P = A.nranks;
+  // op(B) seen in A's coordinates: its row splits are B's column splits for T/C
+  std::vector<Interval> rows = overlay(A.rsplit, tr ? B.csplit : B.rsplit);
+  std::vector<Interval> cols = overlay(A.csplit, tr ? B.rsplit : B.csplit);
+  const bool a_col = A.order == COSTA_COL_MAJOR;
+  const bool b_col = B.order == COSTA_COL_MAJOR;
+  // destination orientation: x along A's contiguous direction
+  const std::vector<Interval>& X = a_col ? rows : cols;
+  const std::vector<Interval>& Y = a_col ? cols : rows;
+  const int32_t KX = (int32_t)X.size(), LY = (int32_t)Y.size();
+  overlay_blocks += (int64_t)KX * LY;
+
+  std::vector<int32_t> open(KX, -1);  // candidate (index into `all`) that starts at kx0 and may grow along y
+  std::vector<Cand> all;
+  std::vector<Cand> strip;
+  for (int32_t ly = 0; ly < LY; ++ly) {
+    strip.clear();
+    const Interval& yi = Y[ly];
+    for (int32_t kx = 0; kx < KX; ++kx) {
+      const Interval& xi = X[kx];
+      const Interval& ri = a_col ? xi : yi;  // row interval of this overlay block
+      const Interval& ci = a_col ? yi : xi;  // column interval
+      // destination block and label
+      const int64_t ba = A.block(ri.a, ci.a);
+      const int32_t t = A.owner[ba];
+      const int32_t r = sigma.empty() ? t : sigma[t];
+      const int64_t pi = ri.start - A.rsplit[ri.a], pj = ci.start - A.csplit[ci.a];
+      const int64_t lda = A.bld[ba];
+      const int64_t dst_off = A.boff[ba] + (a_col ? pi + pj * lda : pi * lda + pj);
+      // source block: op(B) block (ri.b, ci.b) is B block (ci.b, ri.b) for T/C
+      const int32_t bi = tr ? ci.b : ri.b, bj = tr ? ri.b : ci.b;
+      const int64_t bb = B.block(bi, bj);
+      const int32_t s = B.owner[bb];
+      const int64_t ldb = B.bld[bb];
+      // B element of A's (i, j): B(i, j) for N, B(j, i) for T/C
+      const int64_t qrow = tr ? ci.start - B.rsplit[bi] : ri.start - B.rsplit[bi];
+      const int64_t qcol = tr ? ri.start - B.csplit[bj] : ci.start - B.csplit[bj];
+      const int64_t s_brow = b_col ? 1 : ldb, s_bcol = b_col ? ldb : 1;  // strides of B's row / col index
+      const int64_t src_off = B.boff[bb] + qrow * s_brow + qcol * s_bcol;
+      const int64_t s_i = tr ? s_bcol : s_brow;  // stride along A's row index i
+      const int64_t s_j = tr ? s_brow : s_bcol;  // stride along A's column index j
+      const int64_t sx = a_col ? s_i : s_j, sy = a_col ? s_j : s_i;
+
+      Cand c;
+      Piece& p = c.p;
+      p.dst_off = dst_off;
+      p.dst_ld = lda;
+      p.src_off = src_off;
+      p.nx = (int32_t)xi.len;
+      p.ny = (int32_t)yi.len;
+      if (sx == 1 || p.nx == 1) {
+        p.flags = 0;
+        p.src_ld = sy;
+      } else {
+        p.flags = PIECE_TRANSPOSE;  // sy == 1 here: one of the strides is always 1
+        p.src_ld = sx;
+      }
+      p.dst_buf = item * P + r;
+      p.src_buf = nitems * P + item * P + s;
+      p.item = item;
+      p.inv_nx = 0.f;
+      p.pad = 0;
+      c.kx0 = kx;
+      c.kx1 = kx + 1;
+      c.ly_end = ly + 1;
+      c.s = s;
+      c.r = r;
+      const int64_t ne = (int64_t)p.nx * p.ny;
+      if (s == r) n_local += ne;
+      else n_remote += ne;
+      // merge along x with the previous rectangle of this strip
+      if (!strip.empty()) {
+        Piece& q = strip.back().p;
+        const int64_t step = (q.flags & PIECE_TRANSPOSE) ? q.src_ld : 1;
+        if (same_kind(q, p) && q.ny == p.ny && p.dst_off == q.dst_off + q.nx &&
+            p.src_off == q.src_off + (int64_t)q.nx * step && (int64_t)q.nx + p.nx <= INT32_MAX) {
+          q.nx += p.nx;
+          strip.back().kx1 = kx + 1;
+          continue;
+        }
+      }
+      strip.push_back(c);
+    }
+    // merge along y with the rectangle of the previous strip with the same x range
+    for (Cand& c : strip) {
+      int32_t o = open[c.kx0];
+      if (o >= 0) {
+        Cand& q = all[o];
+        const int64_t step = (q.p.flags & PIECE_TRANSPOSE) ? 1 : q.p.src_ld;
+        if (q.ly_end == ly && q.kx1 == c.kx1 && same_kind(q.p, c.p) &&
+            c.p.dst_off == q.p.dst_off + (int64_t)q.p.ny * q.p.dst_ld &&
+            c.p.src_off == q.p.src_off + (int64_t)q.p.ny * step && (int64_t)q.p.ny + c.p.ny <= INT32_MAX) {
+          q.p.ny += c.p.ny;
+          q.ly_end = ly + 1;
+          continue;
+        }
+      }
+      open[c.kx0] = (int32_t)all.size();
+      all.push_back(c);
+    }
+  }
+  for (Cand& c : all) (c.s == c.r ? local : remote).push_back(c);
+}
+
+// Splits rectangles larger than max_elems (tile-aligned for transposes).
+void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
+  std::vector<Cand> out;
+  out.reserve(v.size());
+  const int32_t TS = 64;
+  for (const Cand& c : v) {
+    const Piece& p = c.p;
+    const bool T = p.flags & PIECE_TRANSPOSE;
+    if ((int64_t)p.nx * p.ny <= max_elems) {
+      out.push_back(c);
+      continue;
+    }
+    int64_t cx = std::min<int64_t>(p.nx, max_elems);
+    if (T && cx >= TS) cx -= cx % TS;
+    int64_t cy = std::max<int64_t>(1, max_elems / cx);
+    if (T && cy >= TS) cy -= cy % TS;
+    for (int64_t y0 = 0; y0 < p.ny; y0 += cy)
+      for (int64_t x0 = 0; x0 < p.nx; x0 += cx) {
+        Cand d = c;
+        d.p.nx = (int32_t)std::min<int64_t>(cx, p.nx - x0);
+        d.p.ny = (int32_t)std::min<int64_t>(cy, p.ny - y0);
+        d.p.dst_off = p.dst_off + y0 * p.dst_ld + x0;
+        d.p.src_off = p.src_off + (T ? x0 * p.src_ld + y0 : y0 * p.src_ld + x0);
+        out.push_back(d);
+      }
+  }
+  v.swap(out);
+}
+
+// Marks rectangles whose non-transposed walk can use 16-byte vectors and sets
+// the reciprocal of the row length in the units the kernel walks.
+void finish_piece(Piece& p, int elem_size) {
+  p.flags &= ~PIECE_WIDE;
+  int64_t v = 1;
+  if (!(p.flags & PIECE_TRANSPOSE)) {
+    int64_t want = elem_size >= 16 ? 1 : 16 / elem_size;
+    if (want > 1 && p.nx % want == 0 && p.src_off % want == 0 && p.dst_off % want == 0 &&
+        (p.ny == 1 || (p.src_ld % want == 0 && p.dst_ld % want == 0))) {
+      p.flags |= PIECE_WIDE;
+      v = want;
+    }
+  }
+  p.inv_nx = 1.0f / (float)(p.nx / v);
+}
+
+// Appends one launch: groups of consecutive rectangles.
+LaunchRange add_launch(HostPlan& hp, const std::vector<Piece>& ps, const PlanConfig& cfg, int32_t nitems) {
+  LaunchRange lr;
+  lr.item_elems.assign(nitems, 0);
+  lr.group_begin = (int64_t)hp.groups.size();
+  const int32_t base = (int32_t)hp.pieces.size();
+  int64_t acc = 0;
+  int32_t cnt = 0;
+  for (size_t k = 0; k < ps.size(); ++k) {
+    if (cnt == 0) hp.groups.push_back(base + (int32_t)k);
+    acc += (int64_t)ps[k].nx * ps[k].ny;
+    lr.elems += (int64_t)ps[k].nx * ps[k].ny;
+    lr.item_elems[ps[k].item] += (int64_t)ps[k].nx * ps[k].ny;
+    ++cnt;
+    if (acc >= cfg.min_group_elems || cnt >= cfg.max_group_pieces) {
+      acc = 0;
+      cnt = 0;
+    }
+  }
+  lr.ngroups = (int64_t)hp.groups.size() - lr.group_begin;
+  hp.groups.push_back(base + (int32_t)ps.size());  // end sentinel
+  hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
+  return lr;
+}
+
+bool by_dst(const Piece& a, const Piece& b) {
+  if (a.dst_buf != b.dst_buf) return a.dst_buf < b.dst_buf;
+  return a.dst_off < b.dst_off;
+}
+
+}  // namespace
+
+void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& sigma, const PlanConfig& cfg,
+                const std::function<int64_t(int64_t)>& choose_cap, HostPlan& hp) {
+  auto t0 = std::chrono::steady_clock::now();
+  const int32_t n = (int32_t)items.size();
+  const int es = cfg.elem_size;
+  hp = HostPlan();
+  hp.item_total.assign(n, 0);
+  hp.item_local.assign(n, 0);
+  hp.item_remote.assign(n, 0);
+  std::vector<Cand> local, remote;
+  for (int32_t k = 0; k < n; ++k) {
+    hp.item_total[k] = items[k].A->nrows * items[k].A->ncols;
+    plan_pair(k, n, items[k], sigma, local, remote, hp.overlay_blocks, hp.item_local[k], hp.item_remote[k]);
+  }
+  split_pieces(local, cfg.max_piece_elems);
+  split_pieces(remote, cfg.max_piece_elems);
+
+  // direct path, in destination order
+  std::vector<Piece> direct;
+  direct.reserve(local.size());
+  for (Cand& c : local) {
+    finish_piece(c.p, es);
+    direct.push_back(c.p);
+  }
+  std::sort(direct.begin(), direct.end(), by_dst);
+  hp.pieces_direct = (int32_t)direct.size();
+  hp.direct = add_launch(hp, direct, cfg, n);
+
+  // messages: packages ordered by sender, then receiver (each sender's send
+  // buffer holds one contiguous package per receiver); blocks in source order
+  std::sort(remote.begin(), remote.end(), [](const Cand& a, const Cand& b) {
+    if (a.s != b.s) return a.s < b.s;
+    if (a.r != b.r) return a.r < b.r;
+    if (a.p.src_buf != b.p.src_buf) return a.p.src_buf < b.p.src_buf;
+    return a.p.src_off < b.p.src_off;
+  });
+  auto chunk_bytes = [&](const Piece& p) {
+    int64_t b = (int64_t)p.nx * p.ny * es;
+    return (b + 255) / 256 * 256;  // every message block starts 256-byte aligned
+  };
+  int64_t total_msg = 0;
+  for (const Cand& c : remote) total_msg += chunk_bytes(c.p);
+  int64_t cap = choose_cap ? choose_cap(total_msg) : cfg.workspace_cap;
+  int64_t biggest = 0;
+  for (const Cand& c : remote) biggest = std::max(biggest, chunk_bytes(c.p));
+  cap = std::max(cap, biggest);
+
+  const int32_t msg_buf = 2 * n * (items.empty() ? 0 : items[0].A->nranks);
+  size_t k = 0;
+  while (k < remote.size()) {
+    std::vector<Piece> pack, unpack;
+    int64_t off = 0;
+    while (k < remote.size() && (off == 0 || off + chunk_bytes(remote[k].p) <= cap)) {
+      const Piece& q = remote[k].p;
+      const bool T = q.flags & PIECE_TRANSPOSE;
+      // pack: B -> message, always in the source's orientation (a plain copy)
+      Piece pk = q;
+      pk.flags = 0;
+      pk.nx = T ? q.ny : q.nx;
+      pk.ny = T ? q.nx : q.ny;
+      pk.src_ld = q.src_ld;
+      pk.dst_buf = msg_buf;
+      pk.dst_off = off / es;
+      pk.dst_ld = pk.nx;
+      finish_piece(pk, es);
+      pack.push_back(pk);
+      // unpack-transform: message -> A
+      Piece up = q;
+      up.src_buf = msg_buf;
+      up.src_off = off / es;
+      up.src_ld = T ? q.ny : q.nx;
+      finish_piece(up, es);
+      unpack.push_back(up);
+      off += chunk_bytes(q);
+      ++k;
+    }
+    std::sort(unpack.begin(), unpack.end(), by_dst);
+    Wave w;
+    w.msg_bytes = off;
+    hp.pieces_pack += (int32_t)pack.size();
+    hp.pieces_unpack += (int32_t)unpack.size();
+    w.pack = add_launch(hp, pack, cfg, n);
+    w.unpack = add_launch(hp, unpack, cfg, n);
+    hp.workspace_bytes = std::max(hp.workspace_bytes, off);
+    hp.waves.push_back(w);
+  }
+  hp.plan_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+}
+
+}  // namespace costa

@@ -1,0 +1,280 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bit-exact everywhere: the volume matrix and the relabeling (integers), pure
+reshuffles and transposes, and the scaled cases too, since both sides round
+every product and sum on its own (no FMA contraction).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2106_06601_amd as C
+    from parity import Case
+
+BC, GEN = synth.BlockCyclic, synth.General
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# volume matrix and relabeling on device volumes
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", synth.WORKLOADS)
+def test_volume_matrix_small_matches_oracle(name):
+    w = synth.workload(name, "small")
+    _say(f"volume {name} small")
+    for it in w.items:
+        A, B = C.layout_from_spec(it.A), C.layout_from_spec(it.B)
+        V = C.costa_volume_matrix(A, B, it.op)
+        assert np.array_equal(V, oracle.volume(oracle.OLayout(it.A), oracle.OLayout(it.B), it.op))
+
+
+def test_volume_matrix_full_size_closed_forms():
+    _say("volume full sizes")
+    w = synth.workload("reshuffle_transpose_1k")
+    it = w.items[0]
+    V = C.costa_volume_matrix(C.layout_from_spec(it.A), C.layout_from_spec(it.B), it.op)
+    assert np.array_equal(V, oracle.volume(oracle.OLayout(it.A), oracle.OLayout(it.B), it.op))
+    assert C.costa_relabel(V)[0] == oracle.relabel_bruteforce(V)
+    # 16384^2 block-size change: 64 non-zero pairs of 4,194,304; canonical sigma
+    it = synth.workload("blocksize_change_16k").items[0]
+    V = C.costa_volume_matrix(C.layout_from_spec(it.A), C.layout_from_spec(it.B), it.op)
+    assert (V == 4194304).sum() == 64 and V.sum() == 16384 * 16384
+    assert C.costa_relabel(V)[0] == oracle.relabel_dp(V) == [0, 2, 1, 3, 8, 10, 9, 11, 4, 6, 5, 7, 12, 14, 13, 15]
+    # 20000^2 scaled transpose: identity keeps 12,500,384 local
+    it = synth.workload("scaled_transpose_20k").items[0]
+    V = C.costa_volume_matrix(C.layout_from_spec(it.A), C.layout_from_spec(it.B), it.op)
+    assert V.sum() == 20000 * 20000 and np.trace(V) == 12500384
+    # tall-skinny pairs: V = 4,194,304 where the closed form says so
+    w = synth.workload("rpa_batched_tall_skinny")
+    tot = np.zeros((64, 64), np.int64)
+    for it in (w.items[0], w.items[4]):
+        V = C.costa_volume_matrix(C.layout_from_spec(it.A), C.layout_from_spec(it.B), it.op)
+        s, t = np.meshgrid(np.arange(64), np.arange(64), indexing="ij")
+        hit = (s // 8 == t % 8) if it.op == "N" else (s // 8 == t // 8)
+        assert np.array_equal(V, np.where(hit, 4194304, 0))
+        tot += 4 * V
+    assert oracle.retained(tot, list(range(64))) == 1207959552
+
+
+# ---------------------------------------------------------------------------
+# the five workloads
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", synth.WORKLOADS)
+def test_workload_small_full_compare(name):
+    w = synth.workload(name, "small")
+    _say(f"transform {name} small")
+    case = Case(w)
+    if w.relabel:
+        V = sum(oracle.volume(oracle.OLayout(it.A), oracle.OLayout(it.B), it.op) for it in w.items)
+        assert np.array_equal(case.V, V)
+        assert case.sigma == oracle.relabel(V)
+    case.run()
+    case.check_full()
+    case.run() if w.items[0].beta == 0 else None  # a second call reuses the cached plan
+    if w.items[0].beta == 0:
+        case.check_full()
+
+
+@pytest.mark.parametrize("name", ["reshuffle_transpose_1k", "blocksize_change_16k", "scaled_transpose_20k",
+                                  "cosma_complex_16k"])
+def test_workload_full_size_sampled(name):
+    w = synth.workload(name)
+    _say(f"transform {name} full size")
+    beta0 = all(it.beta == 0 for it in w.items)
+    case = Case(w, a_init="nan" if beta0 else "gen")
+    if w.relabel:
+        assert case.sigma == oracle.relabel(case.V)
+    case.run()
+    n = case.check_sampled()
+    assert n > 100000
+    if beta0:
+        case.check_all_written()
+    if name == "reshuffle_transpose_1k":
+        case.check_full()
+    case.free()
+
+
+def test_workload_rpa_full_size_sampled():
+    w = synth.workload("rpa_batched_tall_skinny")
+    need = sum(2 * it.A.nrows * it.A.ncols * 8 for it in w.items)
+    free, total = torch.cuda.mem_get_info()
+    if free < need + (4 << 30):
+        pytest.skip(f"needs {need / 2**30:.0f} GiB + workspace; {free / 2**30:.0f} GiB free")
+    _say("transform rpa_batched_tall_skinny full size")
+    case = Case(w)
+    case.run()
+    n = case.check_sampled(n_random=50000, n_corners=100000)
+    assert n > 100000
+    case.free()
+
+
+# ---------------------------------------------------------------------------
+# random layouts, every op / order / type / scalar combination
+# ---------------------------------------------------------------------------
+def _random_general(rng, M, N, P, order):
+    nr = int(rng.integers(1, min(M, 9) + 1))
+    nc = int(rng.integers(1, min(N, 9) + 1))
+    rs = [0] + sorted(rng.choice(np.arange(1, M), nr - 1, replace=False).tolist()) + [M] if nr > 1 else [0, M]
+    cs = [0] + sorted(rng.choice(np.arange(1, N), nc - 1, replace=False).tolist()) + [N] if nc > 1 else [0, N]
+    owners = rng.integers(0, P, (len(rs) - 1) * (len(cs) - 1)).tolist()
+    return GEN(M, N, rs, cs, owners, P, order)
+
+
+def _random_layout(rng, M, N, P, order):
+    if rng.random() < 0.5:
+        for pr in range(1, P + 1):
+            if P % pr == 0 and rng.random() < 0.5:
+                break
+        pr = pr if P % pr == 0 else 1
+        return BC(M, N, int(rng.integers(1, 40)), int(rng.integers(1, 40)), pr, P // pr,
+                  "row" if rng.random() < 0.5 else "col", order)
+    return _random_general(rng, M, N, P, order)
+
+
+SCALARS = [(1.0, 0.0), (2.0, 0.5), (-0.75, 1.25), (0.3, 0.0), (1.0, 1.0)]
+CSCALARS = [(1.0, 0.0), (0.5 - 0.25j, 0.25 + 1j), (1 + 0j, 1 + 0j), (0.3 + 0.7j, 0.0)]
+
+
+@pytest.mark.parametrize("dtype", ["f64", "c128", "f32", "c64"])
+def test_random_layouts_full_compare(dtype):
+    rng = np.random.default_rng({"f64": 1, "c128": 2, "f32": 3, "c64": 4}[dtype])
+    for case_no in range(24):
+        P = int(rng.integers(1, 9))
+        M, N = int(rng.integers(1, 300)), int(rng.integers(1, 300))
+        op = ["N", "T", "C"][case_no % 3]
+        oa = "col" if rng.random() < 0.5 else "row"
+        ob = "col" if rng.random() < 0.5 else "row"
+        A = _random_layout(rng, M, N, P, oa)
+        B = _random_layout(rng, M if op == "N" else N, N if op == "N" else M, P, ob)
+        sc = CSCALARS if dtype in ("c128", "c64") else SCALARS
+        alpha, beta = sc[case_no % len(sc)]
+        sigma = rng.permutation(P).tolist() if rng.random() < 0.5 else None
+        w = synth.Workload(f"random{case_no}", dtype, [synth.Item(A, B, op, alpha, beta)], False, seed=case_no + 7)
+        _say(f"random {dtype} case {case_no}: P={P} {M}x{N} op={op} A={A.kind}/{oa} B={B.kind}/{ob} "
+             f"alpha={alpha} beta={beta} sigma={sigma}")
+        case = Case(w, sigma=sigma)
+        case.run()
+        case.check_full()
+
+
+def test_random_batched_full_compare():
+    rng = np.random.default_rng(11)
+    for case_no in range(6):
+        P = int(rng.integers(1, 7))
+        items = []
+        for k in range(int(rng.integers(1, 5))):
+            M, N = int(rng.integers(1, 200)), int(rng.integers(1, 200))
+            op = ["N", "T"][int(rng.integers(0, 2))]
+            A = _random_layout(rng, M, N, P, "col" if rng.random() < 0.5 else "row")
+            B = _random_layout(rng, M if op == "N" else N, N if op == "N" else M, P,
+                               "col" if rng.random() < 0.5 else "row")
+            alpha, beta = SCALARS[int(rng.integers(0, len(SCALARS)))]
+            items.append(synth.Item(A, B, op, alpha, beta))
+        sigma = rng.permutation(P).tolist()
+        w = synth.Workload(f"batch{case_no}", "f64", items, False, seed=100 + case_no)
+        _say(f"batched case {case_no}: P={P} pairs={len(items)} sigma={sigma}")
+        case = Case(w, sigma=sigma)
+        case.run()
+        case.check_full()
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+def test_waves_with_tiny_workspace():
+    _say("waves with a 256 KiB workspace")
+    try:
+        C.costa_set_workspace_limit(256 << 10)
+        for name in ("blocksize_change_16k", "rpa_batched_tall_skinny", "cosma_complex_16k"):
+            w = synth.workload(name, "small")
+            descs = [dict(op=it.op, alpha=it.alpha, beta=it.beta, A=C.layout_from_spec(it.A),
+                          B=C.layout_from_spec(it.B)) for it in w.items]
+            assert C.costa_plan_stats(w.dtype, descs)["waves"] > 4
+            case = Case(w)
+            case.run()
+            case.check_full()
+    finally:
+        C.costa_set_workspace_limit(0)
+
+
+def test_degenerate_shapes():
+    cases = [
+        (GEN(1, 1, [0, 1], [0, 1], [0], 1, "col"), GEN(1, 1, [0, 1], [0, 1], [0], 1, "row"), "T"),
+        (BC(1, 257, 1, 16, 1, 3, "row", "row"), BC(257, 1, 5, 1, 3, 1, "col", "col"), "T"),
+        (BC(130, 1, 7, 1, 2, 1), BC(130, 1, 64, 1, 1, 2), "N"),
+        (BC(5, 7, 100, 100, 2, 2), BC(7, 5, 3, 3, 2, 2), "C"),  # some ranks own nothing
+    ]
+    for k, (A, B, op) in enumerate(cases):
+        for dtype in ("f64", "c128"):
+            _say(f"degenerate case {k} {dtype}")
+            w = synth.Workload(f"deg{k}", dtype, [synth.Item(A, B, op, 2.0, 0.5)], False, seed=k)
+            case = Case(w)
+            case.run()
+            case.check_full()
+
+
+def test_empty_matrix_is_a_no_op():
+    A = C.Layout.general(0, 5, [0], [0, 5], [], 2)
+    B = C.Layout.general(5, 0, [0, 5], [0], [], 2)
+    C.costa_transform("f64", "T", 1.0, 0.0, A, [0, 0], B, [0, 0])
+    torch.cuda.synchronize()
+
+
+def test_unaligned_buffers_take_the_narrow_path():
+    """Buffers offset by one element (8 bytes) are not 16-byte aligned."""
+    it = synth.workload("blocksize_change_16k", "small").items[0]
+    LA, LB = C.layout_from_spec(it.A), C.layout_from_spec(it.B)
+    OA, OB = oracle.OLayout(it.A), oracle.OLayout(it.B)
+    P = 16
+    dA = [torch.zeros(OA.local_elems(r) + 1, dtype=torch.float64, device="cuda") for r in range(P)]
+    dB = [torch.empty(OB.local_elems(s) + 1, dtype=torch.float64, device="cuda") for s in range(P)]
+    hB = []
+    for s in range(P):
+        h = np.zeros(OB.local_elems(s))
+        oracle.fill("f64", h, 5, synth.stream(synth.ROLE_B, 0, s))
+        dB[s][1:].copy_(torch.from_numpy(h))
+        hB.append(h)
+    C.costa_transform("f64", "N", 1.0, 0.0, LA, [t[1:] for t in dA], LB, [t[1:] for t in dB])
+    hA = [np.zeros(OA.local_elems(r)) for r in range(P)]
+    oracle.transform("f64", "N", 1.0, 0.0, OA, hA, OB, hB)
+    torch.cuda.synchronize()
+    for r in range(P):
+        assert np.array_equal(dA[r][1:].cpu().numpy(), hA[r])
+
+
+def test_two_streams_share_the_workspace_safely():
+    w = synth.workload("blocksize_change_16k", "small")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s1):
+        c1 = Case(w, sigma=None)
+    with torch.cuda.stream(s2):
+        c2 = Case(w, sigma=None)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        c1.run()
+    with torch.cuda.stream(s2):
+        c2.run()
+    torch.cuda.synchronize()
+    c1.check_full()
+    c2.check_full()
+
+
+def test_timing_counters():
+    w = synth.workload("blocksize_change_16k", "small")
+    case = Case(w)
+    C.costa_timing_enable(True)
+    for _ in range(3):
+        case.run()
+    t = C.costa_timing_read()
+    C.costa_timing_enable(False)
+    assert t["pack"]["launches"] == 3 and t["unpack"]["launches"] == 3 and t["direct"]["launches"] == 3
+    assert t["pack"]["ms"] > 0 and t["unpack"]["bytes"] > 0

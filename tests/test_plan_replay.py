@@ -1,0 +1,211 @@
+"""CPU replay of the library's plans: the rectangles the kernels will process
+are applied on host buffers with numpy, exactly as the kernels address them.
+
+This checks, without a GPU, that (1) every read and write of every kernel stays
+inside its buffer (the device buffers are sized by costa_layout_local_elems and
+the message workspace by the plan), (2) every element of A is written exactly
+once, (3) message blocks of one wave do not overlap, and (4) pack -> unpack and
+the direct path together reproduce the oracle bit for bit.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+C = pytest.importorskip("paper_2106_06601_amd")
+
+PACK, UNPACK, DIRECT = 0, 1, 2
+
+
+def _descs(w):
+    keep, descs = [], []
+    for it in w.items:
+        a, b = C.layout_from_spec(it.A), C.layout_from_spec(it.B)
+        keep += [a, b]
+        descs.append(dict(op=it.op, alpha=it.alpha, beta=it.beta, A=a, B=b))
+    return descs, keep
+
+
+def _index(p):
+    x = np.arange(p["nx"], dtype=np.int64)[None, :]
+    y = np.arange(p["ny"], dtype=np.int64)[:, None]
+    dst = p["dst_off"] + y * p["dst_ld"] + x
+    if p["flags"] & 1:
+        src = p["src_off"] + x * p["src_ld"] + y
+    else:
+        src = p["src_off"] + y * p["src_ld"] + x
+    return src.ravel(), dst.ravel()
+
+
+def _combine(dtype, b, a, alpha, beta, conj):
+    """alpha*b + beta*a with every product and sum rounded on its own."""
+    cplx = dtype in ("c128", "c64")
+    f = np.float64 if dtype in ("f64", "c128") else np.float32
+    if cplx and conj:
+        b = np.conj(b)  # sign flip of the imaginary part
+    if alpha == 1 and beta == 0:
+        return b
+    if not cplx:
+        t1 = f(alpha.real) * b
+        return t1 if beta == 0 else t1 + f(beta.real) * a
+    ar, ai = f(alpha.real), f(alpha.imag)
+    br_, bi_ = b.real, b.imag
+    t1r = ar * br_ - ai * bi_
+    t1i = ar * bi_ + ai * br_
+    if beta != 0:
+        er, ei = f(beta.real), f(beta.imag)
+        t1r = t1r + (er * a.real - ei * a.imag)
+        t1i = t1i + (er * a.imag + ei * a.real)
+    out = np.empty(b.shape, dtype=oracle.NUMPY[dtype])
+    out.real = t1r
+    out.imag = t1i
+    return out
+
+
+def replay(w, sigma=None, limit=None):
+    descs, keep = _descs(w)
+    if limit:
+        C.costa_set_workspace_limit(limit)
+    try:
+        pieces = C.costa_plan_export(w.dtype, descs, sigma)
+        stats = C.costa_plan_stats(w.dtype, descs, sigma)
+    finally:
+        if limit:
+            C.costa_set_workspace_limit(0)
+    n, P = len(w.items), w.items[0].A.nranks
+    es = synth.ITEMSIZE[w.dtype]
+    npt = oracle.NUMPY[w.dtype]
+    sg = list(range(P)) if sigma is None else list(sigma)
+    inv = [0] * P
+    for t, r in enumerate(sg):
+        inv[r] = t
+    bufs = [None] * (2 * n * P + 1)
+    hits = []
+    for k, it in enumerate(w.items):
+        OA, OB = oracle.OLayout(it.A), oracle.OLayout(it.B)
+        for r in range(P):
+            a = np.zeros(OA.local_elems(inv[r]), dtype=npt)
+            oracle.fill(w.dtype, a, w.seed, synth.stream(synth.ROLE_A, k, r))
+            bufs[k * P + r] = a
+            hits.append(np.zeros(a.size, np.int32))
+        for s in range(P):
+            b = np.zeros(OB.local_elems(s), dtype=npt)
+            oracle.fill(w.dtype, b, w.seed, synth.stream(synth.ROLE_B, k, s))
+            bufs[n * P + k * P + s] = b
+    msg_elems = stats["workspace_bytes"] // es
+    bufs[2 * n * P] = np.full(msg_elems, np.nan, dtype=npt)
+    # launch order as exported: DIRECT, then PACK/UNPACK per wave
+    cur_wave, msg_used = -1, None
+    for p in pieces:
+        if p["kind"] == PACK and p["wave"] != cur_wave:
+            cur_wave, msg_used = p["wave"], np.zeros(msg_elems, np.int8)
+        src, dst = _index(p)
+        sb, db = bufs[p["src_buf"]], bufs[p["dst_buf"]]
+        assert src.min() >= 0 and src.max() < sb.size, f"read out of bounds in {p}"
+        assert dst.min() >= 0 and dst.max() < db.size, f"write out of bounds in {p}"
+        if p["kind"] == PACK:
+            assert p["dst_buf"] == 2 * n * P and not (p["flags"] & 1)
+            assert not msg_used[dst].any(), "message blocks overlap"
+            msg_used[dst] = 1
+            db[dst] = sb[src]
+            continue
+        it = w.items[p["item"]]
+        alpha, beta = complex(it.alpha), complex(it.beta)
+        a_old = db[dst] if beta != 0 else None
+        db[dst] = _combine(w.dtype, sb[src], a_old, alpha, beta, it.op == "C")
+        hits[p["dst_buf"]][dst] += 1
+    # exactly once, and equal to the oracle
+    for k, it in enumerate(w.items):
+        OA, OB = oracle.OLayout(it.A), oracle.OLayout(it.B)
+        ha = []
+        for r in range(P):
+            a = np.zeros(OA.local_elems(inv[r]), dtype=npt)
+            oracle.fill(w.dtype, a, w.seed, synth.stream(synth.ROLE_A, k, r))
+            ha.append(a)
+        hb = [bufs[n * P + k * P + s] for s in range(P)]
+        oracle.transform(w.dtype, it.op, it.alpha, it.beta, OA, ha, OB, hb, sigma)
+        for r in range(P):
+            assert np.all(hits[k * P + r] == 1), "an element of A is not written exactly once"
+            u = np.uint64 if w.dtype in ("f64", "c128") else np.uint32
+            assert np.array_equal(bufs[k * P + r].view(u), ha[r].view(u)), f"pair {k} rank {r} differs"
+    return pieces, stats
+
+
+@pytest.mark.parametrize("name", synth.WORKLOADS)
+def test_replay_small_workloads(name):
+    w = synth.workload(name, "small")
+    sigma = None
+    if w.relabel:
+        V = sum(oracle.volume(oracle.OLayout(it.A), oracle.OLayout(it.B), it.op) for it in w.items)
+        sigma = oracle.relabel(V)
+    replay(w, sigma)
+
+
+def test_replay_with_waves_and_relabeling():
+    w = synth.workload("blocksize_change_16k", "small")
+    pieces, stats = replay(w, sigma=[3, 1, 0, 2, 5, 4, 7, 6, 9, 8, 11, 10, 15, 12, 14, 13], limit=200 << 10)
+    assert stats["waves"] > 10
+    w = synth.workload("cosma_complex_16k", "small")
+    replay(w, limit=1 << 20)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_replay_random_layouts(seed):
+    rng = np.random.default_rng(seed)
+    BC, GEN = synth.BlockCyclic, synth.General
+    P = int(rng.integers(1, 7))
+    M, N = int(rng.integers(1, 150)), int(rng.integers(1, 150))
+    op = ["N", "T", "C"][seed % 3]
+    dtype = ["f64", "c128", "f32", "c64"][seed % 4]
+
+    def lay(m, n, order):
+        if rng.random() < 0.5:
+            return BC(m, n, int(rng.integers(1, 20)), int(rng.integers(1, 20)), 1, P,
+                      "row" if rng.random() < 0.5 else "col", order)
+        nr, nc = int(rng.integers(1, min(m, 6) + 1)), int(rng.integers(1, min(n, 6) + 1))
+        rs = [0] + sorted(rng.choice(np.arange(1, m), nr - 1, replace=False).tolist()) + [m] if nr > 1 else [0, m]
+        cs = [0] + sorted(rng.choice(np.arange(1, n), nc - 1, replace=False).tolist()) + [n] if nc > 1 else [0, n]
+        return GEN(m, n, rs, cs, rng.integers(0, P, (len(rs) - 1) * (len(cs) - 1)).tolist(), P, order)
+
+    A = lay(M, N, "col" if rng.random() < 0.5 else "row")
+    B = lay(M if op == "N" else N, N if op == "N" else M, "col" if rng.random() < 0.5 else "row")
+    alpha, beta = [(1.0, 0.0), (2.0, 0.5), (0.5 - 0.25j, 0.25 + 1j)][seed % 3] if dtype in ("c128", "c64") \
+        else [(1.0, 0.0), (2.0, 0.5), (-1.5, 0.0)][seed % 3]
+    w = synth.Workload("r", dtype, [synth.Item(A, B, op, alpha, beta)], False, seed=seed)
+    replay(w, sigma=rng.permutation(P).tolist())
+
+
+@pytest.mark.parametrize("name", synth.WORKLOADS)
+def test_full_size_plans_stay_in_bounds(name):
+    """Every rectangle of the full-size plans against the buffer sizes
+    (vectorised over rectangles; no data)."""
+    w = synth.workload(name)
+    descs, keep = _descs(w)
+    P, n = w.items[0].A.nranks, len(w.items)
+    sigma = None
+    if name == "blocksize_change_16k":
+        sigma = [0, 2, 1, 3, 8, 10, 9, 11, 4, 6, 5, 7, 12, 14, 13, 15]
+    x = C.costa_plan_export(w.dtype, descs, sigma)
+    st = C.costa_plan_stats(w.dtype, descs, sigma)
+    es = synth.ITEMSIZE[w.dtype]
+    sg = sigma or list(range(P))
+    sizes = np.zeros(2 * n * P + 1, np.int64)
+    for k, it in enumerate(w.items):
+        for t in range(P):
+            sizes[k * P + sg[t]] = C.costa_layout_local_elems(descs[k]["A"].handle, t)
+            sizes[n * P + k * P + t] = C.costa_layout_local_elems(descs[k]["B"].handle, t)
+    sizes[2 * n * P] = st["workspace_bytes"] // es
+    T = (x["flags"] & 1) == 1
+    nx, ny = x["nx"].astype(np.int64), x["ny"].astype(np.int64)
+    src_end = np.where(T, x["src_off"] + (nx - 1) * x["src_ld"] + ny - 1,
+                       x["src_off"] + (ny - 1) * x["src_ld"] + nx - 1)
+    dst_end = x["dst_off"] + (ny - 1) * x["dst_ld"] + nx - 1
+    assert (x["src_off"] >= 0).all() and (x["dst_off"] >= 0).all()
+    assert (src_end < sizes[x["src_buf"]]).all()
+    assert (dst_end < sizes[x["dst_buf"]]).all()
+    assert (nx >= 1).all() and (ny >= 1).all() and (nx * ny <= 1 << 16).all()
+    # rows of a rectangle do not wrap into each other
+    assert ((ny == 1) | (x["dst_ld"] >= nx)).all()
+    written = (nx * ny)[x["kind"] != PACK].sum()
+    assert written == st["total_elems"]
