@@ -60,8 +60,7 @@ struct alignas(16) Piece {
   int32_t ny;
   int32_t item;     // pair of a batched call (selects alpha, beta, mode)
   int32_t flags;
-  float inv_nx;     // 1/nx (in the units the kernel walks: see PIECE_WIDE)
-  int32_t pad;
+  int32_t pad[2];
 };
 static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
 

@@ -91,7 +91,7 @@ __device__ __forceinline__ void move_rows(const S* __restrict__ src, S* __restri
   const int64_t sld = p.src_ld / NEL, dld = p.dst_ld / NEL;
   const int32_t nxu = p.nx / NEL;
   const int32_t n = nxu * p.ny;
-  const float inv = p.inv_nx;
+  const float inv = 1.0f / (float)nxu;
   const int32_t tid = threadIdx.x;
   for (int32_t base = 0; base < n; base += kThreads * UNROLL) {
     U bv[UNROLL], av[UNROLL];
@@ -101,12 +101,14 @@ __device__ __forceinline__ void move_rows(const S* __restrict__ src, S* __restri
       const int32_t e = base + u * kThreads + tid;
       doff[u] = -1;
       if (e < n) {
+        // y = e / nxu from a float estimate, corrected to the exact quotient
         int32_t y = (int32_t)((float)e * inv);
         int32_t x = e - y * nxu;
-        if (x < 0) {
+        while (x < 0) {
           --y;
           x += nxu;
-        } else if (x >= nxu) {
+        }
+        while (x >= nxu) {
           ++y;
           x -= nxu;
         }

@@ -120,8 +120,7 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
       p.dst_buf = item * P + r;
       p.src_buf = nitems * P + item * P + s;
       p.item = item;
-      p.inv_nx = 0.f;
-      p.pad = 0;
+      p.pad[0] = p.pad[1] = 0;
       c.kx0 = kx;
       c.kx1 = kx + 1;
       c.ly_end = ly + 1;
@@ -193,20 +192,15 @@ void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
   v.swap(out);
 }
 
-// Marks rectangles whose non-transposed walk can use 16-byte vectors and sets
-// the reciprocal of the row length in the units the kernel walks.
+// Marks rectangles whose non-transposed walk can use 16-byte vectors.
 void finish_piece(Piece& p, int elem_size) {
   p.flags &= ~PIECE_WIDE;
-  int64_t v = 1;
   if (!(p.flags & PIECE_TRANSPOSE)) {
     int64_t want = elem_size >= 16 ? 1 : 16 / elem_size;
     if (want > 1 && p.nx % want == 0 && p.src_off % want == 0 && p.dst_off % want == 0 &&
-        (p.ny == 1 || (p.src_ld % want == 0 && p.dst_ld % want == 0))) {
+        (p.ny == 1 || (p.src_ld % want == 0 && p.dst_ld % want == 0)))
       p.flags |= PIECE_WIDE;
-      v = want;
-    }
   }
-  p.inv_nx = 1.0f / (float)(p.nx / v);
 }
 
 // Appends one launch: groups of consecutive rectangles.
