@@ -1,0 +1,234 @@
+#!/usr/bin/env python3
+"""Throughput of costa_transform on one MI355X.
+
+One step = one costa_transform (or costa_transform_batched) call: the direct
+path, then pack and unpack-transform of every wave, over synthetic seeded
+inputs already resident in HBM.  The plan (grid overlay, volume kernel,
+relabeling, rectangles) is built before the timed region and cached.
+
+Metric: effective GB/s = model bytes per step / time per step, with model
+bytes = read B + read A (beta != 0) + write A + 2 x message bytes (each
+message element is written by the pack and read by the unpack).
+
+Prints one JSON line.  The default workload is the ScaLAPACK-style block-size
+change: fp64 16384 x 16384, 4x4 process grid, 128x128 -> 256x256 blocks,
+identity op, alpha = 1, beta = 0, relabeling on.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+METRIC = "effective GB/s of costa_transform (and % of HBM peak) per config, 1 MI355X"
+KINDS = ["pack", "unpack", "direct"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("paper_2106_06601_amd/csrc/kernels.hip", "paper_2106_06601_amd/csrc/internal.hpp"):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str, kernel: str, launches_per_step: float):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when it is missing or was taken from a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"counters_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        d = json.load(fh)
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def describe(w) -> dict:
+    def lay(s):
+        if s.kind == "block_cyclic":
+            return (f"block-cyclic {s.prow}x{s.pcol} grid, {s.mb}x{s.nb} blocks, {s.rank_order}-major ranks, "
+                    f"{s.block_order}-major storage")
+        return (f"general grid {len(s.row_splits) - 1}x{len(s.col_splits) - 1} blocks over {s.nranks} ranks, "
+                f"{s.block_order}-major storage")
+    it = w.items[0]
+    return {"workload": w.name, "description": w.description, "dtype": w.dtype, "pairs": len(w.items),
+            "A": f"{it.A.nrows}x{it.A.ncols}", "source": lay(it.B), "target": lay(it.A),
+            "ops": "".join(x.op for x in w.items), "alpha": str(it.alpha), "beta": str(it.beta),
+            "relabel": w.relabel, "P": it.A.nranks}
+
+
+def cpu_baseline(w, sigma, model_bytes_per_elem: float, target_s: float):
+    """The CPU oracle, single-threaded, on the first rows of A of pair 0."""
+    import numpy as np
+    import oracle
+    import synth
+    it = w.items[0]
+    OA, OB = oracle.OLayout(it.A), oracle.OLayout(it.B)
+    P = it.A.nranks
+    sg = sigma if sigma is not None else list(range(P))
+    inv = [0] * P
+    for t, r in enumerate(sg):
+        inv[r] = t
+    npt = oracle.NUMPY[w.dtype]
+    hb = []
+    for s in range(P):
+        b = np.empty(OB.local_elems(s), dtype=npt)
+        oracle.fill(w.dtype, b, w.seed, synth.stream(synth.ROLE_B, 0, s))
+        hb.append(b)
+    ha = []
+    for r in range(P):
+        a = np.empty(OA.local_elems(inv[r]), dtype=npt)
+        oracle.fill(w.dtype, a, w.seed, synth.stream(synth.ROLE_A, 0, r))
+        ha.append(a)
+    M, N = it.A.nrows, it.A.ncols
+    # bands of target rows, in order (wrapping around), until target_s has passed
+    band = max(1, min(M, (1 << 22) // max(1, N)))
+    elems, r0 = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        r1 = min(M, r0 + band)
+        oracle.transform(w.dtype, it.op, it.alpha, it.beta, OA, ha, OB, hb, sigma, r0, r1)
+        elems += (r1 - r0) * N
+        r0 = 0 if r1 == M else r1
+        dt = time.perf_counter() - t0
+        if dt >= target_s:
+            break
+    return {"value": round(elems * model_bytes_per_elem / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{elems} elements of A in pair 0 (bands of {band} target rows of {M}, in order, "
+                      f"{elems / (M * N):.2f} passes over the {M}x{N} matrix) in {dt:.1f} s; single-threaded; "
+                      f"same bytes-per-element model as the GPU figure",
+            "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="blocksize_change_16k")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the transform's virtual ranks all live in "
+              "one GPU's HBM and this build has no multi-GPU exchange", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2106_06601_amd as C
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = synth.workload(args.workload)
+    P = w.items[0].A.nranks
+    stream = torch.cuda.current_stream()
+    dev = torch.device("cuda:0")
+    td = {"f64": torch.float64, "c128": torch.complex128, "f32": torch.float32, "c64": torch.complex64}[w.dtype]
+    LA = [C.layout_from_spec(it.A) for it in w.items]
+    LB = [C.layout_from_spec(it.B) for it in w.items]
+
+    t_plan0 = time.perf_counter()
+    sigma = None
+    if w.relabel:
+        V = sum(C.costa_volume_matrix(a, b, it.op) for a, b, it in zip(LA, LB, w.items))
+        sigma, kept_id, kept_sigma = C.costa_relabel(V)
+    inv = list(range(P)) if sigma is None else [0] * P
+    if sigma is not None:
+        for t, r in enumerate(sigma):
+            inv[r] = t
+    A, B = [], []
+    for k, it in enumerate(w.items):
+        A.append([torch.empty(LA[k].local_elems(inv[r]), dtype=td, device=dev) for r in range(P)])
+        B.append([torch.empty(LB[k].local_elems(s), dtype=td, device=dev) for s in range(P)])
+        for s, t in enumerate(B[k]):
+            if t.numel():
+                synth.fill_device(w.dtype, t.data_ptr(), t.numel(), w.seed, synth.stream(synth.ROLE_B, k, s),
+                                  stream.cuda_stream)
+        for r, t in enumerate(A[k]):
+            if t.numel():
+                synth.fill_device(w.dtype, t.data_ptr(), t.numel(), w.seed, synth.stream(synth.ROLE_A, k, r),
+                                  stream.cuda_stream)
+    descs = [dict(op=it.op, alpha=it.alpha, beta=it.beta, A=LA[k], A_local=A[k], B=LB[k], B_local=B[k])
+             for k, it in enumerate(w.items)]
+    stats = C.costa_plan_stats(w.dtype, descs, sigma)
+
+    def step():
+        if len(descs) == 1:
+            d = descs[0]
+            C.costa_transform(w.dtype, d["op"], d["alpha"], d["beta"], d["A"], d["A_local"], d["B"], d["B_local"],
+                              sigma, stream)
+        else:
+            C.costa_transform_batched(w.dtype, descs, sigma, stream)
+
+    step()  # builds and uploads the plan
+    torch.cuda.synchronize()
+    plan_s = time.perf_counter() - t_plan0
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: per-launch HIP events (on the launch stream) plus one pair around all steps
+    C.costa_timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    kt = C.costa_timing_read()
+    C.costa_timing_enable(False)
+    gpu_ms = e0.elapsed_time(e1)
+    ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
+    value = stats["model_bytes"] / (ms_per_step * 1e-3) / 1e9
+
+    per_kernel = {}
+    for k in KINDS:
+        d = kt[k]
+        if d["launches"]:
+            per_kernel[k] = {"launches_per_step": d["launches"] / args.steps,
+                             "ms_per_launch": round(d["ms"] / d["launches"], 5),
+                             "bytes_per_launch": d["bytes"] // d["launches"],
+                             "GB_s": round(d["bytes"] / (d["ms"] * 1e-3) / 1e9, 1)}
+    dominant = max(per_kernel, key=lambda k: kt[k]["ms"])
+    dk = per_kernel[dominant]
+    achieved = dk["GB_s"]
+    traffic = load_traffic(w.name, dominant, dk["launches_per_step"])
+    roof = {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
+    cpu = None
+    if not args.no_cpu_baseline and len(w.items) == 1:
+        cpu = cpu_baseline(w, sigma, stats["model_bytes"] / stats["total_elems"], args.cpu_seconds)
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "config": describe(w),
+        "model_bytes_per_step": stats["model_bytes"],
+        "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
+        "waves": stats["waves"], "plan_s": round(plan_s, 3),
+        "kernels": per_kernel,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -15,7 +15,7 @@ from typing import List, Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libcosta_mi355x.so")
+LIB_PATH = os.environ.get("COSTA_LIB") or os.path.join(_HERE, "libcosta_mi355x.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "

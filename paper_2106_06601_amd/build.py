@@ -36,29 +36,35 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
+def build(verbose: bool = False, defines=(), out=None, build_dir=None, synth=True) -> str:
+    """defines: extra -D flags (tuning experiments); out: library path."""
+    lib = out or LIB
+    bdir = build_dir or BUILD_DIR
+    os.makedirs(bdir, exist_ok=True)
     objs = []
     jobs = []
     for src in SOURCES:
         path = os.path.join(CSRC, src)
-        obj = os.path.join(BUILD_DIR, src + ".o")
+        obj = os.path.join(bdir, src + ".o")
         objs.append(obj)
         lang = ["-x", "hip"]
-        jobs.append([HIPCC, f"--offload-arch={ARCH}", *COMMON, *lang, "-c", path, "-o", obj])
+        jobs.append([HIPCC, f"--offload-arch={ARCH}", *COMMON, *[f"-D{d}" for d in defines], *lang, "-c", path,
+                     "-o", obj])
     with ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         outs = list(ex.map(_run, jobs))
     if verbose:
         for o in outs:
             if o.strip():
                 print(o)
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+    if not synth:
+        return lib
     tmp = SYNTH_LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", *COMMON, "-shared", "-o", tmp, SYNTH_SRC])
     os.replace(tmp, SYNTH_LIB)
-    return LIB
+    return lib
 
 
 if __name__ == "__main__":

@@ -18,6 +18,7 @@ namespace {
 constexpr int64_t kMaxPieceElems = 1 << 16;
 constexpr int64_t kMinGroupElems = 1 << 14;
 constexpr int32_t kMaxGroupPieces = 64;
+constexpr int64_t kTargetGroups = 4096;
 
 int elem_size(costa_dtype d) {
   switch (d) {
@@ -118,6 +119,7 @@ PlanConfig make_config(int es) {
   c.max_piece_elems = kMaxPieceElems;
   c.min_group_elems = kMinGroupElems;
   c.max_group_pieces = kMaxGroupPieces;
+  c.target_groups = kTargetGroups;
   return c;
 }
 
@@ -227,8 +229,8 @@ costa_status collect_timing(State& S) {
 
 // Launches one mover range, bracketed by timing events when enabled.
 costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePlan& dp, const LaunchRange& lr,
-                       void* const* d_bufs, const ItemParam* d_items, int32_t allow_wide, int64_t bytes,
-                       hipStream_t stream) {
+                       int32_t mode, int32_t conj, void* const* d_bufs, const ItemParam* d_items, int32_t allow_wide,
+                       int64_t bytes, hipStream_t stream) {
   if (lr.ngroups == 0) return COSTA_SUCCESS;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (S.timing) {
@@ -241,7 +243,8 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePla
     if (!e0 || !e1) return fail(COSTA_ERROR_DEVICE, "hipEventCreate failed");
     HIP_OR_FAIL(hipEventRecord(e0, stream));
   }
-  HIP_OR_FAIL(launch_mover(kind, dt, dp.d_pieces, dp.d_groups + lr.group_begin, lr.ngroups, d_bufs, d_items,
+  LaunchSpec spec{mode, conj, lr.has_transpose};
+  HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_groups + lr.group_begin, lr.ngroups, d_bufs, d_items,
                            allow_wide, stream));
   if (S.timing) {
     HIP_OR_FAIL(hipEventRecord(e1, stream));
@@ -399,15 +402,20 @@ costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_des
   void* const* d_bufs = reinterpret_cast<void* const*>(dp->d_table);
   const ItemParam* d_items = reinterpret_cast<const ItemParam*>((unsigned char*)dp->d_table + ptr_bytes);
   const int32_t wide = aligned ? 1 : 0;
-  st = run_range(S, KIND_DIRECT, dt, *dp, hp.direct, d_bufs, d_items, wide, range_bytes(hp.direct, es, reads_a),
-                 stream);
+  // one arithmetic mode for the whole call when every pair agrees
+  int32_t mode = ipar[0].mode, conj = ipar[0].conj;
+  for (int32_t k = 1; k < n; ++k)
+    if (ipar[k].mode != mode || ipar[k].conj != conj) mode = -1;
+  st = run_range(S, KIND_DIRECT, dt, *dp, hp.direct, mode, conj, d_bufs, d_items, wide,
+                 range_bytes(hp.direct, es, reads_a), stream);
   if (st != COSTA_SUCCESS) return st;
   std::vector<char> no_read(n, 0);
   for (const Wave& w : hp.waves) {
-    st = run_range(S, KIND_PACK, dt, *dp, w.pack, d_bufs, d_items, wide, range_bytes(w.pack, es, no_read), stream);
+    st = run_range(S, KIND_PACK, dt, *dp, w.pack, MODE_COPY, 0, d_bufs, d_items, wide,
+                   range_bytes(w.pack, es, no_read), stream);
     if (st != COSTA_SUCCESS) return st;
-    st = run_range(S, KIND_UNPACK, dt, *dp, w.unpack, d_bufs, d_items, wide, range_bytes(w.unpack, es, reads_a),
-                   stream);
+    st = run_range(S, KIND_UNPACK, dt, *dp, w.unpack, mode, conj, d_bufs, d_items, wide,
+                   range_bytes(w.unpack, es, reads_a), stream);
     if (st != COSTA_SUCCESS) return st;
   }
   if (ws->last_use) {

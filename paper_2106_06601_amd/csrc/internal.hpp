@@ -80,6 +80,7 @@ struct LaunchRange {
   int64_t group_begin = 0;  // index into Plan::groups (each group: [groups[g], groups[g+1]) of pieces)
   int64_t ngroups = 0;
   int64_t elems = 0;
+  bool has_transpose = false;
   std::vector<int64_t> item_elems;  // elements of each pair in this launch
 };
 
@@ -90,9 +91,17 @@ struct Wave {
 
 // ---- kernels (kernels.hip) -------------------------------------------------
 enum MoverKind : int32_t { KIND_PACK = 0, KIND_UNPACK = 1, KIND_DIRECT = 2 };
-hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const Piece* pieces, const int32_t* groups,
-                        int64_t ngroups, void* const* bufs, const ItemParam* items, int32_t allow_wide,
-                        hipStream_t stream);
+// What one launch needs: the pairs' common arithmetic mode and conjugation
+// (mode -1: the pairs differ, read per rectangle) and whether any rectangle
+// of the launch is transposed.
+struct LaunchSpec {
+  int32_t mode;
+  int32_t conj;
+  bool has_transpose;
+};
+hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
+                        const int32_t* groups, int64_t ngroups, void* const* bufs, const ItemParam* items,
+                        int32_t allow_wide, hipStream_t stream);
 
 struct VolumeArgs {
   const Interval* rows;

@@ -36,6 +36,63 @@ struct alignas(sizeof(S) * N) Vec {
   S v[N];
 };
 
+// Raw integer vector of a given size, for loads and stores with an optional
+// non-temporal hint (streaming data that is touched exactly once).
+template <int BYTES>
+struct Raw;
+template <>
+struct Raw<4> {
+  using T = uint32_t;
+};
+template <>
+struct Raw<8> {
+  typedef uint32_t T __attribute__((ext_vector_type(2)));
+};
+template <>
+struct Raw<16> {
+  typedef uint32_t T __attribute__((ext_vector_type(4)));
+};
+
+#ifndef COSTA_TILE_X8
+#define COSTA_TILE_X8 32
+#endif
+#ifndef COSTA_NT_LOADS
+#define COSTA_NT_LOADS 0
+#endif
+#ifndef COSTA_NT_STORES
+#define COSTA_NT_STORES 1
+#endif
+#ifndef COSTA_NT_ALOADS
+#define COSTA_NT_ALOADS 0
+#endif
+
+// The buffers reach the kernels through a pointer table, so the compiler
+// cannot see that they are global memory; the casts below make it emit global
+// (not flat) loads and stores, which do not share a wait counter with LDS.
+#define COSTA_GLOBAL __attribute__((address_space(1)))
+
+template <bool NT = COSTA_NT_LOADS, typename U>
+__device__ __forceinline__ U load(const U* p) {
+  using R = typename Raw<sizeof(U)>::T;
+  const COSTA_GLOBAL R* g = (const COSTA_GLOBAL R*)(p);
+  R r;
+  if constexpr (NT) r = __builtin_nontemporal_load(g);
+  else r = *g;
+  U u;
+  __builtin_memcpy(&u, &r, sizeof(U));
+  return u;
+}
+
+template <typename U>
+__device__ __forceinline__ void store(U* p, const U& u) {
+  using R = typename Raw<sizeof(U)>::T;
+  COSTA_GLOBAL R* g = (COSTA_GLOBAL R*)(p);
+  R r;
+  __builtin_memcpy(&r, &u, sizeof(U));
+  if constexpr (COSTA_NT_STORES) __builtin_nontemporal_store(r, g);
+  else *g = r;
+}
+
 // Element arithmetic for a vector of NU scalars (pairs of them for complex).
 template <typename S, int NU, bool CPLX, int MODE, bool CONJ>
 __device__ __forceinline__ Vec<S, NU> combine(const Vec<S, NU>& b, const Vec<S, NU>& a, S ar, S ai, S br, S bi) {
@@ -112,76 +169,95 @@ __device__ __forceinline__ void move_rows(const S* __restrict__ src, S* __restri
           ++y;
           x -= nxu;
         }
-        bv[u] = su[y * sld + x];
+        bv[u] = load(su + (y * sld + x));
         doff[u] = y * dld + x;
-        if constexpr (MODE == MODE_AXPBY) av[u] = du[doff[u]];
+        if constexpr (MODE == MODE_AXPBY) av[u] = load<COSTA_NT_ALOADS>(du + doff[u]);
       }
     }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
-      if (doff[u] >= 0) du[doff[u]] = combine<S, NU, CPLX, MODE, CONJ>(bv[u], av[u], ar, ai, br, bi);
-  }
-}
-
-// Rectangle whose source runs along y while the destination runs along x:
-// staged through an LDS tile of TS x TS elements (one padding column against
-// bank conflicts).  Loads are coalesced along the source, stores along the
-// destination.
-template <typename S, bool CPLX, int MODE, bool CONJ, int TS>
-__device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __restrict__ dst, const Piece& p,
-                                                Vec<S, CPLX ? 2 : 1> (*tile)[TS + 1], S ar, S ai, S br, S bi) {
-  constexpr int NS = CPLX ? 2 : 1;
-  using E = Vec<S, NS>;
-  constexpr int ROWS = kThreads / TS;  // tile rows per pass
-  const E* __restrict__ se = reinterpret_cast<const E*>(src) + p.src_off;
-  E* __restrict__ de = reinterpret_cast<E*>(dst) + p.dst_off;
-  const int32_t tid = threadIdx.x;
-  const int32_t lane = tid % TS, row = tid / TS;
-  for (int32_t ty = 0; ty < p.ny; ty += TS) {
-    for (int32_t tx = 0; tx < p.nx; tx += TS) {
-      // load: source contiguous along y
-      const int32_t y = ty + lane;
-#pragma unroll
-      for (int k = 0; k < TS / ROWS; ++k) {
-        const int32_t lx = row + k * ROWS;
-        const int32_t x = tx + lx;
-        if (x < p.nx && y < p.ny) tile[lx][lane] = se[(int64_t)x * p.src_ld + y];
-      }
-      __syncthreads();
-      // store: destination contiguous along x
-      const int32_t x = tx + lane;
-#pragma unroll
-      for (int k = 0; k < TS / ROWS; ++k) {
-        const int32_t ly = row + k * ROWS;
-        const int32_t yy = ty + ly;
-        if (x < p.nx && yy < p.ny) {
-          const int64_t o = (int64_t)yy * p.dst_ld + x;
-          E a;
-          if constexpr (MODE == MODE_AXPBY) a = de[o];
-          de[o] = combine<S, NS, CPLX, MODE, CONJ>(tile[lane][ly], a, ar, ai, br, bi);
-        }
-      }
-      __syncthreads();
-    }
+      if (doff[u] >= 0) store(du + doff[u], combine<S, NU, CPLX, MODE, CONJ>(bv[u], av[u], ar, ai, br, bi));
   }
 }
 
 template <typename S, bool CPLX>
 struct TypeTraits {
-  static constexpr int NS = CPLX ? 2 : 1;                      // scalars per element
-  static constexpr int ES = (int)sizeof(S) * NS;               // bytes per element
-  static constexpr int WIDE_NEL = ES >= 16 ? 1 : 16 / ES;      // elements per 16-byte unit
-  static constexpr int TS = ES >= 16 ? 32 : 64;                // transpose tile
+  static constexpr int NS = CPLX ? 2 : 1;                  // scalars per element
+  static constexpr int ES = (int)sizeof(S) * NS;           // bytes per element
+  static constexpr int WIDE_NEL = ES >= 16 ? 1 : 16 / ES;  // elements per 16-byte unit
   static constexpr int UNROLL_NARROW = ES >= 16 ? 4 : 8;
+  // transpose tile: TX elements along the destination's contiguous direction
+  // (store lanes), TY along the source's (load lanes)
+  static constexpr int TX = ES >= 16 ? 32 : ES == 8 ? COSTA_TILE_X8 : 64;
+  static constexpr int TY = ES >= 8 ? 32 : 64;
 };
 
+template <typename S, bool CPLX>
+using Tile = Vec<S, CPLX ? 2 : 1> (*)[TypeTraits<S, CPLX>::TY + 1];
+
+// Rectangle whose source runs along y while the destination runs along x:
+// staged through an LDS tile of TX x TY elements (one padding column against
+// bank conflicts).  Loads are coalesced along the source, stores along the
+// destination.  Software pipelined: the loads of the next tile are in flight
+// while the current tile is written out.
 template <typename S, bool CPLX, int MODE, bool CONJ>
-__device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p, bool wide,
-                                           Vec<S, CPLX ? 2 : 1> (*tile)[TypeTraits<S, CPLX>::TS + 1], S ar, S ai,
-                                           S br, S bi) {
+__device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __restrict__ dst, const Piece& p,
+                                                Tile<S, CPLX> tile, S ar, S ai, S br, S bi) {
   using TT = TypeTraits<S, CPLX>;
-  if (p.flags & PIECE_TRANSPOSE) {
-    move_transposed<S, CPLX, MODE, CONJ, TT::TS>(src, dst, p, tile, ar, ai, br, bi);
+  using E = Vec<S, TT::NS>;
+  constexpr int TX = TT::TX, TY = TT::TY;
+  constexpr int LROWS = kThreads / TY;  // x rows per load pass
+  constexpr int SROWS = kThreads / TX;  // y rows per store pass
+  constexpr int NL = TX / LROWS;        // loads per thread per tile
+  const E* __restrict__ se = reinterpret_cast<const E*>(src) + p.src_off;
+  E* __restrict__ de = reinterpret_cast<E*>(dst) + p.dst_off;
+  const int32_t tid = threadIdx.x;
+  const int32_t ly0 = tid % TY, lx0 = tid / TY;  // load mapping
+  const int32_t sx0 = tid % TX, sy0 = tid / TX;  // store mapping
+  const int32_t ntx = (p.nx + TX - 1) / TX, nty = (p.ny + TY - 1) / TY;
+  const int32_t ntiles = ntx * nty;
+  E buf[NL];
+  auto fetch = [&](int32_t t) {
+    const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
+    const int32_t y = ty + ly0;
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int32_t x = tx + lx0 + k * LROWS;
+      if (x < p.nx && y < p.ny) buf[k] = load(se + ((int64_t)x * p.src_ld + y));
+    }
+  };
+  fetch(0);
+  for (int32_t t = 0; t < ntiles; ++t) {
+    const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int32_t lx = lx0 + k * LROWS;
+      if (tx + lx < p.nx && ty + ly0 < p.ny) tile[lx][ly0] = buf[k];
+    }
+    __syncthreads();
+    if (t + 1 < ntiles) fetch(t + 1);
+    const int32_t x = tx + sx0;
+#pragma unroll
+    for (int k = 0; k < TY / SROWS; ++k) {
+      const int32_t ly = sy0 + k * SROWS;
+      const int32_t yy = ty + ly;
+      if (x < p.nx && yy < p.ny) {
+        E* o = de + ((int64_t)yy * p.dst_ld + x);
+        E a;
+        if constexpr (MODE == MODE_AXPBY) a = load<COSTA_NT_ALOADS>(o);
+        store(o, combine<S, TT::NS, CPLX, MODE, CONJ>(tile[sx0][ly], a, ar, ai, br, bi));
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <typename S, bool CPLX, int MODE, bool CONJ, bool HAS_T>
+__device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p, bool wide, Tile<S, CPLX> tile, S ar,
+                                           S ai, S br, S bi) {
+  using TT = TypeTraits<S, CPLX>;
+  if (HAS_T && (p.flags & PIECE_TRANSPOSE)) {
+    if constexpr (HAS_T) move_transposed<S, CPLX, MODE, CONJ>(src, dst, p, tile, ar, ai, br, bi);
   } else if (wide && TT::WIDE_NEL > 1) {
     move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, 4>(src, dst, p, ar, ai, br, bi);
   } else {
@@ -189,51 +265,54 @@ __device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p,
   }
 }
 
-// KIND: 0 pack (bitwise copy, never transposed), 1 unpack-transform, 2 direct.
-template <typename S, bool CPLX, int KIND>
-__global__ void __launch_bounds__(kThreads) costa_mover(const Piece* __restrict__ pieces,
-                                                        const int32_t* __restrict__ groups, int32_t ngroups,
-                                                        void* const* __restrict__ bufs,
-                                                        const ItemParam* __restrict__ items, int32_t allow_wide) {
+constexpr int MODE_ANY = 3;
+
+// One launch over groups of rectangles.
+//   KIND: pack (bitwise copy into message buffers, never transposed),
+//         unpack-transform, or direct.
+//   MODE: the arithmetic of every pair of the call, or MODE_ANY to read it
+//         per rectangle (batches that mix modes); CONJ likewise.
+//   HAS_T: whether the launch contains transposed rectangles (LDS tile).
+template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
+costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ groups, int32_t ngroups,
+            void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
+  __shared__ E tile_mem[HAS_T ? TT::TX : 1][HAS_T ? TT::TY + 1 : 1];
+  Tile<S, CPLX> tile = reinterpret_cast<Tile<S, CPLX>>(&tile_mem[0][0]);
   const int32_t g = xcd_remap((int32_t)blockIdx.x, ngroups);
   const int32_t p0 = groups[g], p1 = groups[g + 1];
-  if constexpr (KIND == KIND_PACK) {
-    for (int32_t pi = p0; pi < p1; ++pi) {
-      const Piece p = pieces[pi];
-      const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
-      S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
-      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
-      if (wide && TT::WIDE_NEL > 1)
-        move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE_COPY, false, 4>(src, dst, p, S(0), S(0), S(0),
-                                                                                      S(0));
-      else
-        move_rows<S, TT::NS, 1, CPLX, MODE_COPY, false, TT::UNROLL_NARROW>(src, dst, p, S(0), S(0), S(0), S(0));
-    }
-  } else {
-    __shared__ E tile[TT::TS][TT::TS + 1];
-    for (int32_t pi = p0; pi < p1; ++pi) {
-      const Piece p = pieces[pi];
-      const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
-      S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
-      const ItemParam ip = items[p.item];
-      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
+  Piece next = pieces[p0];
+  for (int32_t pi = p0; pi < p1; ++pi) {
+    const Piece p = next;
+    if (pi + 1 < p1) next = pieces[pi + 1];  // fetch the next descriptor while this one moves
+    const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
+    S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
+    const bool wide = allow_wide && (p.flags & PIECE_WIDE);
+    if constexpr (KIND == KIND_PACK) {
+      move_piece<S, CPLX, MODE_COPY, false, false>(src, dst, p, wide, tile, S(0), S(0), S(0), S(0));
+    } else {
+      const ItemParam& ip = items[p.item];
       const S ar = (S)ip.alpha[0], ai = (S)ip.alpha[1], br = (S)ip.beta[0], bi = (S)ip.beta[1];
-      const bool conj = CPLX && ip.conj;
-      switch (ip.mode) {
-        case MODE_COPY:
-          if (conj) move_piece<S, CPLX, MODE_COPY, true>(src, dst, p, wide, tile, ar, ai, br, bi);
-          else move_piece<S, CPLX, MODE_COPY, false>(src, dst, p, wide, tile, ar, ai, br, bi);
-          break;
-        case MODE_SCALE:
-          if (conj) move_piece<S, CPLX, MODE_SCALE, true>(src, dst, p, wide, tile, ar, ai, br, bi);
-          else move_piece<S, CPLX, MODE_SCALE, false>(src, dst, p, wide, tile, ar, ai, br, bi);
-          break;
-        default:
-          if (conj) move_piece<S, CPLX, MODE_AXPBY, true>(src, dst, p, wide, tile, ar, ai, br, bi);
-          else move_piece<S, CPLX, MODE_AXPBY, false>(src, dst, p, wide, tile, ar, ai, br, bi);
-          break;
+      if constexpr (MODE != MODE_ANY) {
+        move_piece<S, CPLX, MODE, CONJ, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+      } else {
+        const bool conj = CPLX && ip.conj;
+        switch (ip.mode) {
+          case MODE_COPY:
+            if (conj) move_piece<S, CPLX, MODE_COPY, true, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_COPY, false, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            break;
+          case MODE_SCALE:
+            if (conj) move_piece<S, CPLX, MODE_SCALE, true, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_SCALE, false, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            break;
+          default:
+            if (conj) move_piece<S, CPLX, MODE_AXPBY, true, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_AXPBY, false, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            break;
+        }
       }
     }
   }
@@ -268,40 +347,65 @@ __global__ void __launch_bounds__(kThreads) costa_volume(VolumeArgs a, int32_t u
   }
 }
 
-template <typename S, bool CPLX>
-hipError_t launch_typed(MoverKind kind, const Piece* pieces, const int32_t* groups, int64_t ngroups,
-                        void* const* bufs, const ItemParam* items, int32_t allow_wide, hipStream_t stream) {
-  dim3 grid((unsigned)ngroups), block(kThreads);
-  const int32_t ng = (int32_t)ngroups;
-  switch (kind) {
-    case KIND_PACK:
-      hipLaunchKernelGGL((costa_mover<S, CPLX, KIND_PACK>), grid, block, 0, stream, pieces, groups, ng, bufs, items,
-                         allow_wide);
-      break;
-    case KIND_UNPACK:
-      hipLaunchKernelGGL((costa_mover<S, CPLX, KIND_UNPACK>), grid, block, 0, stream, pieces, groups, ng, bufs,
-                         items, allow_wide);
-      break;
-    default:
-      hipLaunchKernelGGL((costa_mover<S, CPLX, KIND_DIRECT>), grid, block, 0, stream, pieces, groups, ng, bufs,
-                         items, allow_wide);
-      break;
-  }
+struct Launch {
+  dim3 grid, block;
+  hipStream_t stream;
+  const Piece* pieces;
+  const int32_t* groups;
+  int32_t ngroups;
+  void* const* bufs;
+  const ItemParam* items;
+  int32_t allow_wide;
+};
+
+template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
+hipError_t go(const Launch& l) {
+  hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
+                     l.groups, l.ngroups, l.bufs, l.items, l.allow_wide);
   return hipGetLastError();
+}
+
+template <typename S, bool CPLX, int KIND, bool HAS_T>
+hipError_t go_mode(const Launch& l, int mode, int conj) {
+  // fixed-mode kernels for the element types of the hot workloads; the rest
+  // read the mode per rectangle
+  constexpr bool SPECIALISE = sizeof(S) == 8;
+  if constexpr (SPECIALISE) {
+    if (mode == MODE_COPY) return conj ? go<S, CPLX, KIND, MODE_COPY, CPLX, HAS_T>(l)
+                                       : go<S, CPLX, KIND, MODE_COPY, false, HAS_T>(l);
+    if (mode == MODE_SCALE) return conj ? go<S, CPLX, KIND, MODE_SCALE, CPLX, HAS_T>(l)
+                                        : go<S, CPLX, KIND, MODE_SCALE, false, HAS_T>(l);
+    if (mode == MODE_AXPBY) return conj ? go<S, CPLX, KIND, MODE_AXPBY, CPLX, HAS_T>(l)
+                                        : go<S, CPLX, KIND, MODE_AXPBY, false, HAS_T>(l);
+  }
+  return go<S, CPLX, KIND, MODE_ANY, false, HAS_T>(l);
+}
+
+template <typename S, bool CPLX>
+hipError_t launch_typed(MoverKind kind, const LaunchSpec& spec, const Launch& l) {
+  if (kind == KIND_PACK) return go<S, CPLX, KIND_PACK, MODE_COPY, false, false>(l);
+  if (kind == KIND_UNPACK) {
+    return spec.has_transpose ? go_mode<S, CPLX, KIND_UNPACK, true>(l, spec.mode, spec.conj)
+                              : go_mode<S, CPLX, KIND_UNPACK, false>(l, spec.mode, spec.conj);
+  }
+  return spec.has_transpose ? go_mode<S, CPLX, KIND_DIRECT, true>(l, spec.mode, spec.conj)
+                            : go_mode<S, CPLX, KIND_DIRECT, false>(l, spec.mode, spec.conj);
 }
 
 }  // namespace
 
-hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const Piece* pieces, const int32_t* groups,
-                        int64_t ngroups, void* const* bufs, const ItemParam* items, int32_t allow_wide,
-                        hipStream_t stream) {
+hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
+                        const int32_t* groups, int64_t ngroups, void* const* bufs, const ItemParam* items,
+                        int32_t allow_wide, hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
   if (ngroups > INT32_MAX) return hipErrorInvalidValue;
+  Launch l{dim3((unsigned)ngroups), dim3(kThreads), stream, pieces, groups, (int32_t)ngroups, bufs, items,
+           allow_wide};
   switch (dtype) {
-    case COSTA_R64: return launch_typed<double, false>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
-    case COSTA_C128: return launch_typed<double, true>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
-    case COSTA_R32: return launch_typed<float, false>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
-    case COSTA_C64: return launch_typed<float, true>(kind, pieces, groups, ngroups, bufs, items, allow_wide, stream);
+    case COSTA_R64: return launch_typed<double, false>(kind, spec, l);
+    case COSTA_C128: return launch_typed<double, true>(kind, spec, l);
+    case COSTA_R32: return launch_typed<float, false>(kind, spec, l);
+    case COSTA_C64: return launch_typed<float, true>(kind, spec, l);
   }
   return hipErrorInvalidValue;
 }

@@ -18,6 +18,12 @@
 
 #include "plan.hpp"
 
+// Put the direct rectangles into the last unpack launch instead of a launch
+// of their own.
+#ifndef COSTA_MERGE_DIRECT
+#define COSTA_MERGE_DIRECT 1
+#endif
+
 namespace costa {
 
 std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<int64_t>& sb) {
@@ -216,6 +222,7 @@ LaunchRange add_launch(HostPlan& hp, const std::vector<Piece>& ps, const PlanCon
     acc += (int64_t)ps[k].nx * ps[k].ny;
     lr.elems += (int64_t)ps[k].nx * ps[k].ny;
     lr.item_elems[ps[k].item] += (int64_t)ps[k].nx * ps[k].ny;
+    if (ps[k].flags & PIECE_TRANSPOSE) lr.has_transpose = true;
     ++cnt;
     if (acc >= cfg.min_group_elems || cnt >= cfg.max_group_pieces) {
       acc = 0;
@@ -249,8 +256,25 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     hp.item_total[k] = items[k].A->nrows * items[k].A->ncols;
     plan_pair(k, n, items[k], sigma, local, remote, hp.overlay_blocks, hp.item_local[k], hp.item_remote[k]);
   }
-  split_pieces(local, cfg.max_piece_elems);
-  split_pieces(remote, cfg.max_piece_elems);
+  // a launch should offer the chip a few thousand workgroups: small launches
+  // get smaller rectangles and groups
+  auto total_of = [](const std::vector<Cand>& v) {
+    int64_t t = 0;
+    for (const Cand& c : v) t += (int64_t)c.p.nx * c.p.ny;
+    return t;
+  };
+  const int64_t local_total = total_of(local), remote_total = total_of(remote);
+  auto piece_cap = [&](int64_t total) {
+    return std::max<int64_t>(4096, std::min<int64_t>(cfg.max_piece_elems, total / cfg.target_groups));
+  };
+  split_pieces(local, piece_cap(local_total));
+  split_pieces(remote, piece_cap(remote_total));
+  auto group_cfg = [&](int64_t total) {
+    PlanConfig g = cfg;
+    g.min_group_elems = std::max<int64_t>(1024, std::min<int64_t>(cfg.min_group_elems, total / cfg.target_groups));
+    return g;
+  };
+  const PlanConfig cfg_local = group_cfg(local_total), cfg_remote = group_cfg(remote_total);
 
   // direct path, in destination order
   std::vector<Piece> direct;
@@ -261,7 +285,6 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
   }
   std::sort(direct.begin(), direct.end(), by_dst);
   hp.pieces_direct = (int32_t)direct.size();
-  hp.direct = add_launch(hp, direct, cfg, n);
 
   // messages: packages ordered by sender, then receiver (each sender's send
   // buffer holds one contiguous package per receiver); blocks in source order
@@ -311,16 +334,26 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
       off += chunk_bytes(q);
       ++k;
     }
+    hp.pieces_pack += (int32_t)pack.size();
+    hp.pieces_unpack += (int32_t)unpack.size();
+    const bool last = k == remote.size();
+    if (last && COSTA_MERGE_DIRECT) {
+      // the direct rectangles join the last unpack launch: one pass writes A
+      // in destination order (the kernel reads each rectangle's source from
+      // the buffer its descriptor names, B or the message workspace)
+      unpack.insert(unpack.end(), direct.begin(), direct.end());
+      direct.clear();
+    }
     std::sort(unpack.begin(), unpack.end(), by_dst);
     Wave w;
     w.msg_bytes = off;
-    hp.pieces_pack += (int32_t)pack.size();
-    hp.pieces_unpack += (int32_t)unpack.size();
-    w.pack = add_launch(hp, pack, cfg, n);
-    w.unpack = add_launch(hp, unpack, cfg, n);
+    w.pack = add_launch(hp, pack, cfg_remote, n);
+    w.unpack = add_launch(hp, unpack, last && COSTA_MERGE_DIRECT ? group_cfg(remote_total + local_total)
+                                                                 : cfg_remote, n);
     hp.workspace_bytes = std::max(hp.workspace_bytes, off);
     hp.waves.push_back(w);
   }
+  hp.direct = add_launch(hp, direct, cfg_local, n);  // empty when merged above
   hp.plan_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
 }
 

@@ -21,6 +21,7 @@ struct PlanConfig {
   int64_t max_piece_elems; // split rectangles larger than this
   int64_t min_group_elems; // a workgroup takes consecutive rectangles up to this many elements
   int32_t max_group_pieces;
+  int64_t target_groups;   // aim for at least this many workgroups per launch
 };
 
 struct HostPlan {

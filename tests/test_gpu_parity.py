@@ -276,5 +276,10 @@ def test_timing_counters():
         case.run()
     t = C.costa_timing_read()
     C.costa_timing_enable(False)
-    assert t["pack"]["launches"] == 3 and t["unpack"]["launches"] == 3 and t["direct"]["launches"] == 3
-    assert t["pack"]["ms"] > 0 and t["unpack"]["bytes"] > 0
+    # the direct rectangles ride in the unpack launch (no launch of their own)
+    assert t["pack"]["launches"] == 3 and t["unpack"]["launches"] == 3 and t["direct"]["launches"] == 0
+    assert t["pack"]["ms"] > 0
+    descs = [dict(op=it.op, alpha=it.alpha, beta=it.beta, A=case.LA[0], B=case.LB[0]) for it in w.items]
+    st = C.costa_plan_stats(w.dtype, descs, case.sigma)
+    assert t["pack"]["bytes"] == 3 * st["pack_bytes"]
+    assert t["unpack"]["bytes"] == 3 * (st["unpack_bytes"] + st["direct_bytes"])
