@@ -118,6 +118,8 @@ def main():
     ap.add_argument("--workload", default="blocksize_change_16k")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="before warm-up, run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the transform's virtual ranks all live in "
@@ -171,6 +173,13 @@ def main():
         else:
             C.costa_transform_batched(w.dtype, descs, sigma, stream)
 
+    if args.copy_probe:
+        src = torch.ones(args.copy_probe << 17, dtype=torch.float64, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     step()  # builds and uploads the plan
     torch.cuda.synchronize()
     plan_s = time.perf_counter() - t_plan0
