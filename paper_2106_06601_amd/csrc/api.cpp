@@ -15,8 +15,20 @@
 namespace costa {
 namespace {
 
-constexpr int64_t kMaxPieceElems = 1 << 16;
-constexpr int64_t kMinGroupElems = 1 << 14;
+// Work sizes (measured on MI355X): rectangles of at most 16K elements, and a
+// workgroup takes consecutive rectangles until it holds 16 KiB (8-byte
+// elements) to 64 KiB (16-byte elements) of them.
+#ifndef COSTA_MAX_PIECE_ELEMS
+#define COSTA_MAX_PIECE_ELEMS (1 << 14)
+#endif
+#ifndef COSTA_MIN_GROUP_ELEMS
+#define COSTA_MIN_GROUP_ELEMS 0  // 0: by element size
+#endif
+constexpr int64_t kMaxPieceElems = COSTA_MAX_PIECE_ELEMS;
+int64_t min_group_elems(int es) {
+  if (COSTA_MIN_GROUP_ELEMS) return COSTA_MIN_GROUP_ELEMS;
+  return es >= 16 ? 4096 : 2048;
+}
 constexpr int32_t kMaxGroupPieces = 64;
 constexpr int64_t kTargetGroups = 4096;
 
@@ -117,7 +129,7 @@ PlanConfig make_config(int es) {
   c.elem_size = es;
   c.workspace_cap = INT64_MAX;
   c.max_piece_elems = kMaxPieceElems;
-  c.min_group_elems = kMinGroupElems;
+  c.min_group_elems = min_group_elems(es);
   c.max_group_pieces = kMaxGroupPieces;
   c.target_groups = kTargetGroups;
   return c;

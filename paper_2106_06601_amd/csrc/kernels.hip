@@ -19,11 +19,38 @@
 namespace costa {
 namespace {
 
+// Tuning switches (compile-time; the defaults are the measured best).
+#ifndef COSTA_UNROLL_WIDE
+#define COSTA_UNROLL_WIDE 4  // 16-byte units in flight per lane on the row walk
+#endif
+#ifndef COSTA_XCD_REMAP
+#define COSTA_XCD_REMAP 1
+#endif
+#ifndef COSTA_TILE_X8
+#define COSTA_TILE_X8 32
+#endif
+#ifndef COSTA_NT_LOADS
+#define COSTA_NT_LOADS 1  // row walks: each source line is read once
+#endif
+#ifndef COSTA_NT_LOADS_MAX_ES
+#define COSTA_NT_LOADS_MAX_ES 8  // ...for element sizes up to this (measured: helps fp64, hurts complex128)
+#endif
+#ifndef COSTA_NT_TILE_LOADS
+#define COSTA_NT_TILE_LOADS 0  // tile loads: lines may serve two neighbouring tiles
+#endif
+#ifndef COSTA_NT_STORES
+#define COSTA_NT_STORES 1
+#endif
+#ifndef COSTA_NT_ALOADS
+#define COSTA_NT_ALOADS 0
+#endif
+
 constexpr int kThreads = 256;
 
 // Workgroup b of n (dispatched round-robin over the 8 XCDs) gets the b-th
 // slot of a contiguous range per XCD, so consecutive groups share an L2.
 __device__ __forceinline__ int32_t xcd_remap(int32_t b, int32_t n) {
+  if (!COSTA_XCD_REMAP) return b;
   constexpr int32_t X = 8;
   const int32_t q = n / X, r = n % X;
   const int32_t xcd = b % X, idx = b / X;
@@ -52,19 +79,6 @@ template <>
 struct Raw<16> {
   typedef uint32_t T __attribute__((ext_vector_type(4)));
 };
-
-#ifndef COSTA_TILE_X8
-#define COSTA_TILE_X8 32
-#endif
-#ifndef COSTA_NT_LOADS
-#define COSTA_NT_LOADS 0
-#endif
-#ifndef COSTA_NT_STORES
-#define COSTA_NT_STORES 1
-#endif
-#ifndef COSTA_NT_ALOADS
-#define COSTA_NT_ALOADS 0
-#endif
 
 // The buffers reach the kernels through a pointer table, so the compiler
 // cannot see that they are global memory; the casts below make it emit global
@@ -169,7 +183,7 @@ __device__ __forceinline__ void move_rows(const S* __restrict__ src, S* __restri
           ++y;
           x -= nxu;
         }
-        bv[u] = load(su + (y * sld + x));
+        bv[u] = load<COSTA_NT_LOADS && (int)sizeof(S) * (CPLX ? 2 : 1) <= COSTA_NT_LOADS_MAX_ES>(su + (y * sld + x));
         doff[u] = y * dld + x;
         if constexpr (MODE == MODE_AXPBY) av[u] = load<COSTA_NT_ALOADS>(du + doff[u]);
       }
@@ -223,7 +237,7 @@ __device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int32_t x = tx + lx0 + k * LROWS;
-      if (x < p.nx && y < p.ny) buf[k] = load(se + ((int64_t)x * p.src_ld + y));
+      if (x < p.nx && y < p.ny) buf[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)x * p.src_ld + y));
     }
   };
   fetch(0);
@@ -259,7 +273,7 @@ __device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p,
   if (HAS_T && (p.flags & PIECE_TRANSPOSE)) {
     if constexpr (HAS_T) move_transposed<S, CPLX, MODE, CONJ>(src, dst, p, tile, ar, ai, br, bi);
   } else if (wide && TT::WIDE_NEL > 1) {
-    move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, 4>(src, dst, p, ar, ai, br, bi);
+    move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, COSTA_UNROLL_WIDE>(src, dst, p, ar, ai, br, bi);
   } else {
     move_rows<S, TT::NS, 1, CPLX, MODE, CONJ, TT::UNROLL_NARROW>(src, dst, p, ar, ai, br, bi);
   }
