@@ -29,6 +29,18 @@ namespace {
 #ifndef COSTA_TILE_X8
 #define COSTA_TILE_X8 32
 #endif
+#ifndef COSTA_TILE_Y8
+#define COSTA_TILE_Y8 32
+#endif
+#ifndef COSTA_TILE_X16
+#define COSTA_TILE_X16 128  // 16-byte elements: 2 KiB store runs
+#endif
+#ifndef COSTA_TILE_Y16
+#define COSTA_TILE_Y16 16
+#endif
+#ifndef COSTA_TILE_DEPTH
+#define COSTA_TILE_DEPTH 1  // tiles of loads in flight ahead of the one being stored (1 or 2)
+#endif
 #ifndef COSTA_NT_LOADS
 #define COSTA_NT_LOADS 1  // row walks: each source line is read once
 #endif
@@ -201,9 +213,11 @@ struct TypeTraits {
   static constexpr int WIDE_NEL = ES >= 16 ? 1 : 16 / ES;  // elements per 16-byte unit
   static constexpr int UNROLL_NARROW = ES >= 16 ? 4 : 8;
   // transpose tile: TX elements along the destination's contiguous direction
-  // (store lanes), TY along the source's (load lanes)
-  static constexpr int TX = ES >= 16 ? 32 : ES == 8 ? COSTA_TILE_X8 : 64;
-  static constexpr int TY = ES >= 8 ? 32 : 64;
+  // (store lanes), TY along the source's (load lanes).  Long store runs pay
+  // off for 16-byte elements; 8-byte elements keep 32 x 32 (occupancy, and
+  // the narrow transposed rectangles of block-cyclic layouts)
+  static constexpr int TX = ES >= 16 ? COSTA_TILE_X16 : ES == 8 ? COSTA_TILE_X8 : 64;
+  static constexpr int TY = ES >= 16 ? COSTA_TILE_Y16 : ES == 8 ? COSTA_TILE_Y8 : 64;
 };
 
 template <typename S, bool CPLX>
@@ -230,26 +244,26 @@ __device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __
   const int32_t sx0 = tid % TX, sy0 = tid / TX;  // store mapping
   const int32_t ntx = (p.nx + TX - 1) / TX, nty = (p.ny + TY - 1) / TY;
   const int32_t ntiles = ntx * nty;
-  E buf[NL];
-  auto fetch = [&](int32_t t) {
+  auto fetch = [&](int32_t t, E (&b)[NL]) {
     const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
     const int32_t y = ty + ly0;
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int32_t x = tx + lx0 + k * LROWS;
-      if (x < p.nx && y < p.ny) buf[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)x * p.src_ld + y));
+      if (x < p.nx && y < p.ny) b[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)x * p.src_ld + y));
     }
   };
-  fetch(0);
-  for (int32_t t = 0; t < ntiles; ++t) {
+  // one tile: registers -> LDS, start the loads DEPTH tiles ahead into the
+  // freed registers, LDS -> destination
+  auto step = [&](int32_t t, E (&b)[NL]) {
     const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int32_t lx = lx0 + k * LROWS;
-      if (tx + lx < p.nx && ty + ly0 < p.ny) tile[lx][ly0] = buf[k];
+      if (tx + lx < p.nx && ty + ly0 < p.ny) tile[lx][ly0] = b[k];
     }
     __syncthreads();
-    if (t + 1 < ntiles) fetch(t + 1);
+    if (t + COSTA_TILE_DEPTH < ntiles) fetch(t + COSTA_TILE_DEPTH, b);
     const int32_t x = tx + sx0;
 #pragma unroll
     for (int k = 0; k < TY / SROWS; ++k) {
@@ -263,6 +277,18 @@ __device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __
       }
     }
     __syncthreads();
+  };
+  E b0[NL];
+  fetch(0, b0);
+  if constexpr (COSTA_TILE_DEPTH == 2) {
+    E b1[NL];
+    if (ntiles > 1) fetch(1, b1);
+    for (int32_t t = 0; t < ntiles; t += 2) {
+      step(t, b0);
+      if (t + 1 < ntiles) step(t + 1, b1);
+    }
+  } else {
+    for (int32_t t = 0; t < ntiles; ++t) step(t, b0);
   }
 }
 

@@ -23,6 +23,10 @@
 #ifndef COSTA_MERGE_DIRECT
 #define COSTA_MERGE_DIRECT 1
 #endif
+// Cut transposed rectangles into tile-aligned near-square pieces.
+#ifndef COSTA_SPLIT_SQUARE
+#define COSTA_SPLIT_SQUARE 1
+#endif
 
 namespace costa {
 
@@ -169,11 +173,14 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
   for (Cand& c : all) (c.s == c.r ? local : remote).push_back(c);
 }
 
-// Splits rectangles larger than max_elems (tile-aligned for transposes).
+// Splits rectangles larger than max_elems.  Row walks keep whole rows (long
+// contiguous runs); transposed rectangles are cut into near-square pieces
+// whose sides are multiples of the 32-element LDS tile, so that no piece is a
+// thin strip that leaves most of a tile idle.
 void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
   std::vector<Cand> out;
   out.reserve(v.size());
-  const int32_t TS = 64;
+  const int64_t TS = 32;
   for (const Cand& c : v) {
     const Piece& p = c.p;
     const bool T = p.flags & PIECE_TRANSPOSE;
@@ -181,10 +188,21 @@ void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
       out.push_back(c);
       continue;
     }
-    int64_t cx = std::min<int64_t>(p.nx, max_elems);
-    if (T && cx >= TS) cx -= cx % TS;
-    int64_t cy = std::max<int64_t>(1, max_elems / cx);
-    if (T && cy >= TS) cy -= cy % TS;
+    int64_t cx, cy;
+    if (T && COSTA_SPLIT_SQUARE) {
+      int64_t side = TS;
+      while ((2 * side) * (2 * side) <= max_elems) side *= 2;  // largest power-of-two square that fits
+      cx = std::min<int64_t>(p.nx, side);
+      cy = std::max<int64_t>(TS, max_elems / cx);
+      cy = std::min<int64_t>(p.ny, cy - cy % TS);
+      if (cx < side) {  // narrow in x: give the room to y
+        cy = std::max<int64_t>(TS, max_elems / cx);
+        cy = std::min<int64_t>(p.ny, cy - cy % TS);
+      }
+    } else {
+      cx = std::min<int64_t>(p.nx, max_elems);
+      cy = std::max<int64_t>(1, max_elems / cx);
+    }
     for (int64_t y0 = 0; y0 < p.ny; y0 += cy)
       for (int64_t x0 = 0; x0 < p.nx; x0 += cx) {
         Cand d = c;
