@@ -231,7 +231,7 @@ def main():
         "config": describe(w),
         "model_bytes_per_step": stats["model_bytes"],
         "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
-        "waves": stats["waves"], "plan_s": round(plan_s, 3),
+        "waves": per_kernel.get("pack", {}).get("launches_per_step", 0), "plan_s": round(plan_s, 3),
         "kernels": per_kernel,
         "roofline": roof,
         "cpu_baseline": cpu,

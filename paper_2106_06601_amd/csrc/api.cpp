@@ -15,20 +15,21 @@
 namespace costa {
 namespace {
 
-// Work sizes (measured on MI355X): rectangles of at most 16K elements, and a
-// workgroup takes consecutive rectangles until it holds 16 KiB (8-byte
-// elements) to 64 KiB (16-byte elements) of them.
+// Work sizes (measured on MI355X): rectangles of at most 16K elements (times
+// COSTA_T_PIECE_FACTOR when transposed), and a workgroup takes consecutive
+// rectangles until it holds 512 elements, i.e. small rectangles get a
+// workgroup each.
 #ifndef COSTA_MAX_PIECE_ELEMS
 #define COSTA_MAX_PIECE_ELEMS (1 << 14)
 #endif
 #ifndef COSTA_MIN_GROUP_ELEMS
-#define COSTA_MIN_GROUP_ELEMS 0  // 0: by element size
+#define COSTA_MIN_GROUP_ELEMS 512
+#endif
+#ifndef COSTA_T_PIECE_FACTOR
+#define COSTA_T_PIECE_FACTOR 1
 #endif
 constexpr int64_t kMaxPieceElems = COSTA_MAX_PIECE_ELEMS;
-int64_t min_group_elems(int es) {
-  if (COSTA_MIN_GROUP_ELEMS) return COSTA_MIN_GROUP_ELEMS;
-  return es >= 16 ? 4096 : 2048;
-}
+int64_t min_group_elems(int) { return COSTA_MIN_GROUP_ELEMS; }
 constexpr int32_t kMaxGroupPieces = 64;
 constexpr int64_t kTargetGroups = 4096;
 
@@ -132,6 +133,7 @@ PlanConfig make_config(int es) {
   c.min_group_elems = min_group_elems(es);
   c.max_group_pieces = kMaxGroupPieces;
   c.target_groups = kTargetGroups;
+  c.transpose_piece_factor = COSTA_T_PIECE_FACTOR;
   return c;
 }
 

@@ -177,13 +177,14 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
 // contiguous runs); transposed rectangles are cut into near-square pieces
 // whose sides are multiples of the 32-element LDS tile, so that no piece is a
 // thin strip that leaves most of a tile idle.
-void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
+void split_pieces(std::vector<Cand>& v, int64_t max_nt, int64_t t_factor) {
   std::vector<Cand> out;
   out.reserve(v.size());
   const int64_t TS = 32;
   for (const Cand& c : v) {
     const Piece& p = c.p;
     const bool T = p.flags & PIECE_TRANSPOSE;
+    const int64_t max_elems = T ? max_nt * t_factor : max_nt;
     if ((int64_t)p.nx * p.ny <= max_elems) {
       out.push_back(c);
       continue;
@@ -285,11 +286,12 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
   auto piece_cap = [&](int64_t total) {
     return std::max<int64_t>(4096, std::min<int64_t>(cfg.max_piece_elems, total / cfg.target_groups));
   };
-  split_pieces(local, piece_cap(local_total));
-  split_pieces(remote, piece_cap(remote_total));
+  split_pieces(local, piece_cap(local_total), cfg.transpose_piece_factor);
+  split_pieces(remote, piece_cap(remote_total), cfg.transpose_piece_factor);
   auto group_cfg = [&](int64_t total) {
     PlanConfig g = cfg;
-    g.min_group_elems = std::max<int64_t>(1024, std::min<int64_t>(cfg.min_group_elems, total / cfg.target_groups));
+    g.min_group_elems = std::max<int64_t>(std::min<int64_t>(1024, cfg.min_group_elems),
+                                          std::min<int64_t>(cfg.min_group_elems, total / cfg.target_groups));
     return g;
   };
   const PlanConfig cfg_local = group_cfg(local_total), cfg_remote = group_cfg(remote_total);

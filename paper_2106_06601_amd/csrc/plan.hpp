@@ -22,6 +22,7 @@ struct PlanConfig {
   int64_t min_group_elems; // a workgroup takes consecutive rectangles up to this many elements
   int32_t max_group_pieces;
   int64_t target_groups;   // aim for at least this many workgroups per launch
+  int64_t transpose_piece_factor;  // transposed rectangles may be this many times larger
 };
 
 struct HostPlan {
