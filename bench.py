@@ -110,6 +110,40 @@ def cpu_baseline(w, sigma, model_bytes_per_elem: float, target_s: float):
             "seconds": round(dt, 2)}
 
 
+def relabel_report() -> dict:
+    """Local volume kept by the identity, the exact and the greedy relabeling
+    (the paper's matching, Section 6) on every workload, with solve times."""
+    import numpy as np
+    import torch
+    import synth
+    import paper_2106_06601_amd as C
+    torch.cuda.set_device(0)
+    out = {}
+    for name in synth.WORKLOADS:
+        w = synth.workload(name)
+        LA = [C.layout_from_spec(it.A) for it in w.items]
+        LB = [C.layout_from_spec(it.B) for it in w.items]
+        t0 = time.perf_counter()
+        V = sum(C.costa_volume_matrix(a, b, it.op) for a, b, it in zip(LA, LB, w.items))
+        t_v = time.perf_counter() - t0
+        total = int(V.sum())
+        t0 = time.perf_counter()
+        sig_e, kept_id, kept_e = C.costa_relabel(V)
+        t_e = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        sig_g, _, after_g = C.costa_relabel_cost(V, method="greedy")
+        t_g = time.perf_counter() - t0
+        kept_g = total - int(after_g)
+        out[name] = {"P": int(V.shape[0]), "total_elems": total,
+                     "local_identity": int(kept_id), "local_exact": int(kept_e), "local_greedy": kept_g,
+                     "remote_reduction_exact_pct": round(100 * (kept_e - kept_id) / max(1, total - kept_id), 3),
+                     "remote_reduction_greedy_pct": round(100 * (kept_g - kept_id) / max(1, total - kept_id), 3),
+                     "greedy_gap_pct_of_exact_gain": round(100 * (kept_e - kept_g) / max(1, kept_e - kept_id), 3),
+                     "volume_ms": round(t_v * 1e3, 3), "exact_ms": round(t_e * 1e3, 3), "greedy_ms": round(t_g * 1e3, 3)}
+    return {"metric": "relabeling: local volume kept (identity / exact / greedy)", "unit": "elements",
+            "data": "synthetic", "workloads": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -120,7 +154,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="before warm-up, run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--relabel-report", action="store_true",
+                    help="print the relabeling comparison of every workload instead of the throughput line")
     args = ap.parse_args()
+    if args.relabel_report:
+        print(json.dumps(relabel_report()), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the transform's virtual ranks all live in "
               "one GPU's HBM and this build has no multi-GPU exchange", file=sys.stderr)

@@ -147,6 +147,30 @@ costa_status costa_volume_matrix(costa_layout A, costa_layout B, costa_op op, in
 costa_status costa_relabel(int32_t P, const int64_t* V_host, int32_t* sigma, int64_t* retained_identity,
                            int64_t* retained_sigma);
 
+/* Matching used for the relabeling (Section 4.3, Algorithm 1 "MWBPM"). */
+typedef enum {
+  COSTA_RELABEL_EXACT = 0,  /* Hungarian method: an optimal relabeling */
+  COSTA_RELABEL_GREEDY = 1  /* the paper's greedy 2-approximation (Section 6): edges of G_delta
+                               by decreasing gain (ties: smaller label, then smaller rank) are
+                               taken while both ends are free */
+} costa_relabel_method;
+
+/* Relabeling under a general communication cost (Section 3): a package s of
+ * V(s) = V_host[i*P+j] * elem_bytes bytes sent from p_i to p_j costs
+ *     w(p_i, p_j, s) = latency[i*P+j] + inv_bandwidth[i*P+j] * V(s)   (s non-empty),
+ *     w = 0 for an empty package,
+ * the latency-bandwidth model of the network-topology cost.  latency and
+ * inv_bandwidth both NULL: the locally-free volume cost (eq:locally_free_w),
+ * w = V(s) for i != j and 0 for i == j.  The gains delta(p_x, p_y) follow
+ * eq:delta (sum over the left neighbours of p_x); sigma maximises
+ * sum_t delta(p_t, p_sigma[t]) (Lemma 2), exactly or greedily.
+ * cost_before / cost_after (may be NULL): W(G) and W(G_sigma) (def:WG).
+ * Host only.  Errors: INVALID_VALUE for P < 0, null arrays, negative
+ * volumes, non-finite or negative latency/bandwidth entries, unknown method. */
+costa_status costa_relabel_cost(int32_t P, const int64_t* V_host, double elem_bytes, const double* latency,
+                                const double* inv_bandwidth, costa_relabel_method method, int32_t* sigma,
+                                double* cost_before, double* cost_after);
+
 /* ---------------------------------------------------------------------------
  * The transform (Section 5 eq:costa and Algorithm 3; Section 6)
  * ------------------------------------------------------------------------- */

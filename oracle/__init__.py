@@ -217,7 +217,15 @@ def w_locally_free(i: int, j: int, vol: int) -> int:
     return vol if i != j else 0
 
 
-def total_cost(V: np.ndarray, sigma: Sequence[int]) -> int:
+def w_topology(latency: np.ndarray, inv_bandwidth: np.ndarray, elem_bytes: float = 1.0):
+    """Network-topology cost of Section 3: w(p_i, p_j, s) = L(p_i, p_j) +
+    B(p_i, p_j) * V(s) for a non-empty package of V(s) bytes."""
+    def w(i: int, j: int, vol: int):
+        return latency[i, j] + inv_bandwidth[i, j] * (vol * elem_bytes)
+    return w
+
+
+def total_cost(V: np.ndarray, sigma: Sequence[int], w=w_locally_free):
     """W(G_sigma): sum over the edges of the relabeled graph (Definitions of
     W(G) and of the relabeled graph: package S_ij now goes to p_sigma(j))."""
     P = V.shape[0]
@@ -225,24 +233,55 @@ def total_cost(V: np.ndarray, sigma: Sequence[int]) -> int:
     for i in range(P):
         for j in range(P):
             if V[i, j] != 0:  # (p_i, p_j) in E iff S_ij is non-empty
-                W += w_locally_free(i, sigma[j], int(V[i, j]))
+                W += w(i, sigma[j], int(V[i, j]))
     return W
 
 
-def gain(V: np.ndarray, x: int, y: int) -> int:
+def gain(V: np.ndarray, x: int, y: int, w=w_locally_free):
     """delta(p_x, p_y) from its definition, equation (eq:delta): the sum over
     the left neighbours p_i of p_x of w(p_i, p_x, S_ix) - w(p_i, p_y, S_ix)."""
     P = V.shape[0]
     d = 0
     for i in range(P):
         if V[i, x] != 0:
-            d += w_locally_free(i, x, int(V[i, x])) - w_locally_free(i, y, int(V[i, x]))
+            d += w(i, x, int(V[i, x])) - w(i, y, int(V[i, x]))
     return d
 
 
-def total_gain(V: np.ndarray, sigma: Sequence[int]) -> int:
+def total_gain(V: np.ndarray, sigma: Sequence[int], w=w_locally_free):
     """Delta_sigma = sum_j delta(p_j, p_sigma(j))."""
-    return sum(gain(V, j, sigma[j]) for j in range(V.shape[0]))
+    return sum(gain(V, j, sigma[j], w) for j in range(V.shape[0]))
+
+
+def relabel_bruteforce_cost(V: np.ndarray, w) -> List[int]:
+    """argmin_sigma W(G_sigma) under a general cost w, over all P! relabelings
+    (first minimiser in lexicographic order).  P <= 8."""
+    P = V.shape[0]
+    if P > 8:
+        raise ValueError("brute force is for P <= 8")
+    best, best_sigma = None, None
+    for perm in itertools.permutations(range(P)):
+        W = total_cost(V, perm, w)
+        if best is None or W < best:
+            best, best_sigma = W, list(perm)
+    return best_sigma
+
+
+def relabel_greedy(V: np.ndarray, w=w_locally_free) -> List[int]:
+    """Algorithm 1 with the matching the paper's implementation uses (Section 6:
+    a simple greedy 2-approximation): weights[i][j] = delta(p_i, p_j), edges
+    taken by decreasing weight (ties: smaller i, then smaller j) while both ends
+    are free; sigma[i] = j for every matched (p_i, p_j)."""
+    P = V.shape[0]
+    weights = [[gain(V, i, j, w) for j in range(P)] for i in range(P)]
+    edges = sorted(((i, j) for i in range(P) for j in range(P)), key=lambda e: (-weights[e[0]][e[1]], e[0], e[1]))
+    sigma = [-1] * P
+    used = [False] * P
+    for i, j in edges:
+        if sigma[i] < 0 and not used[j]:
+            sigma[i] = j
+            used[j] = True
+    return sigma
 
 
 def retained(V: np.ndarray, sigma: Sequence[int]) -> int:

@@ -65,6 +65,8 @@ _SIGS = {
     "costa_layout_destroy": [_vp],
     "costa_volume_matrix": [_vp, _vp, ctypes.c_int, _vp, _vp],
     "costa_relabel": [_i32, _vp, _vp, _P(_i64), _P(_i64)],
+    "costa_relabel_cost": [_i32, _vp, ctypes.c_double, _vp, _vp, ctypes.c_int, _vp, _P(ctypes.c_double),
+                           _P(ctypes.c_double)],
     "costa_transform": [ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp],
     "costa_transform_batched": [ctypes.c_int, _i32, _vp, _vp, _vp],
     "costa_set_workspace_limit": [ctypes.c_size_t],
@@ -225,6 +227,25 @@ def costa_relabel(V: np.ndarray):
     _check(_lib.costa_relabel(P, V.ctypes.data, sigma.ctypes.data, ctypes.byref(r0), ctypes.byref(r1)),
            "costa_relabel")
     return sigma.tolist(), r0.value, r1.value
+
+
+RELABEL = {"exact": 0, "greedy": 1}
+
+
+def costa_relabel_cost(V: np.ndarray, elem_bytes: float = 1.0, latency=None, inv_bandwidth=None,
+                       method: str = "exact"):
+    """(sigma, W(G), W(G_sigma)) under the locally-free cost (latency and
+    inv_bandwidth None) or the latency-bandwidth cost."""
+    V = np.ascontiguousarray(V, dtype=np.int64)
+    P = V.shape[0]
+    lat = None if latency is None else np.ascontiguousarray(latency, dtype=np.float64)
+    ib = None if inv_bandwidth is None else np.ascontiguousarray(inv_bandwidth, dtype=np.float64)
+    sigma = np.zeros(max(P, 1), dtype=np.int32)
+    before, after = ctypes.c_double(), ctypes.c_double()
+    _check(_lib.costa_relabel_cost(P, V.ctypes.data, elem_bytes, None if lat is None else lat.ctypes.data,
+                                   None if ib is None else ib.ctypes.data, RELABEL[method], sigma.ctypes.data,
+                                   ctypes.byref(before), ctypes.byref(after)), "costa_relabel_cost")
+    return sigma[:P].tolist(), before.value, after.value
 
 
 def _ptr_array(bufs: Sequence) -> ctypes.Array:
