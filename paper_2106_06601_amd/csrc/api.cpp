@@ -566,6 +566,36 @@ extern "C" costa_status costa_plan_stats(costa_dtype dtype, int32_t n, const cos
   return COSTA_SUCCESS;
 }
 
+namespace costa {
+namespace {
+
+// Device allocation released when it goes out of scope.
+struct DevBuf {
+  void* p = nullptr;
+  DevBuf() = default;
+  DevBuf(const DevBuf&) = delete;
+  DevBuf& operator=(const DevBuf&) = delete;
+  ~DevBuf() {
+    if (p) (void)hipFree(p);
+  }
+  hipError_t alloc(size_t n) { return hipMalloc(&p, n ? n : 1); }
+  template <typename T>
+  T* as() const {
+    return reinterpret_cast<T*>(p);
+  }
+};
+
+// Uploads `n` items of `src` into a fresh device buffer on `stream`.
+template <typename T>
+hipError_t upload(DevBuf& d, const T* src, size_t n, hipStream_t stream) {
+  hipError_t e = d.alloc(n * sizeof(T));
+  if (e != hipSuccess || n == 0) return e;
+  return hipMemcpyAsync(d.p, src, n * sizeof(T), hipMemcpyHostToDevice, stream);
+}
+
+}  // namespace
+}  // namespace costa
+
 extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, costa_op op, int64_t* V_host,
                                             hipStream_t stream) {
   const Layout* A = layout_of(A_h);
@@ -577,55 +607,87 @@ extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, 
     return fail(COSTA_ERROR_SHAPE_MISMATCH, "A is not the shape of op(B)");
   if (A->nranks != B->nranks) return fail(COSTA_ERROR_SHAPE_MISMATCH, "layouts of A and B have different P");
   const int32_t P = A->nranks;
-  std::memset(V_host, 0, sizeof(int64_t) * (size_t)P * P);
+  const size_t PP = (size_t)P * P;
+  std::memset(V_host, 0, sizeof(int64_t) * PP);
   std::vector<Interval> rows = overlay(A->rsplit, tr ? B->csplit : B->rsplit);
   std::vector<Interval> cols = overlay(A->csplit, tr ? B->rsplit : B->csplit);
   if (rows.empty() || cols.empty()) return COSTA_SUCCESS;
+  if (rows.size() > INT32_MAX || cols.size() > INT32_MAX)
+    return fail(COSTA_ERROR_NOT_SUPPORTED, "more than 2^31 overlay intervals in one dimension");
   State& S = state();
   std::lock_guard<std::mutex> lock(S.mu);
-  Interval *d_rows = nullptr, *d_cols = nullptr;
-  int32_t *d_oa = nullptr, *d_ob = nullptr;
-  unsigned long long* d_v = nullptr;
+  const bool separable = A->block_cyclic && B->block_cyclic;
+  DevBuf d_rows, d_cols, d_oa, d_ob, d_v, d_hr, d_hc;
+  std::vector<unsigned long long> zeros;
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  costa_status st = COSTA_SUCCESS;
-  auto check = [&](hipError_t e, const char* what) {
-    if (e != hipSuccess && st == COSTA_SUCCESS) st = fail(COSTA_ERROR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
-    return st == COSTA_SUCCESS;
-  };
-  if (check(hipMalloc(&d_rows, rows.size() * sizeof(Interval)), "hipMalloc") &&
-      check(hipMalloc(&d_cols, cols.size() * sizeof(Interval)), "hipMalloc") &&
-      check(hipMalloc(&d_oa, A->owner.size() * sizeof(int32_t)), "hipMalloc") &&
-      check(hipMalloc(&d_ob, B->owner.size() * sizeof(int32_t)), "hipMalloc") &&
-      check(hipMalloc(&d_v, sizeof(unsigned long long) * (size_t)P * P), "hipMalloc") &&
-      check(hipMemcpyAsync(d_rows, rows.data(), rows.size() * sizeof(Interval), hipMemcpyHostToDevice, stream), "copy") &&
-      check(hipMemcpyAsync(d_cols, cols.data(), cols.size() * sizeof(Interval), hipMemcpyHostToDevice, stream), "copy") &&
-      check(hipMemcpyAsync(d_oa, A->owner.data(), A->owner.size() * sizeof(int32_t), hipMemcpyHostToDevice, stream), "copy") &&
-      check(hipMemcpyAsync(d_ob, B->owner.data(), B->owner.size() * sizeof(int32_t), hipMemcpyHostToDevice, stream), "copy") &&
-      check(hipMemcpyAsync(d_v, V_host, sizeof(int64_t) * (size_t)P * P, hipMemcpyHostToDevice, stream), "copy")) {
-    VolumeArgs a{d_rows, (int32_t)rows.size(), d_cols, (int32_t)cols.size(), d_oa, A->nbc, d_ob, B->nbc,
-                 tr ? 1 : 0, P, d_v};
-    if (S.timing) {
-      e0 = get_event(S);
-      e1 = get_event(S);
-      if (e0 && e1) check(hipEventRecord(e0, stream), "event");
-    }
-    if (check(launch_volume(a, stream), "volume kernel")) {
-      if (S.timing && e0 && e1 && check(hipEventRecord(e1, stream), "event")) {
-        S.pending.push_back(TimingRec{COSTA_KERNEL_VOLUME, e0, e1, (int64_t)(rows.size() + cols.size()) * 24});
-        e0 = e1 = nullptr;
-      }
-      if (check(hipMemcpyAsync(V_host, d_v, sizeof(int64_t) * (size_t)P * P, hipMemcpyDeviceToHost, stream), "copy"))
-        check(hipStreamSynchronize(stream), "sync");
-    }
+  if (S.timing) {
+    e0 = get_event(S);
+    e1 = get_event(S);
   }
-  (void)hipStreamSynchronize(stream);
+  auto run = [&]() -> costa_status {
+    HIP_OR_FAIL(d_v.alloc(sizeof(int64_t) * PP));
+    if (separable) {
+      // classes of the covering blocks: process row/column of A's block and
+      // of op(B)'s block (B's process column for the rows of op(B) when
+      // transposed, and its process row for the columns)
+      const int32_t nrb = tr ? B->pcol : B->prow, ncb = tr ? B->prow : B->pcol;
+      for (Interval& v : rows) {
+        v.a %= A->prow;
+        v.b %= nrb;
+      }
+      for (Interval& v : cols) {
+        v.a %= A->pcol;
+        v.b %= ncb;
+      }
+      const size_t nh_r = (size_t)nrb * A->prow, nh_c = (size_t)ncb * A->pcol;
+      zeros.assign(std::max(nh_r, nh_c), 0ull);
+      HIP_OR_FAIL(upload(d_rows, rows.data(), rows.size(), stream));
+      HIP_OR_FAIL(upload(d_cols, cols.data(), cols.size(), stream));
+      HIP_OR_FAIL(upload(d_hr, zeros.data(), nh_r, stream));
+      HIP_OR_FAIL(upload(d_hc, zeros.data(), nh_c, stream));
+      SeparableArgs a{d_rows.as<Interval>(), (int32_t)rows.size(), d_cols.as<Interval>(), (int32_t)cols.size(),
+                      nrb, A->prow, ncb, A->pcol, d_hr.as<unsigned long long>(), d_hc.as<unsigned long long>(),
+                      A->prow, A->pcol, A->rank_order == COSTA_ROW_MAJOR ? 1 : 0, B->prow, B->pcol,
+                      B->rank_order == COSTA_ROW_MAJOR ? 1 : 0, tr ? 1 : 0, P, d_v.as<unsigned long long>()};
+      if (e0) HIP_OR_FAIL(hipEventRecord(e0, stream));
+      HIP_OR_FAIL(launch_volume_separable(a, stream));
+    } else {
+      // owner tables (block-cyclic layouts keep none: write them out here)
+      std::vector<int32_t> oa_tmp, ob_tmp;
+      auto owners = [](const Layout* L, std::vector<int32_t>& tmp) -> const std::vector<int32_t>& {
+        if (!L->block_cyclic) return L->owner;
+        tmp.resize((size_t)L->nbr * L->nbc);
+        for (int32_t bi = 0; bi < L->nbr; ++bi)
+          for (int32_t bj = 0; bj < L->nbc; ++bj) tmp[L->block(bi, bj)] = L->owner_of(bi, bj);
+        return tmp;
+      };
+      const std::vector<int32_t>& oa = owners(A, oa_tmp);
+      const std::vector<int32_t>& ob = owners(B, ob_tmp);
+      zeros.assign(PP, 0ull);
+      HIP_OR_FAIL(upload(d_rows, rows.data(), rows.size(), stream));
+      HIP_OR_FAIL(upload(d_cols, cols.data(), cols.size(), stream));
+      HIP_OR_FAIL(upload(d_oa, oa.data(), oa.size(), stream));
+      HIP_OR_FAIL(upload(d_ob, ob.data(), ob.size(), stream));
+      HIP_OR_FAIL(hipMemcpyAsync(d_v.p, zeros.data(), sizeof(int64_t) * PP, hipMemcpyHostToDevice, stream));
+      VolumeArgs a{d_rows.as<Interval>(), (int32_t)rows.size(), d_cols.as<Interval>(), (int32_t)cols.size(),
+                   d_oa.as<int32_t>(), A->nbc, d_ob.as<int32_t>(), B->nbc, tr ? 1 : 0, P,
+                   d_v.as<unsigned long long>()};
+      if (e0) HIP_OR_FAIL(hipEventRecord(e0, stream));
+      HIP_OR_FAIL(launch_volume(a, stream));
+    }
+    if (e1) {
+      HIP_OR_FAIL(hipEventRecord(e1, stream));
+      S.pending.push_back(TimingRec{COSTA_KERNEL_VOLUME, e0, e1, (int64_t)(rows.size() + cols.size()) * 24});
+      e0 = e1 = nullptr;
+    }
+    HIP_OR_FAIL(hipMemcpyAsync(V_host, d_v.p, sizeof(int64_t) * PP, hipMemcpyDeviceToHost, stream));
+    HIP_OR_FAIL(hipStreamSynchronize(stream));
+    return COSTA_SUCCESS;
+  };
+  costa_status st = run();
+  (void)hipStreamSynchronize(stream);  // device buffers are freed below
   if (e0) S.event_pool.push_back(e0);
   if (e1) S.event_pool.push_back(e1);
-  if (d_rows) (void)hipFree(d_rows);
-  if (d_cols) (void)hipFree(d_cols);
-  if (d_oa) (void)hipFree(d_oa);
-  if (d_ob) (void)hipFree(d_ob);
-  if (d_v) (void)hipFree(d_v);
   return st;
 }
 

@@ -24,10 +24,36 @@ struct Layout {
   int32_t nranks = 0;
   costa_order order = COSTA_COL_MAJOR;
   std::vector<int64_t> rsplit, csplit;  // nbr+1, nbc+1
-  std::vector<int32_t> owner;           // nbr*nbc row-major
-  std::vector<int64_t> boff, bld;       // nbr*nbc
   std::vector<int64_t> local_elems;     // per rank
+  // general grids: per block, row-major over (bi, bj)
+  std::vector<int32_t> owner;
+  std::vector<int64_t> boff, bld;
+  // block-cyclic layouts keep no per-block arrays (a 10^5 x 10^5 matrix in
+  // 1 x 1 blocks has 10^10 of them): block (bi, bj) belongs to process
+  // (bi % prow, bj % pcol) and sits in its ScaLAPACK local matrix
+  bool block_cyclic = false;
+  int32_t prow = 0, pcol = 0;
+  costa_order rank_order = COSTA_ROW_MAJOR;
+  int64_t mb = 0, nb = 0;
+  std::vector<int64_t> lrows, lcols;  // local extents per process row / column
+
   int64_t block(int32_t bi, int32_t bj) const { return (int64_t)bi * nbc + bj; }
+  int32_t owner_of(int32_t bi, int32_t bj) const {
+    if (!block_cyclic) return owner[block(bi, bj)];
+    const int32_t pr = bi % prow, pc = bj % pcol;
+    return rank_order == COSTA_ROW_MAJOR ? pr * pcol + pc : pr + pc * prow;
+  }
+  int64_t ld_of(int32_t bi, int32_t bj) const {
+    if (!block_cyclic) return bld[block(bi, bj)];
+    const int64_t ext = order == COSTA_COL_MAJOR ? lrows[bi % prow] : lcols[bj % pcol];
+    return ext > 1 ? ext : 1;
+  }
+  int64_t offset_of(int32_t bi, int32_t bj) const {
+    if (!block_cyclic) return boff[block(bi, bj)];
+    const int64_t li = (int64_t)(bi / prow) * mb, lj = (int64_t)(bj / pcol) * nb;  // local origin of the block
+    const int64_t ld = ld_of(bi, bj);
+    return order == COSTA_COL_MAJOR ? li + lj * ld : li * ld + lj;
+  }
 };
 
 // ---- grid overlay (Section 5 "Grid Overlay") -------------------------------
@@ -117,6 +143,27 @@ struct VolumeArgs {
   unsigned long long* V;
 };
 hipError_t launch_volume(const VolumeArgs& a, hipStream_t stream);
+
+// Separable volume of two block-cyclic layouts: per-dimension histograms of
+// the overlay intervals over (class in B, class in A) -- Interval::a and ::b
+// hold those classes here -- then V[s][t] as the product of a row and a
+// column histogram entry.
+struct SeparableArgs {
+  const Interval* rows;
+  int32_t K;
+  const Interval* cols;
+  int32_t L;
+  int32_t nrb, nra;  // row classes of B (for rows of op(B)) and of A
+  int32_t ncb, nca;  // column classes
+  unsigned long long* hrow;  // nrb * nra, zeroed by the caller
+  unsigned long long* hcol;  // ncb * nca, zeroed by the caller
+  int32_t prowA, pcolA, rowmajA;
+  int32_t prowB, pcolB, rowmajB;
+  int32_t transposed;
+  int32_t P;
+  unsigned long long* V;
+};
+hipError_t launch_volume_separable(const SeparableArgs& a, hipStream_t stream);
 
 // ---- relabeling (lap.cpp) --------------------------------------------------
 // Lexicographically smallest sigma maximising sum_t V[sigma[t]][t].

@@ -398,6 +398,38 @@ struct Launch {
   int32_t allow_wide;
 };
 
+// Separable volume, step 1: histogram of overlay interval lengths by (class
+// of the covering block in op(B), class of the covering block in A), for the
+// rows (blockIdx.y == 0) and the columns (blockIdx.y == 1).
+__global__ void __launch_bounds__(kThreads) costa_volume_hist(SeparableArgs a) {
+  const bool rows = blockIdx.y == 0;
+  const Interval* iv = rows ? a.rows : a.cols;
+  const int32_t n = rows ? a.K : a.L;
+  unsigned long long* h = rows ? a.hrow : a.hcol;
+  const int32_t na = rows ? a.nra : a.nca;
+  for (int32_t i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads) {
+    const Interval v = iv[i];
+    atomicAdd(&h[(int64_t)v.b * na + v.a], (unsigned long long)v.len);
+  }
+}
+
+// Separable volume, step 2: V[s][t] = hrow[row class of s][row class of t] *
+// hcol[col class of s][col class of t] (for op T the row overlay of op(B)
+// runs over B's process columns and the column overlay over its rows).
+__global__ void __launch_bounds__(kThreads) costa_volume_outer(SeparableArgs a) {
+  const int32_t PP = a.P * a.P;
+  for (int32_t k = blockIdx.x * kThreads + threadIdx.x; k < PP; k += gridDim.x * kThreads) {
+    const int32_t s = k / a.P, t = k % a.P;
+    const int32_t prA = a.rowmajA ? t / a.pcolA : t % a.prowA;
+    const int32_t pcA = a.rowmajA ? t % a.pcolA : t / a.prowA;
+    const int32_t prB = a.rowmajB ? s / a.pcolB : s % a.prowB;
+    const int32_t pcB = a.rowmajB ? s % a.pcolB : s / a.prowB;
+    const int32_t rb = a.transposed ? pcB : prB;  // class of s in the row overlay
+    const int32_t cb = a.transposed ? prB : pcB;  // class of s in the column overlay
+    a.V[k] = a.hrow[(int64_t)rb * a.nra + prA] * a.hcol[(int64_t)cb * a.nca + pcA];
+  }
+}
+
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 hipError_t go(const Launch& l) {
   hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
@@ -448,6 +480,23 @@ hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spe
     case COSTA_C64: return launch_typed<float, true>(kind, spec, l);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_volume_separable(const SeparableArgs& a, hipStream_t stream) {
+  const int32_t nmax = a.K > a.L ? a.K : a.L;
+  if (nmax > 0) {
+    unsigned gx = (unsigned)((nmax + kThreads - 1) / kThreads);
+    if (gx > 1024) gx = 1024;
+    hipLaunchKernelGGL(costa_volume_hist, dim3(gx, 2), dim3(kThreads), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int32_t PP = a.P * a.P;
+  unsigned gx = (unsigned)((PP + kThreads - 1) / kThreads);
+  if (gx > 1024) gx = 1024;
+  if (gx == 0) return hipSuccess;
+  hipLaunchKernelGGL(costa_volume_outer, dim3(gx), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_volume(const VolumeArgs& a, hipStream_t stream) {

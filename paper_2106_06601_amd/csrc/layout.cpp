@@ -158,34 +158,22 @@ extern "C" costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t 
   L.csplit.resize(nbc + 1);
   for (int32_t k = 0; k <= nbc; ++k) L.csplit[k] = std::min<int64_t>((int64_t)k * nb, ncols);
   // local extents of each process row / column: the sum of the blocks it is dealt
-  std::vector<int64_t> lrows(prow, 0), lcols(pcol, 0);
-  for (int32_t bi = 0; bi < nbr; ++bi) lrows[bi % prow] += L.rsplit[bi + 1] - L.rsplit[bi];
-  for (int32_t bj = 0; bj < nbc; ++bj) lcols[bj % pcol] += L.csplit[bj + 1] - L.csplit[bj];
-  int64_t nblocks = (int64_t)nbr * nbc;
-  L.owner.resize(nblocks);
-  L.boff.resize(nblocks);
-  L.bld.resize(nblocks);
-  for (int32_t bi = 0; bi < nbr; ++bi)
-    for (int32_t bj = 0; bj < nbc; ++bj) {
-      int32_t pr = bi % prow, pc = bj % pcol;
-      int64_t b = L.block(bi, bj);
-      L.owner[b] = rank_order == COSTA_ROW_MAJOR ? pr * pcol + pc : pr + pc * prow;
-      int64_t li = (int64_t)(bi / prow) * mb, lj = (int64_t)(bj / pcol) * nb;  // local origin of the block
-      if (block_order == COSTA_COL_MAJOR) {
-        int64_t ld = std::max<int64_t>(1, lrows[pr]);
-        L.bld[b] = ld;
-        L.boff[b] = li + lj * ld;
-      } else {
-        int64_t ld = std::max<int64_t>(1, lcols[pc]);
-        L.bld[b] = ld;
-        L.boff[b] = li * ld + lj;
-      }
-    }
-  costa_status st = finish_layout(L);
-  if (st != COSTA_SUCCESS) {
-    delete h;
-    return st;
-  }
+  L.lrows.assign(prow, 0);
+  L.lcols.assign(pcol, 0);
+  for (int32_t bi = 0; bi < nbr; ++bi) L.lrows[bi % prow] += L.rsplit[bi + 1] - L.rsplit[bi];
+  for (int32_t bj = 0; bj < nbc; ++bj) L.lcols[bj % pcol] += L.csplit[bj + 1] - L.csplit[bj];
+  L.mb = mb;
+  L.nb = nb;
+  L.block_cyclic = true;
+  L.prow = prow;
+  L.pcol = pcol;
+  L.rank_order = rank_order;
+  // every rank holds its local matrix of lrows x lcols elements
+  L.local_elems.assign(L.nranks, 0);
+  for (int32_t pr = 0; pr < prow; ++pr)
+    for (int32_t pc = 0; pc < pcol; ++pc)
+      L.local_elems[rank_order == COSTA_ROW_MAJOR ? pr * pcol + pc : pr + pc * prow] = L.lrows[pr] * L.lcols[pc];
+  L.id = g_next_id.fetch_add(1);
   *out = h;
   return COSTA_SUCCESS;
 }
@@ -202,10 +190,9 @@ extern "C" costa_status costa_layout_block(costa_layout layout, int32_t bi, int3
   if (!layout) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
   const Layout& L = layout->L;
   if (bi < 0 || bi >= L.nbr || bj < 0 || bj >= L.nbc) return fail(COSTA_ERROR_INVALID_VALUE, "block out of range");
-  int64_t b = L.block(bi, bj);
-  if (owner) *owner = L.owner[b];
-  if (offset) *offset = L.boff[b];
-  if (ld) *ld = L.bld[b];
+  if (owner) *owner = L.owner_of(bi, bj);
+  if (offset) *offset = L.offset_of(bi, bj);
+  if (ld) *ld = L.ld_of(bi, bj);
   return COSTA_SUCCESS;
 }
 

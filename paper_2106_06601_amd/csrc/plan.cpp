@@ -93,22 +93,20 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
       const Interval& ri = a_col ? xi : yi;  // row interval of this overlay block
       const Interval& ci = a_col ? yi : xi;  // column interval
       // destination block and label
-      const int64_t ba = A.block(ri.a, ci.a);
-      const int32_t t = A.owner[ba];
+      const int32_t t = A.owner_of(ri.a, ci.a);
       const int32_t r = sigma.empty() ? t : sigma[t];
       const int64_t pi = ri.start - A.rsplit[ri.a], pj = ci.start - A.csplit[ci.a];
-      const int64_t lda = A.bld[ba];
-      const int64_t dst_off = A.boff[ba] + (a_col ? pi + pj * lda : pi * lda + pj);
+      const int64_t lda = A.ld_of(ri.a, ci.a);
+      const int64_t dst_off = A.offset_of(ri.a, ci.a) + (a_col ? pi + pj * lda : pi * lda + pj);
       // source block: op(B) block (ri.b, ci.b) is B block (ci.b, ri.b) for T/C
       const int32_t bi = tr ? ci.b : ri.b, bj = tr ? ri.b : ci.b;
-      const int64_t bb = B.block(bi, bj);
-      const int32_t s = B.owner[bb];
-      const int64_t ldb = B.bld[bb];
+      const int32_t s = B.owner_of(bi, bj);
+      const int64_t ldb = B.ld_of(bi, bj);
       // B element of A's (i, j): B(i, j) for N, B(j, i) for T/C
       const int64_t qrow = tr ? ci.start - B.rsplit[bi] : ri.start - B.rsplit[bi];
       const int64_t qcol = tr ? ri.start - B.csplit[bj] : ci.start - B.csplit[bj];
       const int64_t s_brow = b_col ? 1 : ldb, s_bcol = b_col ? ldb : 1;  // strides of B's row / col index
-      const int64_t src_off = B.boff[bb] + qrow * s_brow + qcol * s_bcol;
+      const int64_t src_off = B.offset_of(bi, bj) + qrow * s_brow + qcol * s_bcol;
       const int64_t s_i = tr ? s_bcol : s_brow;  // stride along A's row index i
       const int64_t s_j = tr ? s_brow : s_bcol;  // stride along A's column index j
       const int64_t sx = a_col ? s_i : s_j, sy = a_col ? s_j : s_i;

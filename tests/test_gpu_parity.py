@@ -283,3 +283,56 @@ def test_timing_counters():
     st = C.costa_plan_stats(w.dtype, descs, case.sigma)
     assert t["pack"]["bytes"] == 3 * st["pack_bytes"]
     assert t["unpack"]["bytes"] == 3 * (st["unpack_bytes"] + st["direct_bytes"])
+
+
+# ---------------------------------------------------------------------------
+# separable volume path and the Section 7.2 relabeling sweep
+# ---------------------------------------------------------------------------
+def _as_general(spec):
+    """The same block-cyclic layout expressed as a general grid with explicit
+    per-block storage (so costa_volume_matrix takes the general kernel)."""
+    L = C.layout_from_spec(spec)
+    nbr, nbc = L.nbr, L.nbc
+    rs = np.minimum(np.arange(nbr + 1, dtype=np.int64) * spec.mb, spec.nrows)
+    cs = np.minimum(np.arange(nbc + 1, dtype=np.int64) * spec.nb, spec.ncols)
+    blocks = [C.costa_layout_block(L.handle, bi, bj) for bi in range(nbr) for bj in range(nbc)]
+    owners = [b[0] for b in blocks]
+    return C.Layout.general(spec.nrows, spec.ncols, rs, cs, owners, spec.nranks, spec.block_order,
+                            [b[1] for b in blocks], [b[2] for b in blocks])
+
+
+@pytest.mark.parametrize("name", ["reshuffle_transpose_1k", "blocksize_change_16k", "scaled_transpose_20k",
+                                  "rpa_batched_tall_skinny"])
+def test_separable_volume_equals_general_kernel(name):
+    _say(f"separable vs general volume {name}")
+    w = synth.workload(name, "small")
+    for it in (w.items[0], w.items[-1]):
+        V_sep = C.costa_volume_matrix(C.layout_from_spec(it.A), C.layout_from_spec(it.B), it.op)
+        V_gen = C.costa_volume_matrix(_as_general(it.A), _as_general(it.B), it.op)
+        assert np.array_equal(V_sep, V_gen)
+        assert np.array_equal(V_sep, oracle.volume(oracle.OLayout(it.A), oracle.OLayout(it.B), it.op))
+
+
+def test_bench2_sweep_volumes_and_relabeling():
+    """Section 7.2: 10^5 x 10^5 on a 10 x 10 grid, row-major ranks initially,
+    column-major finally, target blocks 10^4, source blocks varied.  Equal
+    blocks: relabeling removes all remote volume (the paper's printed point)."""
+    import json
+    import os
+    from scipy.optimize import linear_sum_assignment
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "bench2_equal_blocks.json")))
+    n, p = g["matrix"][0], g["grid"][0]
+    A = BC(n, n, g["target"]["block"], g["target"]["block"], p, p, g["target"]["rank_order"], "col")
+    LA = C.layout_from_spec(A)
+    for b in (10000, 5000, 3000, 1000, 7, 1):
+        _say(f"sweep source block {b}")
+        B = BC(n, n, b, b, p, p, g["source"]["rank_order"], "col")
+        V = C.costa_volume_matrix(LA, C.layout_from_spec(B), "N")
+        assert np.array_equal(V, oracle.volume_separable(A, B, "N"))
+        sigma, kept_id, kept = C.costa_relabel(V)
+        r, c = linear_sum_assignment(V.astype(np.float64), maximize=True)
+        assert kept == int(V[r, c].sum())
+        total = n * n
+        reduction = 100.0 * (kept - kept_id) / (total - kept_id)
+        if b == g["source"]["block"]:
+            assert kept == total and round(reduction) == g["volume_reduction_percent"]
