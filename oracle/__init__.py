@@ -7,8 +7,10 @@ shares no code with it (the only common piece is the seeded input generator of
 
 Contents
 --------
-* ``liboracle.so`` (``costa_oracle.c``): storage maps, element-by-element
-  transform, brute-force volume matrix, expected values at sampled points.
+* ``liboracle.so`` (``costa_oracle.c``): storage maps (general grids,
+  block-cyclic layouts and ScaLAPACK descriptors), element-by-element
+  transform of whole matrices or of windows (submatrices), brute-force volume
+  matrix, expected values at sampled points.
 * Relabeling (Section 4): the communication cost W(G_sigma) of the relabeled
   graph computed from its definition, the relabeling gain delta (eq:delta)
   computed from its definition, and the communication-optimal relabeling
@@ -62,6 +64,7 @@ class _OLayout(ctypes.Structure):
         ("nbr", ctypes.c_int32), ("nbc", ctypes.c_int32),
         ("rsplit", ctypes.c_void_p), ("csplit", ctypes.c_void_p), ("owners", ctypes.c_void_p),
         ("boff", ctypes.c_void_p), ("bld", ctypes.c_void_p),
+        ("rsrc", ctypes.c_int32), ("csrc", ctypes.c_int32), ("lld", ctypes.c_int64),
     ]
 
 
@@ -86,6 +89,14 @@ def lib():
         L.oracle_expect_at.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, P, P, ctypes.c_uint64,
                                        ctypes.c_uint32, ctypes.c_int64, P, P, P, P, P]
         L.oracle_fill.argtypes = [ctypes.c_int, P, ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64]
+        i64 = ctypes.c_int64
+        L.oracle_volume_window.argtypes = [P, i64, i64, P, i64, i64, i64, i64, ctypes.c_int, P]
+        L.oracle_numroc.argtypes = [i64, i64, i64, i64, i64]
+        L.oracle_numroc.restype = i64
+        L.oracle_transform_window.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, P, i64, i64, P, P, i64, i64, i64,
+                                              P, i64, i64]
+        L.oracle_expect_at_window.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, i64, i64, P, i64, i64, P,
+                                              ctypes.c_uint64, ctypes.c_uint32, i64, P, P, P, P, P]
         _lib = L
     return _lib
 
@@ -101,13 +112,20 @@ class OLayout:
         self.spec = spec
         s = _OLayout()
         s.nrows, s.ncols = spec.nrows, spec.ncols
-        s.row_major = 1 if spec.block_order == "row" else 0
+        s.row_major = 1 if getattr(spec, "block_order", "col") == "row" else 0
         s.nranks = spec.nranks
         self._keep = []
         if spec.kind == "block_cyclic":
             s.kind = 0
             s.mb, s.nb, s.prow, s.pcol = spec.mb, spec.nb, spec.prow, spec.pcol
             s.rank_row_major = 1 if spec.rank_order == "row" else 0
+        elif spec.kind == "scalapack":
+            # a ScaLAPACK descriptor: block-cyclic, column-major local matrices
+            s.kind = 0
+            s.row_major = 0
+            s.mb, s.nb, s.prow, s.pcol = spec.mb, spec.nb, spec.nprow, spec.npcol
+            s.rank_row_major = 1 if spec.rank_order == "row" else 0
+            s.rsrc, s.csrc, s.lld = spec.rsrc, spec.csrc, spec.lld
         else:
             s.kind = 1
             rs = np.asarray(spec.row_splits, dtype=np.int64)
@@ -151,6 +169,17 @@ def volume(A: OLayout, B: OLayout, op: str) -> np.ndarray:
     P = A.nranks
     V = np.zeros((P, P), dtype=np.int64)
     if lib().oracle_volume(A.ref, B.ref, OPS[op], _ptr(V)) != 0:
+        raise ValueError("layouts live on different process counts")
+    return V
+
+
+def volume_window(A: OLayout, ia: int, ja: int, B: OLayout, ib: int, jb: int, m: int, n: int,
+                  op: str) -> np.ndarray:
+    """V[s, t] of the m x n window of A at 0-based (ia, ja) receiving op of the
+    window of B at (ib, jb), by brute-force counting."""
+    P = A.nranks
+    V = np.zeros((P, P), dtype=np.int64)
+    if lib().oracle_volume_window(A.ref, ia, ja, B.ref, ib, jb, m, n, OPS[op], _ptr(V)) != 0:
         raise ValueError("layouts live on different process counts")
     return V
 
@@ -233,6 +262,70 @@ def expect_at(dtype: str, op: str, alpha, beta, A: OLayout, B: OLayout, sigma, s
     else:
         v = val[:, 0]
     return rank, off, v.astype(NUMPY[dtype])
+
+
+def transform_window(dtype: str, op: str, alpha, beta, A: OLayout, A_bufs: Sequence[np.ndarray], ia: int, ja: int,
+                     B: OLayout, B_bufs: Sequence[np.ndarray], ib: int, jb: int, m: int, n: int,
+                     sigma: Optional[Sequence[int]] = None) -> None:
+    """The m x n window of A at 0-based (ia, ja) receives alpha*op(window of B
+    at (ib, jb)) + beta*(itself), in place on the host buffers; the rest of A is
+    left alone (Section 5, a submatrix by truncated splits)."""
+    P = A.nranks
+    assert len(A_bufs) == P and len(B_bufs) == P
+    for a in list(A_bufs) + list(B_bufs):
+        assert a.dtype == NUMPY[dtype] and a.flags["C_CONTIGUOUS"]
+    Ap = (ctypes.c_void_p * P)(*[_ptr(a) for a in A_bufs])
+    Bp = (ctypes.c_void_p * P)(*[_ptr(b) for b in B_bufs])
+    sg = None if sigma is None else np.ascontiguousarray(sigma, dtype=np.int32)
+    al, be = _scalar2(alpha), _scalar2(beta)
+    rc = lib().oracle_transform_window(DTYPES[dtype], OPS[op], _ptr(al), _ptr(be), A.ref, Ap, ia, ja, B.ref, Bp,
+                                       ib, jb, n, None if sg is None else _ptr(sg), 0, m)
+    if rc != 0:
+        raise ValueError("layouts live on different process counts")
+
+
+def expect_at_window(dtype: str, op: str, alpha, beta, A: OLayout, ia: int, ja: int, B: OLayout, ib: int, jb: int,
+                     seed: int, item: int, rows: np.ndarray, cols: np.ndarray):
+    """expect_at for the window form of transform_window; rows and cols are
+    window coordinates."""
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    n = rows.size
+    rank = np.zeros(n, dtype=np.int32)
+    off = np.zeros(n, dtype=np.int64)
+    val = np.zeros(2 * n, dtype=np.float64)
+    al, be = _scalar2(alpha), _scalar2(beta)
+    lib().oracle_expect_at_window(DTYPES[dtype], OPS[op], _ptr(al), _ptr(be), A.ref, ia, ja, B.ref, ib, jb, None,
+                                  seed, item, n, _ptr(rows), _ptr(cols), _ptr(rank), _ptr(off), _ptr(val))
+    val = val.reshape(n, 2)
+    v = val[:, 0] + 1j * val[:, 1] if dtype in ("c128", "c64") else val[:, 0]
+    return rank, off, v.astype(NUMPY[dtype])
+
+
+# --------------------------------------------------------------------------
+# ScaLAPACK-style calls (pxgemr2d, pxtran, pxtranu, pxtranc)
+# --------------------------------------------------------------------------
+def numroc(n: int, nb: int, iproc: int, isrc: int, nprocs: int) -> int:
+    """Rows (or columns) of an n-long dimension in blocks of nb that process
+    iproc holds when dealing starts at process isrc (ScaLAPACK NUMROC)."""
+    return int(lib().oracle_numroc(n, nb, iproc, isrc, nprocs))
+
+
+def scalapack_call(call, A_bufs: Sequence[np.ndarray], C_bufs: Sequence[np.ndarray]) -> None:
+    """Runs a ScaLAPACK-style call (a ``synth.ScaLapackCall``) on host buffers:
+    gemr2d copies the m x n window of A at 1-based (ia, ja) into the window of
+    C at (ic, jc); tran / tranu put beta*sub(C) + alpha*sub(A)^T there, tranc
+    the conjugate transpose (sub(A) is then n x m)."""
+    if call.routine == "gemr2d":
+        op, alpha, beta = "N", 1.0, 0.0
+    elif call.routine in ("tran", "tranu"):
+        op, alpha, beta = "T", call.alpha, call.beta
+    elif call.routine == "tranc":
+        op, alpha, beta = "C", call.alpha, call.beta
+    else:
+        raise ValueError(call.routine)
+    transform_window(call.dtype, op, alpha, beta, OLayout(call.C), C_bufs, call.ic - 1, call.jc - 1,
+                     OLayout(call.A), A_bufs, call.ia - 1, call.ja - 1, call.m, call.n)
 
 
 def fill(dtype: str, arr: np.ndarray, seed: int, strm: int) -> None:

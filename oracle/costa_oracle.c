@@ -31,8 +31,12 @@
  *     Algorithm 3); otherwise t1 = alpha*b, t2 = beta*a, result t1 + t2, each
  *     operation rounded on its own (built with -ffp-contract=off), complex
  *     products as (ar*br - ai*bi, ar*bi + ai*br);
- *   - block-cyclic local storage follows the ScaLAPACK convention (first
- *     process row and column 0; local rows from NUMROC);
+ *   - block-cyclic local storage follows the ScaLAPACK convention (local
+ *     rows from NUMROC, first block row/column on process row/column
+ *     rsrc/csrc, leading dimension lld or the local extent);
+ *   - a window (submatrix) keeps every element where the full layout stores
+ *     it: taking a submatrix only truncates the splits (Section 5, "Scale and
+ *     Transpose/Conjugate");
  *   - default storage of a general grid: a rank stores its blocks one after
  *     another in row-major order of (block row, block col), each block packed
  *     with its own leading extent.
@@ -64,17 +68,30 @@ typedef struct {
   const int32_t* owners;  /* nbr*nbc, row-major over (bi, bj) */
   const int64_t* boff;    /* nbr*nbc element offsets inside the owner's buffer */
   const int64_t* bld;     /* nbr*nbc leading dimensions */
+  /* block-cyclic, ScaLAPACK descriptor extras: process row/column holding the
+   * first block row/column, and the local leading dimension (0: the local
+   * extent from NUMROC, at least 1) */
+  int32_t rsrc, csrc;
+  int64_t lld;
 } olayout;
 
-/* ScaLAPACK NUMROC with the first process at 0: how many of n rows (or cols),
- * dealt in blocks of nb over nprocs processes, process iproc holds. */
-static int64_t numroc(int64_t n, int64_t nb, int64_t iproc, int64_t nprocs) {
+/* ScaLAPACK NUMROC: how many of n rows (or cols), dealt in blocks of nb over
+ * nprocs processes starting with process isrc, process iproc holds.  Its
+ * distance from isrc along the cycle decides: the first n/nb full blocks go
+ * round (nblocks/nprocs) full cycles, the next (nblocks mod nprocs) processes
+ * get one more full block, and the one after them the partial last block. */
+static int64_t numroc(int64_t n, int64_t nb, int64_t iproc, int64_t isrc, int64_t nprocs) {
+  int64_t dist = (iproc - isrc + nprocs) % nprocs;
   int64_t nblocks = n / nb;
   int64_t num = (nblocks / nprocs) * nb;
   int64_t extra = nblocks % nprocs;
-  if (iproc < extra) num += nb;
-  else if (iproc == extra) num += n % nb;
+  if (dist < extra) num += nb;
+  else if (dist == extra) num += n % nb;
   return num;
+}
+
+int64_t oracle_numroc(int64_t n, int64_t nb, int64_t iproc, int64_t isrc, int64_t nprocs) {
+  return numroc(n, nb, iproc, isrc, nprocs);
 }
 
 /* Index k of the split interval [s[k], s[k+1]) containing x (binary search). */
@@ -91,18 +108,21 @@ static int32_t interval_of(const int64_t* s, int32_t nb, int64_t x) {
 /* Owner rank and local element offset of global element (i, j). */
 static void locate(const olayout* L, int64_t i, int64_t j, int32_t* rank, int64_t* off) {
   if (L->kind == O_BLOCK_CYCLIC) {
-    int64_t pr = (i / L->mb) % L->prow;
-    int64_t pc = (j / L->nb) % L->pcol;
+    /* block row i/mb lives on process row (rsrc + i/mb) mod prow, as the
+     * (i/(mb*prow))-th block of that process row (ScaLAPACK INDXG2P and
+     * INDXG2L); likewise for columns */
+    int64_t pr = (i / L->mb + L->rsrc) % L->prow;
+    int64_t pc = (j / L->nb + L->csrc) % L->pcol;
     *rank = (int32_t)(L->rank_row_major ? pr * L->pcol + pc : pr + pc * L->prow);
     int64_t li = (i / (L->mb * L->prow)) * L->mb + i % L->mb;
     int64_t lj = (j / (L->nb * L->pcol)) * L->nb + j % L->nb;
     if (L->row_major) {
-      int64_t lc = numroc(L->ncols, L->nb, pc, L->pcol);
-      int64_t ld = lc > 1 ? lc : 1;
+      int64_t lc = numroc(L->ncols, L->nb, pc, L->csrc, L->pcol);
+      int64_t ld = L->lld ? L->lld : (lc > 1 ? lc : 1);
       *off = li * ld + lj;
     } else {
-      int64_t lr = numroc(L->nrows, L->mb, pr, L->prow);
-      int64_t ld = lr > 1 ? lr : 1;
+      int64_t lr = numroc(L->nrows, L->mb, pr, L->rsrc, L->prow);
+      int64_t ld = L->lld ? L->lld : (lr > 1 ? lr : 1);
       *off = li + lj * ld;
     }
   } else {
@@ -138,9 +158,12 @@ int64_t oracle_local_elems(const olayout* L, int32_t rank) {
   if (L->kind == O_BLOCK_CYCLIC) {
     int64_t pr = L->rank_row_major ? rank / L->pcol : rank % L->prow;
     int64_t pc = L->rank_row_major ? rank % L->pcol : rank / L->prow;
-    int64_t lr = numroc(L->nrows, L->mb, pr, L->prow);
-    int64_t lc = numroc(L->ncols, L->nb, pc, L->pcol);
-    return lr * lc;
+    int64_t lr = numroc(L->nrows, L->mb, pr, L->rsrc, L->prow);
+    int64_t lc = numroc(L->ncols, L->nb, pc, L->csrc, L->pcol);
+    if (lr == 0 || lc == 0) return 0;
+    /* one past the last local element */
+    if (L->row_major) return (lr - 1) * (L->lld ? L->lld : lc) + lc;
+    return (lc - 1) * (L->lld ? L->lld : lr) + lr;
   }
   int64_t need = 0;
   for (int64_t b = 0; b < (int64_t)L->nbr * L->nbc; ++b) {
@@ -166,22 +189,29 @@ static void source_of(int op, int64_t i, int64_t j, int64_t* bi, int64_t* bj) {
 }
 
 /* Volume matrix by brute-force element counting (Section 2 volume, Algorithm 2
- * packages): V[s*P + t] += 1 for every element (i, j) of A whose source
- * op^-1(i, j) is owned by s in L(B) and which label t owns in L(A). */
-int oracle_volume(const olayout* A, const olayout* B, int op, int64_t* V) {
+ * packages): V[s*P + t] += 1 for every element (i, j) of the m x n window of A
+ * at (ia, ja) whose source, element op^-1(i, j) of the window of B at
+ * (ib, jb), is owned by s in L(B), and which label t owns in L(A). */
+int oracle_volume_window(const olayout* A, int64_t ia, int64_t ja, const olayout* B, int64_t ib, int64_t jb,
+                         int64_t m, int64_t n, int op, int64_t* V) {
   int32_t P = A->nranks;
   if (B->nranks != P) return 1;
   memset(V, 0, sizeof(int64_t) * (size_t)P * (size_t)P);
-  for (int64_t i = 0; i < A->nrows; ++i)
-    for (int64_t j = 0; j < A->ncols; ++j) {
+  for (int64_t i = 0; i < m; ++i)
+    for (int64_t j = 0; j < n; ++j) {
       int32_t t, s;
       int64_t oa, ob, bi, bj;
-      locate(A, i, j, &t, &oa);
+      locate(A, ia + i, ja + j, &t, &oa);
       source_of(op, i, j, &bi, &bj);
-      locate(B, bi, bj, &s, &ob);
+      locate(B, ib + bi, jb + bj, &s, &ob);
       V[(int64_t)s * P + t] += 1;
     }
   return 0;
+}
+
+/* The volume matrix of the whole matrices. */
+int oracle_volume(const olayout* A, const olayout* B, int op, int64_t* V) {
+  return oracle_volume_window(A, 0, 0, B, 0, 0, A->nrows, A->ncols, op, V);
 }
 
 /* ---- element arithmetic, literally as equation (eq:costa) ---- */
@@ -243,25 +273,33 @@ static void combine32(int cpx, const float* alpha, const float* beta, const floa
   out[0] = t1 + t2;
 }
 
-/* A <- alpha*op(B) + beta*A for the rows [row_begin, row_end) of A.
- * alpha, beta: {re, im} (im ignored for real types).  sigma may be NULL
- * (identity).  A_local[r] / B_local[s]: host buffers of physical ranks. */
-int oracle_transform(int dtype, int op, const double* alpha, const double* beta, const olayout* A,
-                     void* const* A_local, const olayout* B, const void* const* B_local, const int32_t* sigma,
-                     int64_t row_begin, int64_t row_end) {
+/* A window of A receives a window of op(B) (Section 5, "Scale and
+ * Transpose/Conjugate": a submatrix is taken by truncating the splits, which
+ * leaves every element where the full layout stores it):
+ *     A(ia + i, ja + j) <- alpha * op(B~)(i, j) + beta * A(ia + i, ja + j),
+ * for window rows i in [row_begin, row_end) and columns j in [0, n), where
+ * B~ is the window of B starting at (ib, jb): op(B~)(i, j) = B(ib + i, jb + j)
+ * for N, and B(ib + j, jb + i) for T and C.  Elements of A outside the window
+ * are not touched.  alpha, beta: {re, im} (im ignored for real types).  sigma
+ * may be NULL (identity).  A_local[r] / B_local[s]: host buffers of physical
+ * ranks. */
+int oracle_transform_window(int dtype, int op, const double* alpha, const double* beta, const olayout* A,
+                            void* const* A_local, int64_t ia, int64_t ja, const olayout* B,
+                            const void* const* B_local, int64_t ib, int64_t jb, int64_t n, const int32_t* sigma,
+                            int64_t row_begin, int64_t row_end) {
   int cpx = dtype == O_C128 || dtype == O_C64;
   cplx al = {alpha[0], cpx ? alpha[1] : 0.0}, be = {beta[0], cpx ? beta[1] : 0.0};
   float al32[2] = {(float)alpha[0], cpx ? (float)alpha[1] : 0.0f};
   float be32[2] = {(float)beta[0], cpx ? (float)beta[1] : 0.0f};
   if (A->nranks != B->nranks) return 1;
   for (int64_t i = row_begin; i < row_end; ++i)
-    for (int64_t j = 0; j < A->ncols; ++j) {
+    for (int64_t j = 0; j < n; ++j) {
       int32_t t, s;
       int64_t oa, ob, bi, bj;
-      locate(A, i, j, &t, &oa);
+      locate(A, ia + i, ja + j, &t, &oa);
       int32_t r = sigma ? sigma[t] : t;
       source_of(op, i, j, &bi, &bj);
-      locate(B, bi, bj, &s, &ob);
+      locate(B, ib + bi, jb + bj, &s, &ob);
       if (dtype == O_F64 || dtype == O_C128) {
         const double* src = (const double*)B_local[s] + (cpx ? 2 * ob : ob);
         double* dst = (double*)A_local[r] + (cpx ? 2 * oa : oa);
@@ -285,23 +323,34 @@ int oracle_transform(int dtype, int op, const double* alpha, const double* beta,
   return 0;
 }
 
+/* A <- alpha*op(B) + beta*A for the rows [row_begin, row_end) of A: the
+ * window that is all of A and all of B. */
+int oracle_transform(int dtype, int op, const double* alpha, const double* beta, const olayout* A,
+                     void* const* A_local, const olayout* B, const void* const* B_local, const int32_t* sigma,
+                     int64_t row_begin, int64_t row_end) {
+  return oracle_transform_window(dtype, op, alpha, beta, A, A_local, 0, 0, B, B_local, 0, 0, A->ncols, sigma,
+                                 row_begin, row_end);
+}
+
 /* Expected final A at sampled points, for inputs made by the seeded generator
  * (B of physical rank s: stream(B, item, s); initial A of physical rank r:
  * stream(A, item, r)).  out_val holds 2 doubles per point ({re, im}; for f32
  * and c64 the float values widened exactly).  Also returns where the point
- * lives: physical rank and element offset. */
-int oracle_expect_at(int dtype, int op, const double* alpha, const double* beta, const olayout* A, const olayout* B,
-                     const int32_t* sigma, uint64_t seed, uint32_t item, int64_t n, const int64_t* rows,
-                     const int64_t* cols, int32_t* out_rank, int64_t* out_off, double* out_val) {
+ * lives: physical rank and element offset.  Points are given in the window
+ * coordinates of oracle_transform_window. */
+int oracle_expect_at_window(int dtype, int op, const double* alpha, const double* beta, const olayout* A,
+                            int64_t ia, int64_t ja, const olayout* B, int64_t ib, int64_t jb, const int32_t* sigma,
+                            uint64_t seed, uint32_t item, int64_t n, const int64_t* rows, const int64_t* cols,
+                            int32_t* out_rank, int64_t* out_off, double* out_val) {
   int cpx = dtype == O_C128 || dtype == O_C64;
   int beta_zero = beta[0] == 0.0 && (!cpx || beta[1] == 0.0);
   for (int64_t k = 0; k < n; ++k) {
     int32_t t, s;
     int64_t oa, ob, bi, bj;
-    locate(A, rows[k], cols[k], &t, &oa);
+    locate(A, ia + rows[k], ja + cols[k], &t, &oa);
     int32_t r = sigma ? sigma[t] : t;
     source_of(op, rows[k], cols[k], &bi, &bj);
-    locate(B, bi, bj, &s, &ob);
+    locate(B, ib + bi, jb + bj, &s, &ob);
     uint64_t sb = synth_stream(SYNTH_ROLE_B, item, (uint32_t)s), sa = synth_stream(SYNTH_ROLE_A, item, (uint32_t)r);
     out_rank[k] = r;
     out_off[k] = oa;
@@ -335,6 +384,13 @@ int oracle_expect_at(int dtype, int op, const double* alpha, const double* beta,
     }
   }
   return 0;
+}
+
+int oracle_expect_at(int dtype, int op, const double* alpha, const double* beta, const olayout* A, const olayout* B,
+                     const int32_t* sigma, uint64_t seed, uint32_t item, int64_t n, const int64_t* rows,
+                     const int64_t* cols, int32_t* out_rank, int64_t* out_off, double* out_val) {
+  return oracle_expect_at_window(dtype, op, alpha, beta, A, 0, 0, B, 0, 0, sigma, seed, item, n, rows, cols,
+                                 out_rank, out_off, out_val);
 }
 
 /* Host fill of a buffer with the generator (same values as the device fill). */

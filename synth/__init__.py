@@ -202,6 +202,64 @@ class BlockCyclic:
 
 
 @dataclass
+class ScaLapack:
+    """A ScaLAPACK array descriptor (DTYPE_ = 1) on a BLACS-style process grid.
+
+    m x n global matrix in mb x nb blocks; the first block row and column live
+    on process row rsrc and process column csrc; every rank stores its local
+    matrix column-major with leading dimension lld.  rank_order 'row': rank =
+    pr * npcol + pc; 'col': rank = pr + pc * nprow.
+    """
+    m: int
+    n: int
+    mb: int
+    nb: int
+    rsrc: int
+    csrc: int
+    lld: int
+    nprow: int
+    npcol: int
+    rank_order: str = "row"
+    kind: str = "scalapack"
+
+    @property
+    def nranks(self) -> int:
+        return self.nprow * self.npcol
+
+    @property
+    def nrows(self) -> int:
+        return self.m
+
+    @property
+    def ncols(self) -> int:
+        return self.n
+
+    def desc(self) -> List[int]:
+        """The nine descriptor entries (DTYPE_, CTXT_, M_, N_, MB_, NB_, RSRC_, CSRC_, LLD_)."""
+        return [1, 0, self.m, self.n, self.mb, self.nb, self.rsrc, self.csrc, self.lld]
+
+
+@dataclass
+class ScaLapackCall:
+    """One ScaLAPACK-style call: routine 'gemr2d' (sub(C) = sub(A)), 'tran' /
+    'tranu' (sub(C) = beta sub(C) + alpha sub(A)^T) or 'tranc' (conjugate
+    transpose).  sub(C) is the m x n window of C at 1-based (ic, jc); sub(A)
+    the m x n (gemr2d) or n x m (tran*) window of A at (ia, ja)."""
+    routine: str
+    dtype: str
+    m: int
+    n: int
+    alpha: complex
+    beta: complex
+    A: ScaLapack
+    ia: int
+    ja: int
+    C: ScaLapack
+    ic: int
+    jc: int
+
+
+@dataclass
 class General:
     """Arbitrary grid: splits, owners (row-major over blocks), block storage order.
 
