@@ -189,6 +189,8 @@ def main():
                     help="before warm-up, run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--relabel-report", action="store_true",
                     help="print the relabeling comparison of every workload instead of the throughput line")
+    ap.add_argument("--scalapack", metavar="NAME", choices=["pdgemr2d_16k", "pdtran_16k", "pztranc_8k"],
+                    help="time a ScaLAPACK-style call through its C entry point instead of the default workload")
     ap.add_argument("--bench2-sweep", action="store_true",
                     help="print the volume-reduction sweep of the paper's relabeling benchmark")
     args = ap.parse_args()
@@ -208,6 +210,9 @@ def main():
     import paper_2106_06601_amd as C
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.scalapack:
+        print(json.dumps(scalapack_bench(args.scalapack, args)), flush=True)
+        return
     torch.cuda.set_device(0)
     w = synth.workload(args.workload)
     P = w.items[0].A.nranks
@@ -250,6 +255,35 @@ def main():
         else:
             C.costa_transform_batched(w.dtype, descs, sigma, stream)
 
+    t_setup = time.perf_counter() - t_plan0
+    m = measure(step, stats, w.name, args)
+    cpu = None
+    if not args.no_cpu_baseline and len(w.items) == 1:
+        cpu = cpu_baseline(w, sigma, stats["model_bytes"] / stats["total_elems"], args.cpu_seconds)
+
+    out = {
+        "metric": METRIC, "value": m["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": m["ms_per_step"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "pct_of_hbm_peak": round(100 * m["value"] / HBM_PEAK_GBS, 2),
+        "config": describe(w),
+        "model_bytes_per_step": stats["model_bytes"],
+        "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
+        "waves": m["kernels"].get("pack", {}).get("launches_per_step", 0), "plan_s": round(t_setup + m["first_step_s"], 3),
+        "kernels": m["kernels"],
+        "roofline": m["roofline"],
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def measure(step, stats: dict, workload: str, args) -> dict:
+    """Warm-up, then `args.steps` timed steps: per-launch HIP events on the
+    launch stream plus one event pair around all steps."""
+    import torch
+    import paper_2106_06601_amd as C
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
     if args.copy_probe:
         src = torch.ones(args.copy_probe << 17, dtype=torch.float64, device=dev)
         dst = torch.empty_like(src)
@@ -257,14 +291,14 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    t0 = time.perf_counter()
     step()  # builds and uploads the plan
     torch.cuda.synchronize()
-    plan_s = time.perf_counter() - t_plan0
+    first_step_s = time.perf_counter() - t0
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    # timed region: per-launch HIP events (on the launch stream) plus one pair around all steps
     C.costa_timing_enable(True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -292,28 +326,71 @@ def main():
     dominant = max(per_kernel, key=lambda k: kt[k]["ms"])
     dk = per_kernel[dominant]
     achieved = dk["GB_s"]
-    traffic = load_traffic(w.name, dominant, dk["launches_per_step"])
+    traffic = load_traffic(workload, dominant, dk["launches_per_step"])
     roof = {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
             "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
-    cpu = None
-    if not args.no_cpu_baseline and len(w.items) == 1:
-        cpu = cpu_baseline(w, sigma, stats["model_bytes"] / stats["total_elems"], args.cpu_seconds)
+    return {"value": round(value, 1), "ms_per_step": round(ms_per_step, 4), "kernels": per_kernel,
+            "roofline": roof, "first_step_s": first_step_s}
 
-    out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
-        "config": describe(w),
-        "model_bytes_per_step": stats["model_bytes"],
-        "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
-        "waves": per_kernel.get("pack", {}).get("launches_per_step", 0), "plan_s": round(plan_s, 3),
-        "kernels": per_kernel,
-        "roofline": roof,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(out), flush=True)
+
+def scalapack_bench(name: str, args) -> dict:
+    """Throughput of a ScaLAPACK-style call through its C entry point
+    (costa_pdgemr2d, costa_pdtran or costa_pztranc): descriptor and submatrix
+    layouts, plans and message buffers come from the library's caches."""
+    import torch
+    import synth
+    import paper_2106_06601_amd as C
+    torch.cuda.set_device(0)
+    call = synth.scalapack_call(name)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    td = {"f64": torch.float64, "c128": torch.complex128, "f32": torch.float32, "c64": torch.complex64}[call.dtype]
+    LA, LC = C.layout_from_spec(call.A), C.layout_from_spec(call.C)
+    a = [torch.empty(LA.local_elems(q), dtype=td, device=dev) for q in range(call.A.nranks)]
+    c = [torch.empty(LC.local_elems(q), dtype=td, device=dev) for q in range(call.C.nranks)]
+    for q, t in enumerate(a):
+        if t.numel():
+            synth.fill_device(call.dtype, t.data_ptr(), t.numel(), synth.DEFAULT_SEED,
+                              synth.stream(synth.ROLE_B, 0, q), stream.cuda_stream)
+    for q, t in enumerate(c):
+        if t.numel():
+            synth.fill_device(call.dtype, t.data_ptr(), t.numel(), synth.DEFAULT_SEED,
+                              synth.stream(synth.ROLE_A, 0, q), stream.cuda_stream)
+    tr = call.routine != "gemr2d"
+    op = {"gemr2d": "N", "tran": "T", "tranu": "T", "tranc": "C"}[call.routine]
+    ra, ca = (call.n, call.m) if tr else (call.m, call.n)
+    sub_a = LA.submatrix(call.ia - 1, call.ja - 1, ra, ca)
+    sub_c = LC.submatrix(call.ic - 1, call.jc - 1, call.m, call.n)
+    alpha, beta = (1.0, 0.0) if not tr else (call.alpha, call.beta)
+    stats = C.costa_plan_stats(call.dtype, [dict(op=op, alpha=alpha, beta=beta, A=sub_c, B=sub_a)])
+    ga = (call.A.nprow, call.A.npcol, call.A.rank_order)
+    gc = (call.C.nprow, call.C.npcol, call.C.rank_order)
+    da, dc = call.A.desc(), call.C.desc()
+    fn = {"gemr2d": None, "tran": C.costa_pdtran, "tranc": C.costa_pztranc, "tranu": C.costa_pztranu}[call.routine]
+
+    def step():
+        if fn is None:
+            C.costa_pdgemr2d(call.m, call.n, a, call.ia, call.ja, da, ga, c, call.ic, call.jc, dc, gc, stream)
+        else:
+            fn(call.m, call.n, call.alpha, a, call.ia, call.ja, da, ga, call.beta, c, call.ic, call.jc, dc, gc,
+               stream)
+
+    m = measure(step, stats, name, args)
+
+    def dsc(d):
+        return (f"{d.m}x{d.n} in {d.mb}x{d.nb} blocks on a {d.nprow}x{d.npcol} grid ({d.rank_order}-major ranks), "
+                f"RSRC {d.rsrc} CSRC {d.csrc} LLD {d.lld}")
+    return {"metric": METRIC, "value": m["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": m["ms_per_step"], "higher_is_better": True,
+            "dtype": call.dtype, "data": "synthetic", "pct_of_hbm_peak": round(100 * m["value"] / HBM_PEAK_GBS, 2),
+            "config": {"workload": name, "routine": "p" + {"f64": "d", "c128": "z"}[call.dtype] + call.routine,
+                       "m": call.m, "n": call.n, "alpha": str(call.alpha), "beta": str(call.beta),
+                       "source": dsc(call.A) + f", submatrix at ({call.ia}, {call.ja})",
+                       "target": dsc(call.C) + f", submatrix at ({call.ic}, {call.jc})"},
+            "model_bytes_per_step": stats["model_bytes"],
+            "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
+            "kernels": m["kernels"], "roofline": m["roofline"]}
 
 
 if __name__ == "__main__":

@@ -99,7 +99,8 @@ costa_status costa_layout_create(int64_t nrows, int64_t ncols, int32_t nbr, cons
                                  const int64_t* block_ld, costa_layout* out);
 
 /* Block-cyclic (ScaLAPACK) layout: mb x nb blocks dealt cyclically over a
- * prow x pcol process grid, first process row/column 0.  rank_order gives
+ * prow x pcol process grid, first process row/column 0 (for other first
+ * processes and leading dimensions, costa_layout_create_scalapack()).  rank_order gives
  * rank = pr*pcol + pc (ROW_MAJOR) or pr + pc*prow (COL_MAJOR).  Local storage
  * is the ScaLAPACK local matrix of each rank, stored in block_order with
  * leading dimension max(1, local rows) (COL_MAJOR) or max(1, local cols)
@@ -108,6 +109,38 @@ costa_status costa_layout_create(int64_t nrows, int64_t ncols, int32_t nbr, cons
 costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, int64_t nb,
                                               int32_t prow, int32_t pcol, costa_order rank_order,
                                               costa_order block_order, costa_layout* out);
+
+/* A BLACS-style process grid: nprow x npcol processes numbered
+ * rank = pr*npcol + pc (rank_order ROW_MAJOR, BLACS "Row") or
+ * rank = pr + pc*nprow (COL_MAJOR). */
+typedef struct {
+  int32_t nprow;
+  int32_t npcol;
+  costa_order rank_order;
+} costa_grid;
+
+/* Layout of the matrix a ScaLAPACK array descriptor describes on `grid`:
+ * desc[9] = {DTYPE_, CTXT_, M_, N_, MB_, NB_, RSRC_, CSRC_, LLD_}.  MB_ x NB_
+ * blocks dealt cyclically, the first block row to process row RSRC_ and the
+ * first block column to process column CSRC_; each rank stores its local
+ * matrix column-major with leading dimension LLD_ (Section 5 "Matrix Layout"
+ * with the splits at multiples of the block size; the local view of
+ * Figure 1).  CTXT_ is not read: `grid` takes the place of the BLACS context.
+ * One LLD_ serves every rank, so it must be >= max(1, local rows) of every
+ * process row.  Errors: NOT_SUPPORTED for DTYPE_ != 1; INVALID_VALUE for
+ * negative M_/N_, MB_/NB_ < 1, RSRC_/CSRC_ outside the grid, LLD_ too small. */
+costa_status costa_layout_create_scalapack(const int32_t* desc, const costa_grid* grid, costa_layout* out);
+
+/* The m x n submatrix of `parent` whose first element is the parent's
+ * element (i0, j0), 0-based (Section 5, "Scale and Transpose/Conjugate": a
+ * submatrix is taken by truncating the row and column splits).  Every element
+ * keeps its owner and its place in the owner's buffer, so the submatrix
+ * layout addresses the parent's buffers; costa_layout_local_elems() of the
+ * submatrix is the part of the parent's buffer it reaches (0 for a rank that
+ * holds none of it).  The parent may be destroyed afterwards.  Errors:
+ * INVALID_VALUE for a window outside the parent. */
+costa_status costa_layout_submatrix(costa_layout parent, int64_t i0, int64_t j0, int64_t m, int64_t n,
+                                    costa_layout* out);
 
 /* Number of elements the buffer of `rank` must hold (0 if it owns nothing). */
 costa_status costa_layout_local_elems(costa_layout layout, int32_t rank, int64_t* n);
@@ -261,6 +294,58 @@ typedef struct {
  * size the array).  Host only; no device work. */
 costa_status costa_plan_export(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
                                const int32_t* sigma, costa_piece_info* out, int64_t capacity, int64_t* count);
+
+/* ---------------------------------------------------------------------------
+ * ScaLAPACK-compatible routines (Section 5: the operation eq:costa covers
+ * pxgemr2d and pxtran(u/c); a submatrix by truncated splits)
+ *
+ * Arguments follow ScaLAPACK: 1-based global indices of each submatrix's
+ * first element, 9-entry descriptors, m x n the shape of the destination
+ * submatrix.  Each descriptor comes with its costa_grid in place of a BLACS
+ * context, and each matrix is given as the P device pointers of its ranks
+ * (P = nprow*npcol, the same for both grids; NULL allowed for a rank that
+ * holds nothing of the submatrix).  Elements land where the destination
+ * descriptor puts them (no relabeling); elements outside the destination
+ * submatrix are not touched.  m == 0 or n == 0: nothing is enqueued.
+ * Asynchronous on `stream`.  The layouts of descriptor + submatrix pairs and
+ * the plans are cached (until costa_finalize()), so a repeated call only
+ * enqueues kernels.  Errors: those of costa_layout_create_scalapack();
+ * INVALID_VALUE for negative m/n, indices below 1 or submatrices past the
+ * matrix, null pointers; SHAPE_MISMATCH when the grids have different P;
+ * then those of costa_transform().
+ * ------------------------------------------------------------------------- */
+
+/* sub(B) = sub(A): B(ib+i, jb+j) = A(ia+i, ja+j) for 0 <= i < m, 0 <= j < n
+ * (pxgemr2d for any element type; A is the source, B the destination). */
+costa_status costa_pxgemr2d(costa_dtype dtype, int32_t m, int32_t n, const void* const* a, int32_t ia, int32_t ja,
+                            const int32_t* desca, const costa_grid* grida, void* const* b, int32_t ib, int32_t jb,
+                            const int32_t* descb, const costa_grid* gridb, hipStream_t stream);
+
+/* sub(C) = beta*sub(C) + alpha*op(sub(A)), sub(C) m x n at (ic, jc), sub(A)
+ * n x m at (ia, ja); op COSTA_OP_T (pxtran, pxtranu) or COSTA_OP_C (pxtranc).
+ * alpha and beta point to one value of the element type (two for complex).
+ * The element arithmetic is that of costa_transform(). */
+costa_status costa_pxtran(costa_dtype dtype, costa_op op, int32_t m, int32_t n, const void* alpha,
+                          const void* const* a, int32_t ia, int32_t ja, const int32_t* desca, const costa_grid* grida,
+                          const void* beta, void* const* c, int32_t ic, int32_t jc, const int32_t* descc,
+                          const costa_grid* gridc, hipStream_t stream);
+
+/* The ScaLAPACK names: pdgemr2d and pdtran (double), pztranu and pztranc
+ * (double complex; alpha and beta point to {re, im}). */
+costa_status costa_pdgemr2d(int32_t m, int32_t n, const void* const* a, int32_t ia, int32_t ja, const int32_t* desca,
+                            const costa_grid* grida, void* const* b, int32_t ib, int32_t jb, const int32_t* descb,
+                            const costa_grid* gridb, hipStream_t stream);
+costa_status costa_pdtran(int32_t m, int32_t n, const double* alpha, const void* const* a, int32_t ia, int32_t ja,
+                          const int32_t* desca, const costa_grid* grida, const double* beta, void* const* c,
+                          int32_t ic, int32_t jc, const int32_t* descc, const costa_grid* gridc, hipStream_t stream);
+costa_status costa_pztranu(int32_t m, int32_t n, const double* alpha, const void* const* a, int32_t ia, int32_t ja,
+                           const int32_t* desca, const costa_grid* grida, const double* beta, void* const* c,
+                           int32_t ic, int32_t jc, const int32_t* descc, const costa_grid* gridc,
+                           hipStream_t stream);
+costa_status costa_pztranc(int32_t m, int32_t n, const double* alpha, const void* const* a, int32_t ia, int32_t ja,
+                           const int32_t* desca, const costa_grid* grida, const double* beta, void* const* c,
+                           int32_t ic, int32_t jc, const int32_t* descc, const costa_grid* gridc,
+                           hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Kernel timing (HIP events around each launch, on the launch stream)

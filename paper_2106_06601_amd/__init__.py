@@ -52,6 +52,10 @@ class CostaPieceInfo(ctypes.Structure):
                 ("ny", _i32), ("item", _i32), ("flags", _i32)]
 
 
+class CostaGrid(ctypes.Structure):
+    _fields_ = [("nprow", _i32), ("npcol", _i32), ("rank_order", ctypes.c_int)]
+
+
 class CostaTiming(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double * 4), ("launches", _i64 * 4), ("bytes", _i64 * 4)]
 
@@ -59,6 +63,19 @@ class CostaTiming(ctypes.Structure):
 _SIGS = {
     "costa_layout_create": [_i64, _i64, _i32, _vp, _i32, _vp, _vp, _i32, ctypes.c_int, _vp, _vp, _P(_vp)],
     "costa_layout_create_block_cyclic": [_i64, _i64, _i64, _i64, _i32, _i32, ctypes.c_int, ctypes.c_int, _P(_vp)],
+    "costa_layout_create_scalapack": [_vp, _P(CostaGrid), _P(_vp)],
+    "costa_layout_submatrix": [_vp, _i64, _i64, _i64, _i64, _P(_vp)],
+    "costa_pxgemr2d": [ctypes.c_int, _i32, _i32, _vp, _i32, _i32, _vp, _P(CostaGrid), _vp, _i32, _i32, _vp,
+                       _P(CostaGrid), _vp],
+    "costa_pxtran": [ctypes.c_int, ctypes.c_int, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _P(CostaGrid), _vp, _vp,
+                     _i32, _i32, _vp, _P(CostaGrid), _vp],
+    "costa_pdgemr2d": [_i32, _i32, _vp, _i32, _i32, _vp, _P(CostaGrid), _vp, _i32, _i32, _vp, _P(CostaGrid), _vp],
+    "costa_pdtran": [_i32, _i32, _vp, _vp, _i32, _i32, _vp, _P(CostaGrid), _vp, _vp, _i32, _i32, _vp,
+                     _P(CostaGrid), _vp],
+    "costa_pztranu": [_i32, _i32, _vp, _vp, _i32, _i32, _vp, _P(CostaGrid), _vp, _vp, _i32, _i32, _vp,
+                      _P(CostaGrid), _vp],
+    "costa_pztranc": [_i32, _i32, _vp, _vp, _i32, _i32, _vp, _P(CostaGrid), _vp, _vp, _i32, _i32, _vp,
+                      _P(CostaGrid), _vp],
     "costa_layout_local_elems": [_vp, _i32, _P(_i64)],
     "costa_layout_block": [_vp, _i32, _i32, _P(_i32), _P(_i64), _P(_i64)],
     "costa_layout_info": [_vp, _P(_i64), _P(_i64), _P(_i32), _P(_i32), _P(_i32), _P(ctypes.c_int)],
@@ -155,6 +172,30 @@ def costa_layout_create_block_cyclic(nrows: int, ncols: int, mb: int, nb: int, p
     return h.value
 
 
+def _grid(nprow: int, npcol: int, rank_order: str = "row") -> CostaGrid:
+    return CostaGrid(nprow, npcol, ORDERS[rank_order])
+
+
+def _desc9(desc) -> np.ndarray:
+    d = np.ascontiguousarray(desc, dtype=np.int32)
+    if d.size != 9:
+        raise ValueError("a ScaLAPACK descriptor has 9 entries")
+    return d
+
+
+def costa_layout_create_scalapack(desc, nprow: int, npcol: int, rank_order: str = "row") -> int:
+    d, g, h = _desc9(desc), _grid(nprow, npcol, rank_order), _vp()
+    _check(_lib.costa_layout_create_scalapack(d.ctypes.data, ctypes.byref(g), ctypes.byref(h)),
+           "costa_layout_create_scalapack")
+    return h.value
+
+
+def costa_layout_submatrix(layout, i0: int, j0: int, m: int, n: int) -> int:
+    h = _vp()
+    _check(_lib.costa_layout_submatrix(_h(layout), i0, j0, m, n, ctypes.byref(h)), "costa_layout_submatrix")
+    return h.value
+
+
 def costa_layout_local_elems(layout: int, rank: int) -> int:
     n = _i64()
     _check(_lib.costa_layout_local_elems(layout, rank, ctypes.byref(n)), "costa_layout_local_elems")
@@ -195,6 +236,13 @@ class Layout:
     @classmethod
     def general(cls, *args, **kw) -> "Layout":
         return cls(costa_layout_create(*args, **kw))
+
+    @classmethod
+    def scalapack(cls, *args, **kw) -> "Layout":
+        return cls(costa_layout_create_scalapack(*args, **kw))
+
+    def submatrix(self, i0: int, j0: int, m: int, n: int) -> "Layout":
+        return Layout(costa_layout_submatrix(self.handle, i0, j0, m, n))
 
     def local_elems(self, rank: int) -> int:
         return costa_layout_local_elems(self.handle, rank)
@@ -321,6 +369,66 @@ def costa_plan_export(dtype: str, descs: Sequence[dict], sigma=None) -> np.ndarr
     return np.ctypeslib.as_array(out)[:cnt.value].copy()
 
 
+# ---------------------------------------------------------------------------
+# ScaLAPACK-compatible routines (1-based indices, 9-entry descriptors; a grid
+# is (nprow, npcol, rank_order))
+# ---------------------------------------------------------------------------
+def _sl_args(a, ia, ja, desca, grida, c, ic, jc, descc, gridc, keep):
+    da, dc = _desc9(desca), _desc9(descc)
+    ga, gc = _grid(*grida), _grid(*gridc)
+    ap, cp = _ptr_array(a), _ptr_array(c)
+    keep.extend([da, dc, ga, gc, ap, cp])
+    return (ctypes.cast(ap, _vp), ia, ja, da.ctypes.data, ctypes.byref(ga),
+            ctypes.cast(cp, _vp), ic, jc, dc.ctypes.data, ctypes.byref(gc))
+
+
+def costa_pxgemr2d(dtype: str, m: int, n: int, a, ia: int, ja: int, desca, grida, b, ib: int, jb: int, descb,
+                   gridb, stream=None) -> None:
+    keep: List = []
+    _check(_lib.costa_pxgemr2d(DTYPES[dtype], m, n, *_sl_args(a, ia, ja, desca, grida, b, ib, jb, descb, gridb, keep),
+                               _stream(stream)), "costa_pxgemr2d")
+
+
+def costa_pxtran(dtype: str, op: str, m: int, n: int, alpha, a, ia: int, ja: int, desca, grida, beta, c,
+                 ic: int, jc: int, descc, gridc, stream=None) -> None:
+    keep: List = []
+    al, be = _scalar(dtype, alpha), _scalar(dtype, beta)
+    ap, ia_, ja_, da, ga, cp, ic_, jc_, dc, gc = _sl_args(a, ia, ja, desca, grida, c, ic, jc, descc, gridc, keep)
+    _check(_lib.costa_pxtran(DTYPES[dtype], OPS[op], m, n, ctypes.cast(ctypes.pointer(al), _vp), ap, ia_, ja_, da,
+                             ga, ctypes.cast(ctypes.pointer(be), _vp), cp, ic_, jc_, dc, gc, _stream(stream)),
+           "costa_pxtran")
+
+
+def costa_pdgemr2d(m: int, n: int, a, ia: int, ja: int, desca, grida, b, ib: int, jb: int, descb, gridb,
+                   stream=None) -> None:
+    keep: List = []
+    _check(_lib.costa_pdgemr2d(m, n, *_sl_args(a, ia, ja, desca, grida, b, ib, jb, descb, gridb, keep),
+                               _stream(stream)), "costa_pdgemr2d")
+
+
+def _pxtran_named(name: str, dtype: str, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
+                  stream):
+    keep: List = []
+    al, be = _scalar(dtype, alpha), _scalar(dtype, beta)
+    ap, ia_, ja_, da, ga, cp, ic_, jc_, dc, gc = _sl_args(a, ia, ja, desca, grida, c, ic, jc, descc, gridc, keep)
+    _check(getattr(_lib, name)(m, n, ctypes.cast(ctypes.pointer(al), _vp), ap, ia_, ja_, da, ga,
+                               ctypes.cast(ctypes.pointer(be), _vp), cp, ic_, jc_, dc, gc, _stream(stream)), name)
+
+
+def costa_pdtran(m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc, stream=None) -> None:
+    _pxtran_named("costa_pdtran", "f64", m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc, stream)
+
+
+def costa_pztranu(m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc, stream=None) -> None:
+    _pxtran_named("costa_pztranu", "c128", m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
+                  stream)
+
+
+def costa_pztranc(m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc, stream=None) -> None:
+    _pxtran_named("costa_pztranc", "c128", m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
+                  stream)
+
+
 def costa_set_workspace_limit(nbytes: int) -> None:
     _check(_lib.costa_set_workspace_limit(nbytes), "costa_set_workspace_limit")
 
@@ -350,9 +458,12 @@ def costa_last_error() -> str:
 def layout_from_spec(spec) -> Layout:
     """Layout from a recipe object with the attributes of a block-cyclic
     (nrows, ncols, mb, nb, prow, pcol, rank_order, block_order) or general
-    (nrows, ncols, row_splits, col_splits, owners, nranks, block_order) grid."""
+    (nrows, ncols, row_splits, col_splits, owners, nranks, block_order) grid,
+    or of a ScaLAPACK descriptor (desc(), nprow, npcol, rank_order)."""
     if spec.kind == "block_cyclic":
         return Layout.block_cyclic(spec.nrows, spec.ncols, spec.mb, spec.nb, spec.prow, spec.pcol,
                                    spec.rank_order, spec.block_order)
+    if spec.kind == "scalapack":
+        return Layout.scalapack(spec.desc(), spec.nprow, spec.npcol, spec.rank_order)
     return Layout.general(spec.nrows, spec.ncols, spec.row_splits, spec.col_splits, spec.owners, spec.nranks,
                           spec.block_order)

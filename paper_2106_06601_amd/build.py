@@ -25,7 +25,7 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wall", "-Wno-unused-function"]
-SOURCES = ["layout.cpp", "lap.cpp", "plan.cpp", "api.cpp", "kernels.hip"]
+SOURCES = ["layout.cpp", "lap.cpp", "plan.cpp", "api.cpp", "scalapack.cpp", "kernels.hip"]
 
 
 def _run(cmd):

@@ -632,12 +632,12 @@ extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, 
       // transposed, and its process row for the columns)
       const int32_t nrb = tr ? B->pcol : B->prow, ncb = tr ? B->prow : B->pcol;
       for (Interval& v : rows) {
-        v.a %= A->prow;
-        v.b %= nrb;
+        v.a = A->prow_of(v.a);
+        v.b = tr ? B->pcol_of(v.b) : B->prow_of(v.b);
       }
       for (Interval& v : cols) {
-        v.a %= A->pcol;
-        v.b %= ncb;
+        v.a = A->pcol_of(v.a);
+        v.b = tr ? B->prow_of(v.b) : B->pcol_of(v.b);
       }
       const size_t nh_r = (size_t)nrb * A->prow, nh_c = (size_t)ncb * A->pcol;
       zeros.assign(std::max(nh_r, nh_c), 0ull);
@@ -725,5 +725,6 @@ extern "C" costa_status costa_finalize(void) {
   S.event_pool.clear();
   S.timing = false;
   S.totals = costa_timing{};
+  release_scalapack_layouts();
   return COSTA_SUCCESS;
 }

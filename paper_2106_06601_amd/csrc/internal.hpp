@@ -29,28 +29,46 @@ struct Layout {
   std::vector<int32_t> owner;
   std::vector<int64_t> boff, bld;
   // block-cyclic layouts keep no per-block arrays (a 10^5 x 10^5 matrix in
-  // 1 x 1 blocks has 10^10 of them): block (bi, bj) belongs to process
-  // (bi % prow, bj % pcol) and sits in its ScaLAPACK local matrix
+  // 1 x 1 blocks has 10^10 of them).  They follow a ScaLAPACK descriptor: the
+  // full matrix is dealt in mb x nb blocks over a prow x pcol grid starting
+  // at process (rsrc, csrc), and each rank keeps its local matrix with
+  // leading dimension lld (0: its own local extent, at least 1).  A layout
+  // may be a window of that matrix: its element (i, j) is element
+  // (r0 + i, c0 + j) of the full one, and its block bi is the full
+  // matrix's block row r0/mb + bi, truncated to the window (Section 5,
+  // a submatrix by truncating the splits).
   bool block_cyclic = false;
   int32_t prow = 0, pcol = 0;
+  int32_t rsrc = 0, csrc = 0;
   costa_order rank_order = COSTA_ROW_MAJOR;
   int64_t mb = 0, nb = 0;
-  std::vector<int64_t> lrows, lcols;  // local extents per process row / column
+  int64_t lld = 0;
+  int64_t r0 = 0, c0 = 0;            // window origin in the full matrix
+  int64_t rb0 = 0, cb0 = 0;          // r0 / mb, c0 / nb
+  std::vector<int64_t> lrows, lcols;  // local extents of the full matrix per process row / column
 
   int64_t block(int32_t bi, int32_t bj) const { return (int64_t)bi * nbc + bj; }
+  int32_t prow_of(int32_t bi) const { return (int32_t)((rb0 + bi + rsrc) % prow); }
+  int32_t pcol_of(int32_t bj) const { return (int32_t)((cb0 + bj + csrc) % pcol); }
+  int32_t rank_at(int32_t pr, int32_t pc) const {
+    return rank_order == COSTA_ROW_MAJOR ? pr * pcol + pc : pr + pc * prow;
+  }
   int32_t owner_of(int32_t bi, int32_t bj) const {
     if (!block_cyclic) return owner[block(bi, bj)];
-    const int32_t pr = bi % prow, pc = bj % pcol;
-    return rank_order == COSTA_ROW_MAJOR ? pr * pcol + pc : pr + pc * prow;
+    return rank_at(prow_of(bi), pcol_of(bj));
   }
   int64_t ld_of(int32_t bi, int32_t bj) const {
     if (!block_cyclic) return bld[block(bi, bj)];
-    const int64_t ext = order == COSTA_COL_MAJOR ? lrows[bi % prow] : lcols[bj % pcol];
+    if (lld) return lld;
+    const int64_t ext = order == COSTA_COL_MAJOR ? lrows[prow_of(bi)] : lcols[pcol_of(bj)];
     return ext > 1 ? ext : 1;
   }
   int64_t offset_of(int32_t bi, int32_t bj) const {
     if (!block_cyclic) return boff[block(bi, bj)];
-    const int64_t li = (int64_t)(bi / prow) * mb, lj = (int64_t)(bj / pcol) * nb;  // local origin of the block
+    // local position of the block's first element (ScaLAPACK INDXG2L)
+    const int64_t gi = r0 + rsplit[bi], gj = c0 + csplit[bj];
+    const int64_t li = ((rb0 + bi) / prow) * mb + gi % mb;
+    const int64_t lj = ((cb0 + bj) / pcol) * nb + gj % nb;
     const int64_t ld = ld_of(bi, bj);
     return order == COSTA_COL_MAJOR ? li + lj * ld : li * ld + lj;
   }
@@ -164,6 +182,10 @@ struct SeparableArgs {
   unsigned long long* V;
 };
 hipError_t launch_volume_separable(const SeparableArgs& a, hipStream_t stream);
+
+// ---- ScaLAPACK-compatible routines (scalapack.cpp) ----------------------------
+// Destroys the cached descriptor layouts (called by costa_finalize).
+void release_scalapack_layouts();
 
 // ---- relabeling (lap.cpp) --------------------------------------------------
 // Lexicographically smallest sigma maximising sum_t V[sigma[t]][t].

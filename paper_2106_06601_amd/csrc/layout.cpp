@@ -127,11 +127,67 @@ extern "C" costa_status costa_layout_create(int64_t nrows, int64_t ncols, int32_
   return COSTA_SUCCESS;
 }
 
-extern "C" costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, int64_t nb,
-                                                         int32_t prow, int32_t pcol, costa_order rank_order,
-                                                         costa_order block_order, costa_layout* out) {
-  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
-  *out = nullptr;
+namespace costa {
+
+// Splits of the window [r0, r0 + m) of a dimension dealt in blocks of mb: the
+// full matrix's block boundaries inside the window, shifted to start at 0.
+static bool window_splits(int64_t r0, int64_t m, int64_t mb, std::vector<int64_t>& s) {
+  s.assign(1, 0);
+  if (m == 0) return true;
+  const int64_t first = r0 / mb, last = (r0 + m - 1) / mb;
+  if (last - first + 1 > INT32_MAX) return false;
+  for (int64_t k = first + 1; k <= last; ++k) s.push_back(k * mb - r0);
+  s.push_back(m);
+  return true;
+}
+
+// Sets the window of a block-cyclic layout (origin r0, c0 in the full
+// matrix; m x n) and the buffer size each rank needs for it: one past the
+// rank's last window element.
+static costa_status set_window(Layout& L, int64_t r0, int64_t c0, int64_t m, int64_t n) {
+  if (!window_splits(r0, m, L.mb, L.rsplit) || !window_splits(c0, n, L.nb, L.csplit))
+    return fail(COSTA_ERROR_INVALID_VALUE, "too many blocks");
+  L.nrows = m;
+  L.ncols = n;
+  L.nbr = (int32_t)(L.rsplit.size() - 1);
+  L.nbc = (int32_t)(L.csplit.size() - 1);
+  L.r0 = r0;
+  L.c0 = c0;
+  L.rb0 = r0 / L.mb;
+  L.cb0 = c0 / L.nb;
+  // one past the largest local row (column) index of the window on each
+  // process row (column): the window's last block on it ends there
+  std::vector<int64_t> rows_used(L.prow, 0), cols_used(L.pcol, 0);
+  for (int32_t bi = 0; bi < L.nbr; ++bi) {
+    const int64_t g = r0 + L.rsplit[bi + 1] - 1;
+    rows_used[L.prow_of(bi)] = ((L.rb0 + bi) / L.prow) * L.mb + g % L.mb + 1;
+  }
+  for (int32_t bj = 0; bj < L.nbc; ++bj) {
+    const int64_t g = c0 + L.csplit[bj + 1] - 1;
+    cols_used[L.pcol_of(bj)] = ((L.cb0 + bj) / L.pcol) * L.nb + g % L.nb + 1;
+  }
+  L.local_elems.assign(L.nranks, 0);
+  for (int32_t pr = 0; pr < L.prow; ++pr)
+    for (int32_t pc = 0; pc < L.pcol; ++pc) {
+      if (rows_used[pr] == 0 || cols_used[pc] == 0) continue;
+      int64_t need;
+      if (L.order == COSTA_COL_MAJOR) {
+        const int64_t ld = L.lld ? L.lld : std::max<int64_t>(1, L.lrows[pr]);
+        need = (cols_used[pc] - 1) * ld + rows_used[pr];
+      } else {
+        const int64_t ld = L.lld ? L.lld : std::max<int64_t>(1, L.lcols[pc]);
+        need = (rows_used[pr] - 1) * ld + cols_used[pc];
+      }
+      L.local_elems[L.rank_at(pr, pc)] = need;
+    }
+  L.id = g_next_id.fetch_add(1);
+  return COSTA_SUCCESS;
+}
+
+// Block-cyclic layout of a whole matrix dealt from process (rsrc, csrc).
+static costa_status make_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, int64_t nb, int32_t prow,
+                                      int32_t pcol, int32_t rsrc, int32_t csrc, int64_t lld, costa_order rank_order,
+                                      costa_order block_order, costa_layout* out) {
   if (nrows < 0 || ncols < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative dimension");
   if (mb < 1 || nb < 1) return fail(COSTA_ERROR_INVALID_VALUE, "block sizes must be >= 1");
   if (prow < 1 || pcol < 1) return fail(COSTA_ERROR_INVALID_VALUE, "process grid must be at least 1x1");
@@ -140,40 +196,127 @@ extern "C" costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t 
     return fail(COSTA_ERROR_INVALID_VALUE, "unknown rank order");
   if (block_order != COSTA_COL_MAJOR && block_order != COSTA_ROW_MAJOR)
     return fail(COSTA_ERROR_INVALID_VALUE, "unknown block order");
-  int64_t nbr64 = (nrows + mb - 1) / mb, nbc64 = (ncols + nb - 1) / nb;
-  if (nbr64 > INT32_MAX || nbc64 > INT32_MAX) return fail(COSTA_ERROR_INVALID_VALUE, "too many blocks");
-  int32_t nbr = (int32_t)nbr64, nbc = (int32_t)nbc64;
-
+  if ((nrows + mb - 1) / mb > INT32_MAX || (ncols + nb - 1) / nb > INT32_MAX)
+    return fail(COSTA_ERROR_INVALID_VALUE, "too many blocks");
   costa_layout_s* h = new (std::nothrow) costa_layout_s();
   if (!h) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
   Layout& L = h->L;
-  L.nrows = nrows;
-  L.ncols = ncols;
-  L.nbr = nbr;
-  L.nbc = nbc;
   L.nranks = prow * pcol;
   L.order = block_order;
-  L.rsplit.resize(nbr + 1);
-  for (int32_t k = 0; k <= nbr; ++k) L.rsplit[k] = std::min<int64_t>((int64_t)k * mb, nrows);
-  L.csplit.resize(nbc + 1);
-  for (int32_t k = 0; k <= nbc; ++k) L.csplit[k] = std::min<int64_t>((int64_t)k * nb, ncols);
-  // local extents of each process row / column: the sum of the blocks it is dealt
-  L.lrows.assign(prow, 0);
-  L.lcols.assign(pcol, 0);
-  for (int32_t bi = 0; bi < nbr; ++bi) L.lrows[bi % prow] += L.rsplit[bi + 1] - L.rsplit[bi];
-  for (int32_t bj = 0; bj < nbc; ++bj) L.lcols[bj % pcol] += L.csplit[bj + 1] - L.csplit[bj];
-  L.mb = mb;
-  L.nb = nb;
   L.block_cyclic = true;
   L.prow = prow;
   L.pcol = pcol;
+  L.rsrc = rsrc;
+  L.csrc = csrc;
   L.rank_order = rank_order;
-  // every rank holds its local matrix of lrows x lcols elements
-  L.local_elems.assign(L.nranks, 0);
-  for (int32_t pr = 0; pr < prow; ++pr)
-    for (int32_t pc = 0; pc < pcol; ++pc)
-      L.local_elems[rank_order == COSTA_ROW_MAJOR ? pr * pcol + pc : pr + pc * prow] = L.lrows[pr] * L.lcols[pc];
-  L.id = g_next_id.fetch_add(1);
+  L.mb = mb;
+  L.nb = nb;
+  // local extents of each process row / column: the blocks dealt to it, the
+  // first block to process row rsrc (column csrc)
+  L.lrows.assign(prow, 0);
+  L.lcols.assign(pcol, 0);
+  for (int64_t k = 0; k * mb < nrows; ++k) L.lrows[(k + rsrc) % prow] += std::min(mb, nrows - k * mb);
+  for (int64_t k = 0; k * nb < ncols; ++k) L.lcols[(k + csrc) % pcol] += std::min(nb, ncols - k * nb);
+  const int64_t need_ld = std::max<int64_t>(
+      1, block_order == COSTA_COL_MAJOR ? *std::max_element(L.lrows.begin(), L.lrows.end())
+                                        : *std::max_element(L.lcols.begin(), L.lcols.end()));
+  if (lld != 0 && lld < need_ld) {
+    delete h;
+    return fail(COSTA_ERROR_INVALID_VALUE, "local leading dimension smaller than the local extent");
+  }
+  L.lld = lld;
+  costa_status st = set_window(L, 0, 0, nrows, ncols);
+  if (st != COSTA_SUCCESS) {
+    delete h;
+    return st;
+  }
+  *out = h;
+  return COSTA_SUCCESS;
+}
+
+}  // namespace costa
+
+extern "C" costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, int64_t nb,
+                                                         int32_t prow, int32_t pcol, costa_order rank_order,
+                                                         costa_order block_order, costa_layout* out) {
+  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
+  *out = nullptr;
+  return make_block_cyclic(nrows, ncols, mb, nb, prow, pcol, 0, 0, 0, rank_order, block_order, out);
+}
+
+extern "C" costa_status costa_layout_create_scalapack(const int32_t* desc, const costa_grid* grid,
+                                                      costa_layout* out) {
+  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
+  *out = nullptr;
+  if (!desc || !grid) return fail(COSTA_ERROR_INVALID_VALUE, "null descriptor or grid");
+  if (desc[0] != 1) return fail(COSTA_ERROR_NOT_SUPPORTED, "descriptor type (DTYPE_) other than 1 (dense)");
+  if (grid->nprow < 1 || grid->npcol < 1) return fail(COSTA_ERROR_INVALID_VALUE, "process grid must be at least 1x1");
+  if (desc[6] < 0 || desc[6] >= grid->nprow) return fail(COSTA_ERROR_INVALID_VALUE, "RSRC_ outside the process grid");
+  if (desc[7] < 0 || desc[7] >= grid->npcol) return fail(COSTA_ERROR_INVALID_VALUE, "CSRC_ outside the process grid");
+  if (desc[8] < 1) return fail(COSTA_ERROR_INVALID_VALUE, "LLD_ must be >= 1");
+  return make_block_cyclic(desc[2], desc[3], desc[4], desc[5], grid->nprow, grid->npcol, desc[6], desc[7], desc[8],
+                           grid->rank_order, COSTA_COL_MAJOR, out);
+}
+
+extern "C" costa_status costa_layout_submatrix(costa_layout parent, int64_t i0, int64_t j0, int64_t m, int64_t n,
+                                               costa_layout* out) {
+  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
+  *out = nullptr;
+  if (!parent) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
+  const Layout& P = parent->L;
+  if (i0 < 0 || j0 < 0 || m < 0 || n < 0 || i0 > P.nrows - m || j0 > P.ncols - n)
+    return fail(COSTA_ERROR_INVALID_VALUE, "submatrix outside the matrix");
+  costa_layout_s* h = new (std::nothrow) costa_layout_s();
+  if (!h) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
+  Layout& L = h->L;
+  costa_status st;
+  if (P.block_cyclic) {
+    L = P;
+    st = set_window(L, P.r0 + i0, P.c0 + j0, m, n);
+  } else {
+    // keep the blocks the window meets, cut to it; each keeps its storage,
+    // the offset moving to the window's first element inside it
+    auto range = [](const std::vector<int64_t>& s, int64_t lo, int64_t len, int32_t& first) -> int32_t {
+      if (len == 0) {
+        first = 0;
+        return 0;
+      }
+      first = (int32_t)(std::upper_bound(s.begin(), s.end(), lo) - s.begin() - 1);
+      const int32_t last = (int32_t)(std::upper_bound(s.begin(), s.end(), lo + len - 1) - s.begin() - 1);
+      return last - first + 1;
+    };
+    int32_t fr, fc;
+    const int32_t nbr = range(P.rsplit, i0, m, fr), nbc = range(P.csplit, j0, n, fc);
+    L.nrows = m;
+    L.ncols = n;
+    L.nbr = nbr;
+    L.nbc = nbc;
+    L.nranks = P.nranks;
+    L.order = P.order;
+    L.rsplit.assign(nbr + 1, 0);
+    for (int32_t k = 1; k < nbr; ++k) L.rsplit[k] = P.rsplit[fr + k] - i0;
+    L.rsplit[nbr] = m;
+    L.csplit.assign(nbc + 1, 0);
+    for (int32_t k = 1; k < nbc; ++k) L.csplit[k] = P.csplit[fc + k] - j0;
+    L.csplit[nbc] = n;
+    const size_t nblocks = (size_t)nbr * nbc;
+    L.owner.resize(nblocks);
+    L.boff.resize(nblocks);
+    L.bld.resize(nblocks);
+    for (int32_t bi = 0; bi < nbr; ++bi)
+      for (int32_t bj = 0; bj < nbc; ++bj) {
+        const int64_t pb = P.block(fr + bi, fc + bj), b = L.block(bi, bj);
+        const int64_t pi = i0 + L.rsplit[bi] - P.rsplit[fr + bi], pj = j0 + L.csplit[bj] - P.csplit[fc + bj];
+        L.owner[b] = P.owner[pb];
+        L.bld[b] = P.bld[pb];
+        L.boff[b] = P.boff[pb] + (P.order == COSTA_COL_MAJOR ? pi + pj * P.bld[pb] : pi * P.bld[pb] + pj);
+      }
+    st = finish_layout(L);
+  }
+  if (st != COSTA_SUCCESS) {
+    delete h;
+    return st;
+  }
   *out = h;
   return COSTA_SUCCESS;
 }

@@ -360,3 +360,35 @@ def workload(name: str, scale: str = "full", seed: int = DEFAULT_SEED) -> Worklo
 
 WORKLOADS = ["reshuffle_transpose_1k", "blocksize_change_16k", "scaled_transpose_20k",
              "cosma_complex_16k", "rpa_batched_tall_skinny"]
+
+
+def _lld(m: int, mb: int, nprow: int, pad: int) -> int:
+    """A valid local leading dimension: a whole share of blocks per process
+    row (ceil(ceil(m/mb)/nprow) blocks) plus `pad` rows of slack."""
+    return -(-(-(-m // mb)) // nprow) * mb + pad
+
+
+def scalapack_call(name: str, scale: str = "full") -> ScaLapackCall:
+    """ScaLAPACK-style calls of the paper's ScaLAPACK comparison: a 16 x 16
+    process grid, fp64, 32 x 32 source blocks -> 128 x 128 target blocks, the
+    source a submatrix starting mid-block of a larger matrix, the target's
+    first block on process (3, 5), padded leading dimensions; at full size
+    ('full', 16384^2) or with the same grids and blocks at 2048^2 ('small')."""
+    small = scale == "small"
+    n = 2048 if small else 16384
+    big = n + 512
+    src = ScaLapack(big, big, 32, 32, 0, 0, _lld(big, 32, 16, 8), 16, 16)
+    dst = ScaLapack(n, n, 128, 128, 3, 5, _lld(n, 128, 16, 8), 16, 16)
+    if name == "pdgemr2d_16k":
+        return ScaLapackCall("gemr2d", "f64", n, n, 1.0, 0.0, src, 17, 273, dst, 1, 1)
+    if name == "pdtran_16k":
+        return ScaLapackCall("tran", "f64", n, n, 1.0, 0.0, src, 17, 273, dst, 1, 1)
+    if name == "pztranc_8k":
+        m = 1024 if small else 8192
+        a = ScaLapack(m + 100, m + 100, 64, 64, 1, 2, _lld(m + 100, 64, 8, 4), 8, 8, "col")
+        c = ScaLapack(m, m, 96, 96, 0, 0, _lld(m, 96, 8, 0), 8, 8)
+        return ScaLapackCall("tranc", "c128", m, m, 1.0 - 1.0j, 0.5, a, 50, 51, c, 1, 1)
+    raise KeyError(name)
+
+
+SCALAPACK_CALLS = ["pdgemr2d_16k", "pdtran_16k", "pztranc_8k"]

@@ -1,0 +1,42 @@
+"""Helpers of the CPU plan replays: the addressing of a work rectangle and
+the element arithmetic, written out with numpy (every product and sum
+rounded on its own)."""
+import numpy as np
+
+import oracle
+
+
+def _index(p):
+    x = np.arange(p["nx"], dtype=np.int64)[None, :]
+    y = np.arange(p["ny"], dtype=np.int64)[:, None]
+    dst = p["dst_off"] + y * p["dst_ld"] + x
+    if p["flags"] & 1:
+        src = p["src_off"] + x * p["src_ld"] + y
+    else:
+        src = p["src_off"] + y * p["src_ld"] + x
+    return src.ravel(), dst.ravel()
+
+
+def _combine(dtype, b, a, alpha, beta, conj):
+    """alpha*b + beta*a with every product and sum rounded on its own."""
+    cplx = dtype in ("c128", "c64")
+    f = np.float64 if dtype in ("f64", "c128") else np.float32
+    if cplx and conj:
+        b = np.conj(b)  # sign flip of the imaginary part
+    if alpha == 1 and beta == 0:
+        return b
+    if not cplx:
+        t1 = f(alpha.real) * b
+        return t1 if beta == 0 else t1 + f(beta.real) * a
+    ar, ai = f(alpha.real), f(alpha.imag)
+    br_, bi_ = b.real, b.imag
+    t1r = ar * br_ - ai * bi_
+    t1i = ar * bi_ + ai * br_
+    if beta != 0:
+        er, ei = f(beta.real), f(beta.imag)
+        t1r = t1r + (er * a.real - ei * a.imag)
+        t1i = t1i + (er * a.imag + ei * a.real)
+    out = np.empty(b.shape, dtype=oracle.NUMPY[dtype])
+    out.real = t1r
+    out.imag = t1i
+    return out
