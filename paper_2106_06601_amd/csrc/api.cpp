@@ -18,12 +18,20 @@ namespace {
 // Work sizes (measured on MI355X): rectangles of at most 16K elements (times
 // COSTA_T_PIECE_FACTOR when transposed), and a workgroup takes consecutive
 // rectangles until it holds 512 elements, i.e. small rectangles get a
-// workgroup each.
+// workgroup each; transposed 8-byte rectangles are grouped up to 4096
+// elements (four 32 x 32 tiles, pipelined across rectangles), transposed
+// 16-byte ones stay one per workgroup.
 #ifndef COSTA_MAX_PIECE_ELEMS
 #define COSTA_MAX_PIECE_ELEMS (1 << 14)
 #endif
 #ifndef COSTA_MIN_GROUP_ELEMS
 #define COSTA_MIN_GROUP_ELEMS 512
+#endif
+#ifndef COSTA_MIN_GROUP_ELEMS_T
+#define COSTA_MIN_GROUP_ELEMS_T 512
+#endif
+#ifndef COSTA_MIN_GROUP_ELEMS_T8
+#define COSTA_MIN_GROUP_ELEMS_T8 4096
 #endif
 #ifndef COSTA_T_PIECE_FACTOR
 #define COSTA_T_PIECE_FACTOR 1
@@ -131,6 +139,7 @@ PlanConfig make_config(int es) {
   c.workspace_cap = INT64_MAX;
   c.max_piece_elems = kMaxPieceElems;
   c.min_group_elems = min_group_elems(es);
+  c.min_group_elems_t = es == 8 ? COSTA_MIN_GROUP_ELEMS_T8 : COSTA_MIN_GROUP_ELEMS_T;
   c.max_group_pieces = kMaxGroupPieces;
   c.target_groups = kTargetGroups;
   c.transpose_piece_factor = COSTA_T_PIECE_FACTOR;

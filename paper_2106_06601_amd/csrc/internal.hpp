@@ -91,7 +91,14 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 // direction.  dst(x, y) = dst_off + y*dst_ld + x.  The source is
 //   src_off + y*src_ld + x   (flag TRANSPOSE clear: contiguous along x), or
 //   src_off + x*src_ld + y   (flag TRANSPOSE set: contiguous along y).
-enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2 };
+// PIECE_NARROW_T: a transposed rectangle of 16-byte elements at most
+// kNarrowT16 elements wide along the destination's contiguous direction; the
+// kernels stage it through a narrower LDS tile.
+enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_NARROW_T = 4 };
+#ifndef COSTA_NARROW_T16
+#define COSTA_NARROW_T16 64
+#endif
+constexpr int32_t kNarrowT16 = COSTA_NARROW_T16;
 
 struct alignas(16) Piece {
   int64_t src_off;

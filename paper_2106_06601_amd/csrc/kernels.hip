@@ -38,8 +38,11 @@ namespace {
 #ifndef COSTA_TILE_Y16
 #define COSTA_TILE_Y16 16
 #endif
-#ifndef COSTA_TILE_DEPTH
-#define COSTA_TILE_DEPTH 1  // tiles of loads in flight ahead of the one being stored (1 or 2)
+#ifndef COSTA_TILE_X16N
+#define COSTA_TILE_X16N 64  // narrow rectangles of 16-byte elements
+#endif
+#ifndef COSTA_TILE_Y16N
+#define COSTA_TILE_Y16N 16
 #endif
 #ifndef COSTA_NT_LOADS
 #define COSTA_NT_LOADS 1  // row walks: each source line is read once
@@ -218,33 +221,44 @@ struct TypeTraits {
   // the narrow transposed rectangles of block-cyclic layouts)
   static constexpr int TX = ES >= 16 ? COSTA_TILE_X16 : ES == 8 ? COSTA_TILE_X8 : 64;
   static constexpr int TY = ES >= 16 ? COSTA_TILE_Y16 : ES == 8 ? COSTA_TILE_Y8 : 64;
+  // rectangles marked PIECE_NARROW_T (16-byte elements only): a narrower tile
+  // keeps the store lanes busy
+  static constexpr int TXN = ES >= 16 ? COSTA_TILE_X16N : TX;
+  static constexpr int TYN = ES >= 16 ? COSTA_TILE_Y16N : TY;
+  static constexpr int LDS_ELEMS = TX * (TY + 1) > TXN * (TYN + 1) ? TX * (TY + 1) : TXN * (TYN + 1);
 };
 
-template <typename S, bool CPLX>
-using Tile = Vec<S, CPLX ? 2 : 1> (*)[TypeTraits<S, CPLX>::TY + 1];
-
-// Rectangle whose source runs along y while the destination runs along x:
+// Rectangles whose source runs along y while the destination runs along x:
 // staged through an LDS tile of TX x TY elements (one padding column against
 // bank conflicts).  Loads are coalesced along the source, stores along the
-// destination.  Software pipelined: the loads of the next tile are in flight
-// while the current tile is written out.
-template <typename S, bool CPLX, int MODE, bool CONJ>
-__device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __restrict__ dst, const Piece& p,
-                                                Tile<S, CPLX> tile, S ar, S ai, S br, S bi) {
+// destination.  The workgroup walks the tiles of the consecutive transposed
+// rectangles [pi, p1) as one sequence, software pipelined across rectangle
+// boundaries: the loads of the next tile (of this rectangle or of the next
+// one) are in flight while the current tile is written out.  Returns the
+// index of the first rectangle it did not process (the run stops at a
+// rectangle that is not transposed or takes the other tile shape).  MODE_ANY
+// callers pass p1 = pi + 1.
+template <typename S, bool CPLX, int MODE, bool CONJ, int TX, int TY>
+__device__ __forceinline__ int32_t move_transposed_run(const Piece* __restrict__ pieces, int32_t pi, int32_t p1,
+                                                       void* const* __restrict__ bufs,
+                                                       const ItemParam* __restrict__ items,
+                                                       Vec<S, CPLX ? 2 : 1>* lds) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
-  constexpr int TX = TT::TX, TY = TT::TY;
+  E (*tile)[TY + 1] = reinterpret_cast<E (*)[TY + 1]>(lds);
   constexpr int LROWS = kThreads / TY;  // x rows per load pass
   constexpr int SROWS = kThreads / TX;  // y rows per store pass
   constexpr int NL = TX / LROWS;        // loads per thread per tile
-  const E* __restrict__ se = reinterpret_cast<const E*>(src) + p.src_off;
-  E* __restrict__ de = reinterpret_cast<E*>(dst) + p.dst_off;
+  static_assert(kThreads % TX == 0 && kThreads % TY == 0 && TX % LROWS == 0 && TY % SROWS == 0,
+                "the load and store passes must cover the tile exactly");
   const int32_t tid = threadIdx.x;
   const int32_t ly0 = tid % TY, lx0 = tid / TY;  // load mapping
   const int32_t sx0 = tid % TX, sy0 = tid / TX;  // store mapping
-  const int32_t ntx = (p.nx + TX - 1) / TX, nty = (p.ny + TY - 1) / TY;
-  const int32_t ntiles = ntx * nty;
-  auto fetch = [&](int32_t t, E (&b)[NL]) {
+  auto tiles_x = [](const Piece& p) { return (p.nx + TX - 1) / TX; };
+  auto tiles_of = [&](const Piece& p) { return tiles_x(p) * ((p.ny + TY - 1) / TY); };
+  auto fetch = [&](const Piece& p, int32_t t, E (&b)[NL]) {
+    const E* __restrict__ se = reinterpret_cast<const E*>(bufs[p.src_buf]) + p.src_off;
+    const int32_t ntx = tiles_x(p);
     const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
     const int32_t y = ty + ly0;
 #pragma unroll
@@ -253,52 +267,71 @@ __device__ __forceinline__ void move_transposed(const S* __restrict__ src, S* __
       if (x < p.nx && y < p.ny) b[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)x * p.src_ld + y));
     }
   };
-  // one tile: registers -> LDS, start the loads DEPTH tiles ahead into the
-  // freed registers, LDS -> destination
-  auto step = [&](int32_t t, E (&b)[NL]) {
+  Piece cur = pieces[pi];
+  int32_t ntiles = tiles_of(cur);
+  E b[NL];
+  fetch(cur, 0, b);
+  int32_t t = 0;
+  while (true) {
+    const int32_t ntx = tiles_x(cur);
     const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
+    // registers -> LDS
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int32_t lx = lx0 + k * LROWS;
-      if (tx + lx < p.nx && ty + ly0 < p.ny) tile[lx][ly0] = b[k];
+      if (tx + lx < cur.nx && ty + ly0 < cur.ny) tile[lx][ly0] = b[k];
     }
     __syncthreads();
-    if (t + COSTA_TILE_DEPTH < ntiles) fetch(t + COSTA_TILE_DEPTH, b);
+    // the next tile: of this rectangle, else the first of the next one if it
+    // is transposed too; its loads go out before this tile is stored
+    Piece nxt = cur;
+    int32_t nt = t + 1;
+    bool more = nt < ntiles;
+    if (!more && pi + 1 < p1) {
+      nxt = pieces[pi + 1];
+      constexpr int32_t kClass = PIECE_TRANSPOSE | PIECE_NARROW_T;  // same tile shape
+      more = (nxt.flags & kClass) == (cur.flags & kClass);
+      nt = 0;
+    }
+    if (more) fetch(nxt, nt, b);
+    // LDS -> destination
+    E* __restrict__ de = reinterpret_cast<E*>(bufs[cur.dst_buf]) + cur.dst_off;
+    S ar = S(0), ai = S(0), br = S(0), bi = S(0);
+    if constexpr (MODE != MODE_COPY) {
+      const ItemParam& ip = items[cur.item];
+      ar = (S)ip.alpha[0];
+      ai = (S)ip.alpha[1];
+      br = (S)ip.beta[0];
+      bi = (S)ip.beta[1];
+    }
     const int32_t x = tx + sx0;
 #pragma unroll
     for (int k = 0; k < TY / SROWS; ++k) {
       const int32_t ly = sy0 + k * SROWS;
       const int32_t yy = ty + ly;
-      if (x < p.nx && yy < p.ny) {
-        E* o = de + ((int64_t)yy * p.dst_ld + x);
+      if (x < cur.nx && yy < cur.ny) {
+        E* o = de + ((int64_t)yy * cur.dst_ld + x);
         E a;
         if constexpr (MODE == MODE_AXPBY) a = load<COSTA_NT_ALOADS>(o);
         store(o, combine<S, TT::NS, CPLX, MODE, CONJ>(tile[sx0][ly], a, ar, ai, br, bi));
       }
     }
     __syncthreads();
-  };
-  E b0[NL];
-  fetch(0, b0);
-  if constexpr (COSTA_TILE_DEPTH == 2) {
-    E b1[NL];
-    if (ntiles > 1) fetch(1, b1);
-    for (int32_t t = 0; t < ntiles; t += 2) {
-      step(t, b0);
-      if (t + 1 < ntiles) step(t + 1, b1);
+    if (!more) return pi + 1;
+    if (nt == 0) {
+      ++pi;
+      cur = nxt;
+      ntiles = tiles_of(cur);
     }
-  } else {
-    for (int32_t t = 0; t < ntiles; ++t) step(t, b0);
+    t = nt;
   }
 }
 
-template <typename S, bool CPLX, int MODE, bool CONJ, bool HAS_T>
-__device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p, bool wide, Tile<S, CPLX> tile, S ar,
-                                           S ai, S br, S bi) {
+// A rectangle whose source and destination run the same way.
+template <typename S, bool CPLX, int MODE, bool CONJ>
+__device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p, bool wide, S ar, S ai, S br, S bi) {
   using TT = TypeTraits<S, CPLX>;
-  if (HAS_T && (p.flags & PIECE_TRANSPOSE)) {
-    if constexpr (HAS_T) move_transposed<S, CPLX, MODE, CONJ>(src, dst, p, tile, ar, ai, br, bi);
-  } else if (wide && TT::WIDE_NEL > 1) {
+  if (wide && TT::WIDE_NEL > 1) {
     move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, COSTA_UNROLL_WIDE>(src, dst, p, ar, ai, br, bi);
   } else {
     move_rows<S, TT::NS, 1, CPLX, MODE, CONJ, TT::UNROLL_NARROW>(src, dst, p, ar, ai, br, bi);
@@ -319,41 +352,74 @@ costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ groups
             void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
-  __shared__ E tile_mem[HAS_T ? TT::TX : 1][HAS_T ? TT::TY + 1 : 1];
-  Tile<S, CPLX> tile = reinterpret_cast<Tile<S, CPLX>>(&tile_mem[0][0]);
+  __shared__ E lds[HAS_T ? TT::LDS_ELEMS : 1];
   const int32_t g = xcd_remap((int32_t)blockIdx.x, ngroups);
   const int32_t p0 = groups[g], p1 = groups[g + 1];
-  Piece next = pieces[p0];
-  for (int32_t pi = p0; pi < p1; ++pi) {
-    const Piece p = next;
-    if (pi + 1 < p1) next = pieces[pi + 1];  // fetch the next descriptor while this one moves
-    const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
-    S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
-    const bool wide = allow_wide && (p.flags & PIECE_WIDE);
+  int32_t pi = p0;
+  Piece ahead = pieces[p0];  // the next rectangle's descriptor, fetched while the current one moves
+  int32_t ahead_i = p0;
+  while (pi < p1) {
+    const Piece p = ahead_i == pi ? ahead : pieces[pi];
+    if (pi + 1 < p1) {
+      ahead = pieces[pi + 1];
+      ahead_i = pi + 1;
+    }
     if constexpr (KIND == KIND_PACK) {
-      move_piece<S, CPLX, MODE_COPY, false, false>(src, dst, p, wide, tile, S(0), S(0), S(0), S(0));
+      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
+      move_piece<S, CPLX, MODE_COPY, false>(reinterpret_cast<const S*>(bufs[p.src_buf]),
+                                            reinterpret_cast<S*>(bufs[p.dst_buf]), p, wide, S(0), S(0), S(0), S(0));
+      ++pi;
+      continue;
     } else {
       const ItemParam& ip = items[p.item];
+      if constexpr (HAS_T) {
+        if (p.flags & PIECE_TRANSPOSE) {
+          if constexpr (MODE != MODE_ANY) {
+            if (TT::TXN != TT::TX && (p.flags & PIECE_NARROW_T))
+              pi = move_transposed_run<S, CPLX, MODE, CONJ, TT::TXN, TT::TYN>(pieces, pi, p1, bufs, items, lds);
+            else
+              pi = move_transposed_run<S, CPLX, MODE, CONJ, TT::TX, TT::TY>(pieces, pi, p1, bufs, items, lds);
+          } else {
+            // mixed batches: one rectangle at a time, the big tile
+            const bool conj = CPLX && ip.conj;
+            constexpr int X = TT::TX, Y = TT::TY;
+            if (ip.mode == MODE_COPY)
+              pi = conj ? move_transposed_run<S, CPLX, MODE_COPY, true, X, Y>(pieces, pi, pi + 1, bufs, items, lds)
+                        : move_transposed_run<S, CPLX, MODE_COPY, false, X, Y>(pieces, pi, pi + 1, bufs, items, lds);
+            else if (ip.mode == MODE_SCALE)
+              pi = conj ? move_transposed_run<S, CPLX, MODE_SCALE, true, X, Y>(pieces, pi, pi + 1, bufs, items, lds)
+                        : move_transposed_run<S, CPLX, MODE_SCALE, false, X, Y>(pieces, pi, pi + 1, bufs, items, lds);
+            else
+              pi = conj ? move_transposed_run<S, CPLX, MODE_AXPBY, true, X, Y>(pieces, pi, pi + 1, bufs, items, lds)
+                        : move_transposed_run<S, CPLX, MODE_AXPBY, false, X, Y>(pieces, pi, pi + 1, bufs, items, lds);
+          }
+          continue;
+        }
+      }
+      const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
+      S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
+      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
       const S ar = (S)ip.alpha[0], ai = (S)ip.alpha[1], br = (S)ip.beta[0], bi = (S)ip.beta[1];
       if constexpr (MODE != MODE_ANY) {
-        move_piece<S, CPLX, MODE, CONJ, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+        move_piece<S, CPLX, MODE, CONJ>(src, dst, p, wide, ar, ai, br, bi);
       } else {
         const bool conj = CPLX && ip.conj;
         switch (ip.mode) {
           case MODE_COPY:
-            if (conj) move_piece<S, CPLX, MODE_COPY, true, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_COPY, false, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            if (conj) move_piece<S, CPLX, MODE_COPY, true>(src, dst, p, wide, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_COPY, false>(src, dst, p, wide, ar, ai, br, bi);
             break;
           case MODE_SCALE:
-            if (conj) move_piece<S, CPLX, MODE_SCALE, true, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_SCALE, false, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            if (conj) move_piece<S, CPLX, MODE_SCALE, true>(src, dst, p, wide, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_SCALE, false>(src, dst, p, wide, ar, ai, br, bi);
             break;
           default:
-            if (conj) move_piece<S, CPLX, MODE_AXPBY, true, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_AXPBY, false, HAS_T>(src, dst, p, wide, tile, ar, ai, br, bi);
+            if (conj) move_piece<S, CPLX, MODE_AXPBY, true>(src, dst, p, wide, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_AXPBY, false>(src, dst, p, wide, ar, ai, br, bi);
             break;
         }
       }
+      ++pi;
     }
   }
 }

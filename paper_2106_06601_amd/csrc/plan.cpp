@@ -215,9 +215,11 @@ void split_pieces(std::vector<Cand>& v, int64_t max_nt, int64_t t_factor) {
   v.swap(out);
 }
 
-// Marks rectangles whose non-transposed walk can use 16-byte vectors.
+// Marks rectangles whose non-transposed walk can use 16-byte vectors, and
+// narrow transposed rectangles of 16-byte elements.
 void finish_piece(Piece& p, int elem_size) {
-  p.flags &= ~PIECE_WIDE;
+  p.flags &= ~(PIECE_WIDE | PIECE_NARROW_T);
+  if ((p.flags & PIECE_TRANSPOSE) && elem_size == 16 && p.nx <= kNarrowT16) p.flags |= PIECE_NARROW_T;
   if (!(p.flags & PIECE_TRANSPOSE)) {
     int64_t want = elem_size >= 16 ? 1 : 16 / elem_size;
     if (want > 1 && p.nx % want == 0 && p.src_off % want == 0 && p.dst_off % want == 0 &&
@@ -241,7 +243,8 @@ LaunchRange add_launch(HostPlan& hp, const std::vector<Piece>& ps, const PlanCon
     lr.item_elems[ps[k].item] += (int64_t)ps[k].nx * ps[k].ny;
     if (ps[k].flags & PIECE_TRANSPOSE) lr.has_transpose = true;
     ++cnt;
-    if (acc >= cfg.min_group_elems || cnt >= cfg.max_group_pieces) {
+    const int64_t enough = (ps[k].flags & PIECE_TRANSPOSE) ? cfg.min_group_elems_t : cfg.min_group_elems;
+    if (acc >= enough || cnt >= cfg.max_group_pieces) {
       acc = 0;
       cnt = 0;
     }
@@ -251,6 +254,10 @@ LaunchRange add_launch(HostPlan& hp, const std::vector<Piece>& ps, const PlanCon
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
 }
+
+#ifndef COSTA_PACK_BY_SOURCE
+#define COSTA_PACK_BY_SOURCE 1
+#endif
 
 bool by_dst(const Piece& a, const Piece& b) {
   if (a.dst_buf != b.dst_buf) return a.dst_buf < b.dst_buf;
@@ -290,6 +297,8 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     PlanConfig g = cfg;
     g.min_group_elems = std::max<int64_t>(std::min<int64_t>(1024, cfg.min_group_elems),
                                           std::min<int64_t>(cfg.min_group_elems, total / cfg.target_groups));
+    g.min_group_elems_t = std::max<int64_t>(std::min<int64_t>(1024, cfg.min_group_elems_t),
+                                            std::min<int64_t>(cfg.min_group_elems_t, total / cfg.target_groups));
     return g;
   };
   const PlanConfig cfg_local = group_cfg(local_total), cfg_remote = group_cfg(remote_total);
@@ -352,6 +361,22 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
       off += chunk_bytes(q);
       ++k;
     }
+    // When many source rows start or end inside a 128-byte line (blocks cut
+    // by the other layout's splits), the pack walks the sources in storage
+    // order, so that rectangles sharing an edge line are read by the same or
+    // neighbouring workgroups while the line is still in L2.  Otherwise it
+    // keeps package order (sequential message writes).  The message offsets
+    // stay in package order either way.
+    int64_t partial = 0;
+    for (const Piece& pk : pack) {
+      const int64_t a = pk.src_off * es % 128, e = (pk.src_off + pk.nx) * es % 128;
+      if (a != 0 || e != 0 || (pk.ny > 1 && pk.src_ld * es % 128 != 0)) ++partial;
+    }
+    if (COSTA_PACK_BY_SOURCE && 4 * partial > (int64_t)pack.size())
+      std::sort(pack.begin(), pack.end(), [](const Piece& a, const Piece& b) {
+        if (a.src_buf != b.src_buf) return a.src_buf < b.src_buf;
+        return a.src_off < b.src_off;
+      });
     hp.pieces_pack += (int32_t)pack.size();
     hp.pieces_unpack += (int32_t)unpack.size();
     const bool last = k == remote.size();

@@ -20,6 +20,7 @@ struct PlanConfig {
   int64_t workspace_cap;   // max message bytes per wave (>= 1)
   int64_t max_piece_elems; // split rectangles larger than this
   int64_t min_group_elems; // a workgroup takes consecutive rectangles up to this many elements
+  int64_t min_group_elems_t;  // ...while they are transposed (their tiles are pipelined across rectangles)
   int32_t max_group_pieces;
   int64_t target_groups;   // aim for at least this many workgroups per launch
   int64_t transpose_piece_factor;  // transposed rectangles may be this many times larger
