@@ -91,13 +91,17 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 // direction.  dst(x, y) = dst_off + y*dst_ld + x.  The source is
 //   src_off + y*src_ld + x   (flag TRANSPOSE clear: contiguous along x), or
 //   src_off + x*src_ld + y   (flag TRANSPOSE set: contiguous along y).
-// PIECE_NARROW_T: a transposed rectangle of 16-byte elements at most
-// kNarrowT16 elements wide along the destination's contiguous direction; the
-// kernels stage it through a narrower LDS tile.
+// PIECE_NARROW_T: a transposed rectangle at most kNarrowT8 (8-byte
+// elements) or kNarrowT16 (16-byte elements) wide along the destination's
+// contiguous direction; the kernels stage it through a narrower LDS tile.
 enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_NARROW_T = 4 };
+#ifndef COSTA_NARROW_T8
+#define COSTA_NARROW_T8 16
+#endif
 #ifndef COSTA_NARROW_T16
 #define COSTA_NARROW_T16 64
 #endif
+constexpr int32_t kNarrowT8 = COSTA_NARROW_T8;
 constexpr int32_t kNarrowT16 = COSTA_NARROW_T16;
 
 struct alignas(16) Piece {

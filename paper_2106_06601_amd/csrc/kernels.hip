@@ -41,6 +41,12 @@ namespace {
 #ifndef COSTA_TILE_X16N
 #define COSTA_TILE_X16N 64  // narrow rectangles of 16-byte elements
 #endif
+#ifndef COSTA_TILE_X8N
+#define COSTA_TILE_X8N 16  // narrow rectangles of 8-byte elements
+#endif
+#ifndef COSTA_TILE_Y8N
+#define COSTA_TILE_Y8N 32
+#endif
 #ifndef COSTA_TILE_Y16N
 #define COSTA_TILE_Y16N 16
 #endif
@@ -221,10 +227,10 @@ struct TypeTraits {
   // the narrow transposed rectangles of block-cyclic layouts)
   static constexpr int TX = ES >= 16 ? COSTA_TILE_X16 : ES == 8 ? COSTA_TILE_X8 : 64;
   static constexpr int TY = ES >= 16 ? COSTA_TILE_Y16 : ES == 8 ? COSTA_TILE_Y8 : 64;
-  // rectangles marked PIECE_NARROW_T (16-byte elements only): a narrower tile
-  // keeps the store lanes busy
-  static constexpr int TXN = ES >= 16 ? COSTA_TILE_X16N : TX;
-  static constexpr int TYN = ES >= 16 ? COSTA_TILE_Y16N : TY;
+  // rectangles marked PIECE_NARROW_T: a narrower tile keeps the store lanes
+  // busy
+  static constexpr int TXN = ES >= 16 ? COSTA_TILE_X16N : ES == 8 ? COSTA_TILE_X8N : TX;
+  static constexpr int TYN = ES >= 16 ? COSTA_TILE_Y16N : ES == 8 ? COSTA_TILE_Y8N : TY;
   static constexpr int LDS_ELEMS = TX * (TY + 1) > TXN * (TYN + 1) ? TX * (TY + 1) : TXN * (TYN + 1);
 };
 

@@ -239,7 +239,9 @@ void split_pieces(std::vector<Cand>& v, int64_t max_nt, int64_t t_factor) {
 // narrow transposed rectangles of 16-byte elements.
 void finish_piece(Piece& p, int elem_size) {
   p.flags &= ~(PIECE_WIDE | PIECE_NARROW_T);
-  if ((p.flags & PIECE_TRANSPOSE) && elem_size == 16 && p.nx <= kNarrowT16) p.flags |= PIECE_NARROW_T;
+  if ((p.flags & PIECE_TRANSPOSE) &&
+      ((elem_size == 16 && p.nx <= kNarrowT16) || (elem_size == 8 && p.nx <= kNarrowT8)))
+    p.flags |= PIECE_NARROW_T;
   if (!(p.flags & PIECE_TRANSPOSE)) {
     int64_t want = elem_size >= 16 ? 1 : 16 / elem_size;
     if (want > 1 && p.nx % want == 0 && p.src_off % want == 0 && p.dst_off % want == 0 &&
