@@ -10,6 +10,10 @@ Metric: effective GB/s = model bytes per step / time per step, with model
 bytes = read B + read A (beta != 0) + write A + 2 x message bytes (each
 message element is written by the pack and read by the unpack).
 
+Also reported: the median and minimum step time (events between the timed
+steps), and the bytes a transform without message staging would move
+(read B + read A if beta != 0 + write A).
+
 Prints one JSON line.  The default workload is the ScaLAPACK-style block-size
 change: fp64 16384 x 16384, 4x4 process grid, 128x128 -> 256x256 blocks,
 identity op, alpha = 1, beta = 0, relabeling on.
@@ -33,7 +37,9 @@ KINDS = ["pack", "unpack", "direct"]
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("paper_2106_06601_amd/csrc/kernels.hip", "paper_2106_06601_amd/csrc/internal.hpp"):
+    # the kernels and what decides their launches (rectangles, groups, order)
+    for f in ("paper_2106_06601_amd/csrc/kernels.hip", "paper_2106_06601_amd/csrc/internal.hpp",
+              "paper_2106_06601_amd/csrc/plan.cpp", "paper_2106_06601_amd/csrc/api.cpp"):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -66,8 +72,21 @@ def describe(w) -> dict:
             "relabel": w.relabel, "P": it.A.nranks}
 
 
-def cpu_baseline(w, sigma, model_bytes_per_elem: float, target_s: float):
-    """The CPU oracle, single-threaded, on the first rows of A of pair 0."""
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, sigma, model_bytes_per_elem: float, target_s: float, threads: int):
+    """The CPU oracle on bands of target rows of pair 0, run by `threads`
+    threads at once (the oracle's C loop runs outside the GIL)."""
+    import threading
     import numpy as np
     import oracle
     import synth
@@ -90,24 +109,38 @@ def cpu_baseline(w, sigma, model_bytes_per_elem: float, target_s: float):
         oracle.fill(w.dtype, a, w.seed, synth.stream(synth.ROLE_A, 0, r))
         ha.append(a)
     M, N = it.A.nrows, it.A.ncols
-    # bands of target rows, in order (wrapping around), until target_s has passed
-    band = max(1, min(M, (1 << 22) // max(1, N)))
-    elems, r0 = 0, 0
+    # bands of target rows handed out in order (wrapping around) until
+    # target_s has passed
+    band = max(1, min((M + threads - 1) // threads, (1 << 22) // max(1, N)))
+    nbands = (M + band - 1) // band
+    lock = threading.Lock()
+    state = {"next": 0, "elems": 0}
     t0 = time.perf_counter()
-    while True:
-        r1 = min(M, r0 + band)
-        oracle.transform(w.dtype, it.op, it.alpha, it.beta, OA, ha, OB, hb, sigma, r0, r1)
-        elems += (r1 - r0) * N
-        r0 = 0 if r1 == M else r1
-        dt = time.perf_counter() - t0
-        if dt >= target_s:
-            break
-    return {"value": round(elems * model_bytes_per_elem / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+
+    def worker():
+        while time.perf_counter() - t0 < target_s:
+            with lock:
+                k = state["next"] % nbands
+                state["next"] += 1
+            r0 = k * band
+            r1 = min(M, r0 + band)
+            oracle.transform(w.dtype, it.op, it.alpha, it.beta, OA, ha, OB, hb, sigma, r0, r1)
+            with lock:
+                state["elems"] += (r1 - r0) * N
+
+    pool = [threading.Thread(target=worker) for _ in range(threads)]
+    for t in pool:
+        t.start()
+    for t in pool:
+        t.join()
+    dt = time.perf_counter() - t0
+    elems = state["elems"]
+    return {"value": round(elems * model_bytes_per_elem / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"{elems} elements of A in pair 0 (bands of {band} target rows of {M}, in order, "
-                      f"{elems / (M * N):.2f} passes over the {M}x{N} matrix) in {dt:.1f} s; single-threaded; "
+            "sample": f"{elems} elements of A in pair 0 (bands of {band} target rows of {M}, handed out in order, "
+                      f"{elems / (M * N):.2f} passes over the {M}x{N} matrix) in {dt:.1f} s by {threads} threads; "
                       f"same bytes-per-element model as the GPU figure",
-            "seconds": round(dt, 2)}
+            "cpu": _cpu_model(), "seconds": round(dt, 2)}
 
 
 def relabel_report() -> dict:
@@ -185,6 +218,8 @@ def main():
     ap.add_argument("--workload", default="blocksize_change_16k")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1),
+                    help="threads of the CPU baseline (default: up to 16, the host share of one GPU)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="before warm-up, run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--relabel-report", action="store_true",
@@ -259,7 +294,8 @@ def main():
     m = measure(step, stats, w.name, args)
     cpu = None
     if not args.no_cpu_baseline and len(w.items) == 1:
-        cpu = cpu_baseline(w, sigma, stats["model_bytes"] / stats["total_elems"], args.cpu_seconds)
+        cpu = cpu_baseline(w, sigma, stats["model_bytes"] / stats["total_elems"], args.cpu_seconds,
+                           max(1, args.cpu_threads))
 
     out = {
         "metric": METRIC, "value": m["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -267,7 +303,9 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "pct_of_hbm_peak": round(100 * m["value"] / HBM_PEAK_GBS, 2),
         "config": describe(w),
+        "ms_per_step_median": m["ms_per_step_median"], "ms_per_step_min": m["ms_per_step_min"],
         "model_bytes_per_step": stats["model_bytes"],
+        "bytes_without_staging_per_step": stats["model_bytes"] - 2 * stats["message_bytes"],
         "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
         "waves": m["kernels"].get("pack", {}).get("launches_per_step", 0), "plan_s": round(t_setup + m["first_step_s"], 3),
         "kernels": m["kernels"],
@@ -300,18 +338,19 @@ def measure(step, stats: dict, workload: str, args) -> dict:
     torch.cuda.synchronize()
 
     C.costa_timing_enable(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
+    ev[0].record(stream)
+    for i in range(args.steps):
         step()
-    e1.record(stream)
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     kt = C.costa_timing_read()
     C.costa_timing_enable(False)
-    gpu_ms = e0.elapsed_time(e1)
+    gpu_ms = ev[0].elapsed_time(ev[-1])
+    per_step = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
     ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
     value = stats["model_bytes"] / (ms_per_step * 1e-3) / 1e9
 
@@ -331,7 +370,8 @@ def measure(step, stats: dict, workload: str, args) -> dict:
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
             "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
     return {"value": round(value, 1), "ms_per_step": round(ms_per_step, 4), "kernels": per_kernel,
-            "roofline": roof, "first_step_s": first_step_s}
+            "roofline": roof, "first_step_s": first_step_s,
+            "ms_per_step_median": round(per_step[len(per_step) // 2], 4), "ms_per_step_min": round(per_step[0], 4)}
 
 
 def scalapack_bench(name: str, args) -> dict:
@@ -388,7 +428,9 @@ def scalapack_bench(name: str, args) -> dict:
                        "m": call.m, "n": call.n, "alpha": str(call.alpha), "beta": str(call.beta),
                        "source": dsc(call.A) + f", submatrix at ({call.ia}, {call.ja})",
                        "target": dsc(call.C) + f", submatrix at ({call.ic}, {call.jc})"},
+            "ms_per_step_median": m["ms_per_step_median"], "ms_per_step_min": m["ms_per_step_min"],
             "model_bytes_per_step": stats["model_bytes"],
+            "bytes_without_staging_per_step": stats["model_bytes"] - 2 * stats["message_bytes"],
             "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
             "kernels": m["kernels"], "roofline": m["roofline"]}
 
