@@ -23,6 +23,12 @@ namespace {
 #ifndef COSTA_UNROLL_WIDE
 #define COSTA_UNROLL_WIDE 4  // 16-byte units in flight per lane on the row walk
 #endif
+#ifndef COSTA_UNROLL_WIDE_AXPBY
+#define COSTA_UNROLL_WIDE_AXPBY 8  // ...when A is read too (beta != 0) in a launch without LDS tiles
+#endif
+#ifndef COSTA_UNROLL_NARROW16
+#define COSTA_UNROLL_NARROW16 4  // 16-byte elements in flight per lane on the row walk
+#endif
 #ifndef COSTA_XCD_REMAP
 #define COSTA_XCD_REMAP 1
 #endif
@@ -220,7 +226,7 @@ struct TypeTraits {
   static constexpr int NS = CPLX ? 2 : 1;                  // scalars per element
   static constexpr int ES = (int)sizeof(S) * NS;           // bytes per element
   static constexpr int WIDE_NEL = ES >= 16 ? 1 : 16 / ES;  // elements per 16-byte unit
-  static constexpr int UNROLL_NARROW = ES >= 16 ? 4 : 8;
+  static constexpr int UNROLL_NARROW = ES >= 16 ? COSTA_UNROLL_NARROW16 : 8;
   // transpose tile: TX elements along the destination's contiguous direction
   // (store lanes), TY along the source's (load lanes).  Long store runs pay
   // off for 16-byte elements; 8-byte elements keep 32 x 32 (occupancy, and
@@ -333,12 +339,15 @@ __device__ __forceinline__ int32_t move_transposed_run(const Piece* __restrict__
   }
 }
 
-// A rectangle whose source and destination run the same way.
-template <typename S, bool CPLX, int MODE, bool CONJ>
+// A rectangle whose source and destination run the same way.  A launch that
+// also holds transposed rectangles (HAS_T) keeps the shallower unroll: the
+// register budget of its tile path sets the launch's occupancy.
+template <typename S, bool CPLX, int MODE, bool CONJ, bool HAS_T>
 __device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p, bool wide, S ar, S ai, S br, S bi) {
   using TT = TypeTraits<S, CPLX>;
   if (wide && TT::WIDE_NEL > 1) {
-    move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, COSTA_UNROLL_WIDE>(src, dst, p, ar, ai, br, bi);
+    constexpr int U = MODE == MODE_AXPBY && !HAS_T ? COSTA_UNROLL_WIDE_AXPBY : COSTA_UNROLL_WIDE;
+    move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, U>(src, dst, p, ar, ai, br, bi);
   } else {
     move_rows<S, TT::NS, 1, CPLX, MODE, CONJ, TT::UNROLL_NARROW>(src, dst, p, ar, ai, br, bi);
   }
@@ -372,7 +381,7 @@ costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ groups
     }
     if constexpr (KIND == KIND_PACK) {
       const bool wide = allow_wide && (p.flags & PIECE_WIDE);
-      move_piece<S, CPLX, MODE_COPY, false>(reinterpret_cast<const S*>(bufs[p.src_buf]),
+      move_piece<S, CPLX, MODE_COPY, false, false>(reinterpret_cast<const S*>(bufs[p.src_buf]),
                                             reinterpret_cast<S*>(bufs[p.dst_buf]), p, wide, S(0), S(0), S(0), S(0));
       ++pi;
       continue;
@@ -407,21 +416,21 @@ costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ groups
       const bool wide = allow_wide && (p.flags & PIECE_WIDE);
       const S ar = (S)ip.alpha[0], ai = (S)ip.alpha[1], br = (S)ip.beta[0], bi = (S)ip.beta[1];
       if constexpr (MODE != MODE_ANY) {
-        move_piece<S, CPLX, MODE, CONJ>(src, dst, p, wide, ar, ai, br, bi);
+        move_piece<S, CPLX, MODE, CONJ, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
       } else {
         const bool conj = CPLX && ip.conj;
         switch (ip.mode) {
           case MODE_COPY:
-            if (conj) move_piece<S, CPLX, MODE_COPY, true>(src, dst, p, wide, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_COPY, false>(src, dst, p, wide, ar, ai, br, bi);
+            if (conj) move_piece<S, CPLX, MODE_COPY, true, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_COPY, false, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
             break;
           case MODE_SCALE:
-            if (conj) move_piece<S, CPLX, MODE_SCALE, true>(src, dst, p, wide, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_SCALE, false>(src, dst, p, wide, ar, ai, br, bi);
+            if (conj) move_piece<S, CPLX, MODE_SCALE, true, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_SCALE, false, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
             break;
           default:
-            if (conj) move_piece<S, CPLX, MODE_AXPBY, true>(src, dst, p, wide, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_AXPBY, false>(src, dst, p, wide, ar, ai, br, bi);
+            if (conj) move_piece<S, CPLX, MODE_AXPBY, true, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
+            else move_piece<S, CPLX, MODE_AXPBY, false, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
             break;
         }
       }
