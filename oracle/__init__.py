@@ -65,6 +65,7 @@ class _OLayout(ctypes.Structure):
         ("rsplit", ctypes.c_void_p), ("csplit", ctypes.c_void_p), ("owners", ctypes.c_void_p),
         ("boff", ctypes.c_void_p), ("bld", ctypes.c_void_p),
         ("rsrc", ctypes.c_int32), ("csrc", ctypes.c_int32), ("lld", ctypes.c_int64),
+        ("rank_map", ctypes.c_void_p),
     ]
 
 
@@ -126,6 +127,11 @@ class OLayout:
             s.mb, s.nb, s.prow, s.pcol = spec.mb, spec.nb, spec.nprow, spec.npcol
             s.rank_row_major = 1 if spec.rank_order == "row" else 0
             s.rsrc, s.csrc, s.lld = spec.rsrc, spec.csrc, spec.lld
+            if getattr(spec, "rank_map", None) is not None:
+                rm = np.ascontiguousarray(spec.rank_map, dtype=np.int32)
+                assert rm.size == spec.nprow * spec.npcol
+                s.rank_map = _ptr(rm)
+                self._keep = [rm]
         else:
             s.kind = 1
             rs = np.asarray(spec.row_splits, dtype=np.int64)

@@ -73,6 +73,9 @@ typedef struct {
    * extent from NUMROC, at least 1) */
   int32_t rsrc, csrc;
   int64_t lld;
+  /* block-cyclic: process at grid position (pr, pc) is rank_map[pr + pc*prow]
+   * (a BLACS-style map into nranks >= prow*pcol ranks; NULL: rank order) */
+  const int32_t* rank_map;
 } olayout;
 
 /* ScaLAPACK NUMROC: how many of n rows (or cols), dealt in blocks of nb over
@@ -113,7 +116,8 @@ static void locate(const olayout* L, int64_t i, int64_t j, int32_t* rank, int64_
      * INDXG2L); likewise for columns */
     int64_t pr = (i / L->mb + L->rsrc) % L->prow;
     int64_t pc = (j / L->nb + L->csrc) % L->pcol;
-    *rank = (int32_t)(L->rank_row_major ? pr * L->pcol + pc : pr + pc * L->prow);
+    if (L->rank_map) *rank = L->rank_map[pr + pc * L->prow];
+    else *rank = (int32_t)(L->rank_row_major ? pr * L->pcol + pc : pr + pc * L->prow);
     int64_t li = (i / (L->mb * L->prow)) * L->mb + i % L->mb;
     int64_t lj = (j / (L->nb * L->pcol)) * L->nb + j % L->nb;
     if (L->row_major) {
@@ -156,8 +160,15 @@ int oracle_default_packing(int32_t nbr, int32_t nbc, const int64_t* rsplit, cons
 /* Number of elements the buffer of `rank` must hold. */
 int64_t oracle_local_elems(const olayout* L, int32_t rank) {
   if (L->kind == O_BLOCK_CYCLIC) {
-    int64_t pr = L->rank_row_major ? rank / L->pcol : rank % L->prow;
-    int64_t pc = L->rank_row_major ? rank % L->pcol : rank / L->prow;
+    int64_t pr = -1, pc = -1;
+    if (L->rank_map) {
+      for (int64_t k = 0; k < (int64_t)L->prow * L->pcol; ++k)
+        if (L->rank_map[k] == rank) { pr = k % L->prow; pc = k / L->prow; }
+      if (pr < 0) return 0; /* not in the grid: holds nothing */
+    } else {
+      pr = L->rank_row_major ? rank / L->pcol : rank % L->prow;
+      pc = L->rank_row_major ? rank % L->pcol : rank / L->prow;
+    }
     int64_t lr = numroc(L->nrows, L->mb, pr, L->rsrc, L->prow);
     int64_t lc = numroc(L->ncols, L->nb, pc, L->csrc, L->pcol);
     if (lr == 0 || lc == 0) return 0;

@@ -208,7 +208,9 @@ class ScaLapack:
     m x n global matrix in mb x nb blocks; the first block row and column live
     on process row rsrc and process column csrc; every rank stores its local
     matrix column-major with leading dimension lld.  rank_order 'row': rank =
-    pr * npcol + pc; 'col': rank = pr + pc * nprow.
+    pr * npcol + pc; 'col': rank = pr + pc * nprow.  With rank_map (nprow *
+    npcol entries, column-major over the grid, like a BLACS user map) the
+    process at (pr, pc) is rank rank_map[pr + pc * nprow] of `world` ranks.
     """
     m: int
     n: int
@@ -221,10 +223,12 @@ class ScaLapack:
     npcol: int
     rank_order: str = "row"
     kind: str = "scalapack"
+    world: int = 0                      # ranks in all (0: nprow * npcol)
+    rank_map: Optional[List[int]] = None
 
     @property
     def nranks(self) -> int:
-        return self.nprow * self.npcol
+        return self.world or self.nprow * self.npcol
 
     @property
     def nrows(self) -> int:

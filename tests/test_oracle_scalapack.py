@@ -44,6 +44,8 @@ def _random_desc(rng, nprow=None, npcol=None, pad=None):
 
 
 def _rank(d, pr, pc):
+    if d.rank_map is not None:
+        return d.rank_map[pr + pc * d.nprow]
     return pr * d.npcol + pc if d.rank_order == "row" else pr + pc * d.nprow
 
 
@@ -200,3 +202,74 @@ def test_window_volume_matches_counting():
             s = rbm[ib + i, jb + j] if op == "N" else rbm[ib + j, jb + i]
             want[s, ra[ia + i, ja + j]] += 1
         assert np.array_equal(V, want)
+
+
+def _mapped(rng, d, world):
+    """The descriptor on `world` ranks: its grid positions take distinct
+    random ranks (column-major over the grid, like a BLACS user map)."""
+    d.world = world
+    d.rank_map = [int(x) for x in rng.permutation(world)[:d.nprow * d.npcol]]
+    return d
+
+
+def test_rank_map_storage_matches_dealing():
+    """With a rank map the grid is any subset of a larger set of ranks; ranks
+    outside it hold nothing."""
+    rng = np.random.default_rng(36)
+    for _ in range(40):
+        d = _mapped(rng, _random_desc(rng), int(rng.integers(9, 14)))
+        L = oracle.OLayout(d)
+        rank, off = _brute_map(d)
+        ii, jj = np.meshgrid(np.arange(d.m), np.arange(d.n), indexing="ij")
+        r, o = L.locate(ii.ravel(), jj.ravel())
+        assert np.array_equal(r, rank.ravel()) and np.array_equal(o, off.ravel())
+        for q in range(d.world):
+            sel = rank.ravel() == q
+            assert L.local_elems(q) == (int(off.ravel()[sel].max()) + 1 if sel.any() else 0)
+            if q not in d.rank_map:
+                assert L.local_elems(q) == 0
+
+
+def test_rank_map_identity_equals_rank_order():
+    rng = np.random.default_rng(37)
+    for order in ("row", "col"):
+        d = _random_desc(rng, 2, 3, pad=1)
+        d.rank_order = order
+        e = synth.ScaLapack(d.m, d.n, d.mb, d.nb, d.rsrc, d.csrc, d.lld, 2, 3, "row", world=6,
+                            rank_map=[(pr * 3 + pc) if order == "row" else (pr + pc * 2)
+                                      for pc in range(3) for pr in range(2)])
+        ii, jj = np.meshgrid(np.arange(d.m), np.arange(d.n), indexing="ij")
+        x = oracle.OLayout(d).locate(ii.ravel(), jj.ravel())
+        y = oracle.OLayout(e).locate(ii.ravel(), jj.ravel())
+        assert np.array_equal(x[0], y[0]) and np.array_equal(x[1], y[1])
+
+
+@pytest.mark.parametrize("routine", ["gemr2d", "tran"])
+def test_scalapack_call_between_grids_of_different_sizes(routine):
+    """pxgemr2d / pxtran between a grid and a smaller (or one-process) grid of
+    the same ranks, e.g. scattering a matrix held by one process."""
+    rng = np.random.default_rng(38 if routine == "gemr2d" else 39)
+    for trial in range(10):
+        world = int(rng.integers(4, 9))
+        shapes = [(1, 1), (1, 2), (2, 2), (2, 1), (1, 3), (3, 1), (2, 3)]
+        ok = [g for g in shapes if g[0] * g[1] <= world]
+        ga, gc = ok[int(rng.integers(len(ok)))], ok[int(rng.integers(len(ok)))]
+        dA = _mapped(rng, _random_desc(rng, *ga), world)
+        dC = _mapped(rng, _random_desc(rng, *gc), world)
+        tr = routine != "gemr2d"
+        m = min(dC.m, dA.n if tr else dA.m)
+        n = min(dC.n, dA.m if tr else dA.n)
+        m, n = int(rng.integers(0, m + 1)), int(rng.integers(0, n + 1))
+        ra, ca = (n, m) if tr else (m, n)
+        ia, ja = int(rng.integers(1, dA.m - ra + 2)), int(rng.integers(1, dA.n - ca + 2))
+        ic, jc = int(rng.integers(1, dC.m - m + 2)), int(rng.integers(1, dC.n - n + 2))
+        call = synth.ScaLapackCall(routine, "f64", m, n, 2.0, 0.5, dA, ia, ja, dC, ic, jc)
+        A_bufs = _bufs(dA, "f64", rng)
+        C_bufs = _bufs(dC, "f64", rng)
+        gA, gC0 = _gather(dA, A_bufs), _gather(dC, C_bufs)
+        oracle.scalapack_call(call, A_bufs, C_bufs)
+        want = gC0.copy()
+        src = gA[ia - 1:ia - 1 + ra, ja - 1:ja - 1 + ca]
+        win = (slice(ic - 1, ic - 1 + m), slice(jc - 1, jc - 1 + n))
+        want[win] = src if not tr else src.T * 2.0 + gC0[win] * 0.5
+        assert np.array_equal(_gather(dC, C_bufs), want)
