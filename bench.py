@@ -224,7 +224,8 @@ def main():
                     help="before warm-up, run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--relabel-report", action="store_true",
                     help="print the relabeling comparison of every workload instead of the throughput line")
-    ap.add_argument("--scalapack", metavar="NAME", choices=["pdgemr2d_16k", "pdtran_16k", "pztranc_8k"],
+    ap.add_argument("--scalapack", metavar="NAME",
+                    choices=["pdgemr2d_16k", "pdtran_16k", "pztranc_8k", "pdgemr2d_scatter_16k"],
                     help="time a ScaLAPACK-style call through its C entry point instead of the default workload")
     ap.add_argument("--bench2-sweep", action="store_true",
                     help="print the volume-reduction sweep of the paper's relabeling benchmark")
@@ -404,8 +405,8 @@ def scalapack_bench(name: str, args) -> dict:
     sub_c = LC.submatrix(call.ic - 1, call.jc - 1, call.m, call.n)
     alpha, beta = (1.0, 0.0) if not tr else (call.alpha, call.beta)
     stats = C.costa_plan_stats(call.dtype, [dict(op=op, alpha=alpha, beta=beta, A=sub_c, B=sub_a)])
-    ga = (call.A.nprow, call.A.npcol, call.A.rank_order)
-    gc = (call.C.nprow, call.C.npcol, call.C.rank_order)
+    ga = (call.A.nprow, call.A.npcol, call.A.rank_order, call.A.world, call.A.rank_map)
+    gc = (call.C.nprow, call.C.npcol, call.C.rank_order, call.C.world, call.C.rank_map)
     da, dc = call.A.desc(), call.C.desc()
     fn = {"gemr2d": None, "tran": C.costa_pdtran, "tranc": C.costa_pztranc, "tranu": C.costa_pztranu}[call.routine]
 
@@ -419,7 +420,8 @@ def scalapack_bench(name: str, args) -> dict:
     m = measure(step, stats, name, args)
 
     def dsc(d):
-        return (f"{d.m}x{d.n} in {d.mb}x{d.nb} blocks on a {d.nprow}x{d.npcol} grid ({d.rank_order}-major ranks), "
+        ranks = f"ranks {d.rank_map} of {d.nranks}" if d.rank_map is not None else f"{d.rank_order}-major ranks"
+        return (f"{d.m}x{d.n} in {d.mb}x{d.nb} blocks on a {d.nprow}x{d.npcol} grid ({ranks}), "
                 f"RSRC {d.rsrc} CSRC {d.csrc} LLD {d.lld}")
     return {"metric": METRIC, "value": m["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": m["ms_per_step"], "higher_is_better": True,

@@ -110,13 +110,20 @@ costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t ncols, int6
                                               int32_t prow, int32_t pcol, costa_order rank_order,
                                               costa_order block_order, costa_layout* out);
 
-/* A BLACS-style process grid: nprow x npcol processes numbered
- * rank = pr*npcol + pc (rank_order ROW_MAJOR, BLACS "Row") or
- * rank = pr + pc*nprow (COL_MAJOR). */
+/* A BLACS-style process grid: nprow x npcol processes out of `nranks`
+ * ranks in all (0: exactly nprow*npcol).  Without a map the process at grid
+ * position (pr, pc) is rank pr*npcol + pc (rank_order ROW_MAJOR, BLACS
+ * "Row") or pr + pc*nprow (COL_MAJOR).  rank_map (may be NULL): nprow*npcol
+ * distinct ranks in [0, nranks), column-major over the grid like a BLACS user
+ * map: the process at (pr, pc) is rank_map[pr + pc*nprow]; rank_order is then
+ * not read.  Ranks outside the grid hold nothing of the matrix.  The map is
+ * copied by the calls that take a grid. */
 typedef struct {
   int32_t nprow;
   int32_t npcol;
   costa_order rank_order;
+  int32_t nranks;
+  const int32_t* rank_map;
 } costa_grid;
 
 /* Layout of the matrix a ScaLAPACK array descriptor describes on `grid`:
@@ -127,8 +134,10 @@ typedef struct {
  * with the splits at multiples of the block size; the local view of
  * Figure 1).  CTXT_ is not read: `grid` takes the place of the BLACS context.
  * One LLD_ serves every rank, so it must be >= max(1, local rows) of every
- * process row.  Errors: NOT_SUPPORTED for DTYPE_ != 1; INVALID_VALUE for
- * negative M_/N_, MB_/NB_ < 1, RSRC_/CSRC_ outside the grid, LLD_ too small. */
+ * process row.  The layout has the grid's nranks ranks.  Errors:
+ * NOT_SUPPORTED for DTYPE_ != 1; INVALID_VALUE for negative M_/N_, MB_/NB_ < 1,
+ * RSRC_/CSRC_ outside the grid, LLD_ too small, nranks below nprow*npcol, a
+ * rank map with entries out of range or repeated. */
 costa_status costa_layout_create_scalapack(const int32_t* desc, const costa_grid* grid, costa_layout* out);
 
 /* The m x n submatrix of `parent` whose first element is the parent's
@@ -303,15 +312,17 @@ costa_status costa_plan_export(costa_dtype dtype, int32_t n, const costa_transfo
  * first element, 9-entry descriptors, m x n the shape of the destination
  * submatrix.  Each descriptor comes with its costa_grid in place of a BLACS
  * context, and each matrix is given as the P device pointers of its ranks
- * (P = nprow*npcol, the same for both grids; NULL allowed for a rank that
- * holds nothing of the submatrix).  Elements land where the destination
+ * (P = the grid's nranks, the same for both grids, which may be grids of
+ * different shapes over the same ranks, as for ScaLAPACK contexts within one
+ * union context; NULL allowed for a rank that holds nothing of the
+ * submatrix).  Elements land where the destination
  * descriptor puts them (no relabeling); elements outside the destination
  * submatrix are not touched.  m == 0 or n == 0: nothing is enqueued.
  * Asynchronous on `stream`.  The layouts of descriptor + submatrix pairs and
  * the plans are cached (until costa_finalize()), so a repeated call only
  * enqueues kernels.  Errors: those of costa_layout_create_scalapack();
  * INVALID_VALUE for negative m/n, indices below 1 or submatrices past the
- * matrix, null pointers; SHAPE_MISMATCH when the grids have different P;
+ * matrix, null pointers; SHAPE_MISMATCH when the grids have different nranks;
  * then those of costa_transform().
  * ------------------------------------------------------------------------- */
 

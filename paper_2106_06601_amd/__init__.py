@@ -53,7 +53,8 @@ class CostaPieceInfo(ctypes.Structure):
 
 
 class CostaGrid(ctypes.Structure):
-    _fields_ = [("nprow", _i32), ("npcol", _i32), ("rank_order", ctypes.c_int)]
+    _fields_ = [("nprow", _i32), ("npcol", _i32), ("rank_order", ctypes.c_int), ("nranks", _i32),
+                ("rank_map", _vp)]
 
 
 class CostaTiming(ctypes.Structure):
@@ -172,8 +173,16 @@ def costa_layout_create_block_cyclic(nrows: int, ncols: int, mb: int, nb: int, p
     return h.value
 
 
-def _grid(nprow: int, npcol: int, rank_order: str = "row") -> CostaGrid:
-    return CostaGrid(nprow, npcol, ORDERS[rank_order])
+def _grid(nprow: int, npcol: int, rank_order: str = "row", nranks: int = 0, rank_map=None) -> CostaGrid:
+    """A grid; rank_map (nprow*npcol ranks, column-major over the grid) makes
+    it a subset of `nranks` ranks.  The map array is kept on the returned
+    structure for as long as it lives."""
+    g = CostaGrid(nprow, npcol, ORDERS[rank_order], nranks, None)
+    if rank_map is not None:
+        rm = np.ascontiguousarray(rank_map, dtype=np.int32)
+        g.rank_map = rm.ctypes.data
+        g._keep = rm
+    return g
 
 
 def _desc9(desc) -> np.ndarray:
@@ -183,8 +192,9 @@ def _desc9(desc) -> np.ndarray:
     return d
 
 
-def costa_layout_create_scalapack(desc, nprow: int, npcol: int, rank_order: str = "row") -> int:
-    d, g, h = _desc9(desc), _grid(nprow, npcol, rank_order), _vp()
+def costa_layout_create_scalapack(desc, nprow: int, npcol: int, rank_order: str = "row", nranks: int = 0,
+                                  rank_map=None) -> int:
+    d, g, h = _desc9(desc), _grid(nprow, npcol, rank_order, nranks, rank_map), _vp()
     _check(_lib.costa_layout_create_scalapack(d.ctypes.data, ctypes.byref(g), ctypes.byref(h)),
            "costa_layout_create_scalapack")
     return h.value
@@ -371,7 +381,7 @@ def costa_plan_export(dtype: str, descs: Sequence[dict], sigma=None) -> np.ndarr
 
 # ---------------------------------------------------------------------------
 # ScaLAPACK-compatible routines (1-based indices, 9-entry descriptors; a grid
-# is (nprow, npcol, rank_order))
+# is (nprow, npcol, rank_order[, nranks, rank_map]))
 # ---------------------------------------------------------------------------
 def _sl_args(a, ia, ja, desca, grida, c, ic, jc, descc, gridc, keep):
     da, dc = _desc9(desca), _desc9(descc)
@@ -464,6 +474,7 @@ def layout_from_spec(spec) -> Layout:
         return Layout.block_cyclic(spec.nrows, spec.ncols, spec.mb, spec.nb, spec.prow, spec.pcol,
                                    spec.rank_order, spec.block_order)
     if spec.kind == "scalapack":
-        return Layout.scalapack(spec.desc(), spec.nprow, spec.npcol, spec.rank_order)
+        return Layout.scalapack(spec.desc(), spec.nprow, spec.npcol, spec.rank_order, getattr(spec, "world", 0),
+                                getattr(spec, "rank_map", None))
     return Layout.general(spec.nrows, spec.ncols, spec.row_splits, spec.col_splits, spec.owners, spec.nranks,
                           spec.block_order)

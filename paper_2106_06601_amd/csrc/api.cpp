@@ -625,7 +625,8 @@ extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, 
     return fail(COSTA_ERROR_NOT_SUPPORTED, "more than 2^31 overlay intervals in one dimension");
   State& S = state();
   std::lock_guard<std::mutex> lock(S.mu);
-  const bool separable = A->block_cyclic && B->block_cyclic;
+  // the separable kernels number the ranks of a grid by its rank order
+  const bool separable = A->block_cyclic && B->block_cyclic && A->rank_map.empty() && B->rank_map.empty();
   DevBuf d_rows, d_cols, d_oa, d_ob, d_v, d_hr, d_hc;
   std::vector<unsigned long long> zeros;
   hipEvent_t e0 = nullptr, e1 = nullptr;

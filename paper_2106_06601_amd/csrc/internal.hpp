@@ -46,11 +46,13 @@ struct Layout {
   int64_t r0 = 0, c0 = 0;            // window origin in the full matrix
   int64_t rb0 = 0, cb0 = 0;          // r0 / mb, c0 / nb
   std::vector<int64_t> lrows, lcols;  // local extents of the full matrix per process row / column
+  std::vector<int32_t> rank_map;      // empty, or the rank of grid position (pr, pc) at pr + pc*prow
 
   int64_t block(int32_t bi, int32_t bj) const { return (int64_t)bi * nbc + bj; }
   int32_t prow_of(int32_t bi) const { return (int32_t)((rb0 + bi + rsrc) % prow); }
   int32_t pcol_of(int32_t bj) const { return (int32_t)((cb0 + bj + csrc) % pcol); }
   int32_t rank_at(int32_t pr, int32_t pc) const {
+    if (!rank_map.empty()) return rank_map[(size_t)pr + (size_t)pc * prow];
     return rank_order == COSTA_ROW_MAJOR ? pr * pcol + pc : pr + pc * prow;
   }
   int32_t owner_of(int32_t bi, int32_t bj) const {

@@ -187,7 +187,8 @@ static costa_status set_window(Layout& L, int64_t r0, int64_t c0, int64_t m, int
 // Block-cyclic layout of a whole matrix dealt from process (rsrc, csrc).
 static costa_status make_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, int64_t nb, int32_t prow,
                                       int32_t pcol, int32_t rsrc, int32_t csrc, int64_t lld, costa_order rank_order,
-                                      costa_order block_order, costa_layout* out) {
+                                      costa_order block_order, int32_t nranks, const int32_t* rank_map,
+                                      costa_layout* out) {
   if (nrows < 0 || ncols < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative dimension");
   if (mb < 1 || nb < 1) return fail(COSTA_ERROR_INVALID_VALUE, "block sizes must be >= 1");
   if (prow < 1 || pcol < 1) return fail(COSTA_ERROR_INVALID_VALUE, "process grid must be at least 1x1");
@@ -198,10 +199,24 @@ static costa_status make_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, 
     return fail(COSTA_ERROR_INVALID_VALUE, "unknown block order");
   if ((nrows + mb - 1) / mb > INT32_MAX || (ncols + nb - 1) / nb > INT32_MAX)
     return fail(COSTA_ERROR_INVALID_VALUE, "too many blocks");
+  const int32_t grid_size = prow * pcol;
+  if (nranks == 0) nranks = grid_size;
+  if (nranks < grid_size) return fail(COSTA_ERROR_INVALID_VALUE, "fewer ranks than grid positions");
+  if (!rank_map && nranks != grid_size)
+    return fail(COSTA_ERROR_INVALID_VALUE, "a grid smaller than its set of ranks needs a rank map");
+  if (rank_map) {
+    std::vector<char> seen(nranks, 0);
+    for (int32_t k = 0; k < grid_size; ++k) {
+      if (rank_map[k] < 0 || rank_map[k] >= nranks || seen[rank_map[k]])
+        return fail(COSTA_ERROR_INVALID_VALUE, "rank map entries must be distinct ranks in [0, nranks)");
+      seen[rank_map[k]] = 1;
+    }
+  }
   costa_layout_s* h = new (std::nothrow) costa_layout_s();
   if (!h) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
   Layout& L = h->L;
-  L.nranks = prow * pcol;
+  L.nranks = nranks;
+  if (rank_map) L.rank_map.assign(rank_map, rank_map + grid_size);
   L.order = block_order;
   L.block_cyclic = true;
   L.prow = prow;
@@ -241,7 +256,7 @@ extern "C" costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t 
                                                          costa_order block_order, costa_layout* out) {
   if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
   *out = nullptr;
-  return make_block_cyclic(nrows, ncols, mb, nb, prow, pcol, 0, 0, 0, rank_order, block_order, out);
+  return make_block_cyclic(nrows, ncols, mb, nb, prow, pcol, 0, 0, 0, rank_order, block_order, 0, nullptr, out);
 }
 
 extern "C" costa_status costa_layout_create_scalapack(const int32_t* desc, const costa_grid* grid,
@@ -254,8 +269,10 @@ extern "C" costa_status costa_layout_create_scalapack(const int32_t* desc, const
   if (desc[6] < 0 || desc[6] >= grid->nprow) return fail(COSTA_ERROR_INVALID_VALUE, "RSRC_ outside the process grid");
   if (desc[7] < 0 || desc[7] >= grid->npcol) return fail(COSTA_ERROR_INVALID_VALUE, "CSRC_ outside the process grid");
   if (desc[8] < 1) return fail(COSTA_ERROR_INVALID_VALUE, "LLD_ must be >= 1");
+  if (grid->nranks < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative number of ranks");
   return make_block_cyclic(desc[2], desc[3], desc[4], desc[5], grid->nprow, grid->npcol, desc[6], desc[7], desc[8],
-                           grid->rank_order, COSTA_COL_MAJOR, out);
+                           grid->rank_map ? COSTA_ROW_MAJOR : grid->rank_order, COSTA_COL_MAJOR, grid->nranks,
+                           grid->rank_map, out);
 }
 
 extern "C" costa_status costa_layout_submatrix(costa_layout parent, int64_t i0, int64_t j0, int64_t m, int64_t n,

@@ -5,7 +5,6 @@
 // cached by descriptor, grid and window (a block-cyclic layout is a few
 // hundred bytes, whatever the matrix size) until costa_finalize, so that
 // repeated calls keep the same layouts and therefore find their cached plans.
-#include <array>
 #include <map>
 #include <mutex>
 
@@ -14,8 +13,9 @@
 namespace costa {
 namespace {
 
-// M_, N_, MB_, NB_, RSRC_, CSRC_, LLD_, nprow, npcol, rank order, i0, j0, m, n
-using Key = std::array<int64_t, 14>;
+// M_, N_, MB_, NB_, RSRC_, CSRC_, LLD_, nprow, npcol, rank order, nranks, i0,
+// j0, m, n, then the rank map if there is one
+using Key = std::vector<int64_t>;
 
 struct Cache {
   std::mutex mu;
@@ -40,8 +40,10 @@ costa_status window_layout(const char* name, const int32_t* desc, const costa_gr
   if (i1 < 1 || j1 < 1) return fail(COSTA_ERROR_INVALID_VALUE, std::string("indices of ") + name + " below 1");
   if ((int64_t)i1 - 1 + rows > desc[2] || (int64_t)j1 - 1 + cols > desc[3])
     return fail(COSTA_ERROR_INVALID_VALUE, std::string("submatrix of ") + name + " past the matrix");
-  const Key key{desc[2], desc[3], desc[4], desc[5], desc[6], desc[7], desc[8], grid->nprow, grid->npcol,
-                (int64_t)grid->rank_order, (int64_t)i1 - 1, (int64_t)j1 - 1, rows, cols};
+  if (grid->nprow < 1 || grid->npcol < 1) return fail(COSTA_ERROR_INVALID_VALUE, "process grid must be at least 1x1");
+  Key key{desc[2], desc[3], desc[4], desc[5], desc[6], desc[7], desc[8], grid->nprow, grid->npcol,
+          (int64_t)grid->rank_order, grid->nranks, (int64_t)i1 - 1, (int64_t)j1 - 1, rows, cols};
+  if (grid->rank_map) key.insert(key.end(), grid->rank_map, grid->rank_map + (size_t)grid->nprow * grid->npcol);
   Cache& C = cache();
   std::lock_guard<std::mutex> lock(C.mu);
   auto it = C.layouts.find(key);
@@ -71,8 +73,9 @@ costa_status scalapack_transform(costa_dtype dtype, costa_op op, int32_t m, int3
   if (st != COSTA_SUCCESS) return st;
   st = check_desc("the destination", descd, gridd);
   if (st != COSTA_SUCCESS) return st;
-  if ((int64_t)grids->nprow * grids->npcol != (int64_t)gridd->nprow * gridd->npcol)
-    return fail(COSTA_ERROR_SHAPE_MISMATCH, "the two process grids have different numbers of processes");
+  auto world = [](const costa_grid* g) { return g->nranks ? (int64_t)g->nranks : (int64_t)g->nprow * g->npcol; };
+  if (world(grids) != world(gridd))
+    return fail(COSTA_ERROR_SHAPE_MISMATCH, "the two process grids live on different numbers of ranks");
   if (m == 0 || n == 0) return COSTA_SUCCESS;
   if (!src || !dst) return fail(COSTA_ERROR_INVALID_VALUE, "null buffer array");
   const bool tr = op != COSTA_OP_N;

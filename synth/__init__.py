@@ -377,7 +377,10 @@ def scalapack_call(name: str, scale: str = "full") -> ScaLapackCall:
     process grid, fp64, 32 x 32 source blocks -> 128 x 128 target blocks, the
     source a submatrix starting mid-block of a larger matrix, the target's
     first block on process (3, 5), padded leading dimensions; at full size
-    ('full', 16384^2) or with the same grids and blocks at 2048^2 ('small')."""
+    ('full', 16384^2) or with the same grids and blocks at 2048^2 ('small').
+    pztranc_8k is the complex conjugate transpose on 8 x 8 grids, and
+    pdgemr2d_scatter_16k deals a matrix held by one process out to a 4 x 4
+    grid of the same 16 ranks."""
     small = scale == "small"
     n = 2048 if small else 16384
     big = n + 512
@@ -387,6 +390,11 @@ def scalapack_call(name: str, scale: str = "full") -> ScaLapackCall:
         return ScaLapackCall("gemr2d", "f64", n, n, 1.0, 0.0, src, 17, 273, dst, 1, 1)
     if name == "pdtran_16k":
         return ScaLapackCall("tran", "f64", n, n, 1.0, 0.0, src, 17, 273, dst, 1, 1)
+    if name == "pdgemr2d_scatter_16k":
+        # a matrix held by one process (rank 0 of 16) dealt out to a 4 x 4 grid
+        root = ScaLapack(n, n, 128, 128, 0, 0, n, 1, 1, world=16, rank_map=[0])
+        grid = ScaLapack(n, n, 128, 128, 0, 0, _lld(n, 128, 4, 0), 4, 4)
+        return ScaLapackCall("gemr2d", "f64", n, n, 1.0, 0.0, root, 1, 1, grid, 1, 1)
     if name == "pztranc_8k":
         m = 1024 if small else 8192
         a = ScaLapack(m + 100, m + 100, 64, 64, 1, 2, _lld(m + 100, 64, 8, 4), 8, 8, "col")
@@ -395,4 +403,4 @@ def scalapack_call(name: str, scale: str = "full") -> ScaLapackCall:
     raise KeyError(name)
 
 
-SCALAPACK_CALLS = ["pdgemr2d_16k", "pdtran_16k", "pztranc_8k"]
+SCALAPACK_CALLS = ["pdgemr2d_16k", "pdtran_16k", "pztranc_8k", "pdgemr2d_scatter_16k"]

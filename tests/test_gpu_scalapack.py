@@ -29,7 +29,7 @@ def _bits(x, dtype):
 
 
 def _grid(d):
-    return (d.nprow, d.npcol, d.rank_order)
+    return (d.nprow, d.npcol, d.rank_order, d.world, d.rank_map)
 
 
 class SLCase:
@@ -124,8 +124,14 @@ class SLCase:
         # process row of each window row and process column of each window column
         rr, _ = self.OC.locate(wr + c.ic - 1, np.full(c.m, c.jc - 1))
         rc, _ = self.OC.locate(np.full(c.n, c.ic - 1), wc + c.jc - 1)
-        prow_of = (lambda r: r // c.C.npcol) if c.C.rank_order == "row" else (lambda r: r % c.C.nprow)
-        pcol_of = (lambda r: r % c.C.npcol) if c.C.rank_order == "row" else (lambda r: r // c.C.nprow)
+        if c.C.rank_map is not None:
+            where = {rk: (k % c.C.nprow, k // c.C.nprow) for k, rk in enumerate(c.C.rank_map)}
+            prow_of = np.vectorize(lambda r: where[int(r)][0])
+            pcol_of = np.vectorize(lambda r: where[int(r)][1])
+        elif c.C.rank_order == "row":
+            prow_of, pcol_of = (lambda r: r // c.C.npcol), (lambda r: r % c.C.npcol)
+        else:
+            prow_of, pcol_of = (lambda r: r % c.C.nprow), (lambda r: r // c.C.nprow)
         for q in ranks:
             pr, pc = prow_of(q), pcol_of(q)
             rows = wr[prow_of(rr) == pr]
@@ -208,7 +214,8 @@ def test_scalapack_full_size(name):
     if call.beta == 0:
         k.run(named=True)  # the cached plan again: the same result
     P = call.C.nranks
-    k.check_ranks_and_samples([0, 1, P // 2 + 3, P - 1])
+    held = [q for q in range(P) if k.OC.local_elems(q)]
+    k.check_ranks_and_samples(sorted({held[0], held[1 % len(held)], held[len(held) // 2], held[-1]}))
 
 
 def test_scalapack_alternating_windows_and_empty_calls():
@@ -261,3 +268,38 @@ def test_window_volume_matrix_matches_oracle(seed):
     want = oracle.volume_window(oracle.OLayout(call.C), call.ic - 1, call.jc - 1, oracle.OLayout(G), i0, j0,
                                 call.m, call.n, op)
     assert np.array_equal(V, want)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_scalapack_between_grids_of_different_sizes(seed):
+    """pxgemr2d / pxtran between grids of different shapes over one set of
+    ranks (BLACS-style rank maps): scatter from one process, gather to one
+    process, mixed grids; ranks outside a grid pass NULL."""
+    rng = np.random.default_rng(4000 + seed)
+    routine = ["gemr2d", "tran", "tranc", "gemr2d"][seed % 4]
+    dtype = ["f64", "c128"][(seed // 4) % 2]
+    world = int(rng.integers(6, 17))
+    pairs = [((1, 1), (2, 3)), ((2, 3), (1, 1)), ((1, 2), (3, 2)), ((2, 2), (1, 3))]
+    ga, gc = pairs[seed % len(pairs)]
+
+    def desc(grid):
+        m, n = int(rng.integers(1, 300)), int(rng.integers(1, 300))
+        mb, nb = int(rng.integers(1, 50)), int(rng.integers(1, 50))
+        rsrc, csrc = int(rng.integers(0, grid[0])), int(rng.integers(0, grid[1]))
+        lr = max(oracle.numroc(m, mb, p, rsrc, grid[0]) for p in range(grid[0]))
+        return synth.ScaLapack(m, n, mb, nb, rsrc, csrc, max(1, lr) + 3, grid[0], grid[1], "row", world=world,
+                               rank_map=[int(x) for x in rng.permutation(world)[:grid[0] * grid[1]]])
+
+    dA, dC = desc(ga), desc(gc)
+    tr = routine != "gemr2d"
+    mmax, nmax = min(dC.m, dA.n if tr else dA.m), min(dC.n, dA.m if tr else dA.n)
+    m, n = int(rng.integers(1, mmax + 1)), int(rng.integers(1, nmax + 1))
+    ra, ca = (n, m) if tr else (m, n)
+    ia, ja = int(rng.integers(1, dA.m - ra + 2)), int(rng.integers(1, dA.n - ca + 2))
+    ic, jc = int(rng.integers(1, dC.m - m + 2)), int(rng.integers(1, dC.n - n + 2))
+    alpha, beta = (2 - 1j, 0.5) if dtype == "c128" else (2.0, 0.5)
+    call = synth.ScaLapackCall(routine, dtype, m, n, alpha, beta, dA, ia, ja, dC, ic, jc)
+    _say(f"scalapack grids {ga} -> {gc} of {world} ranks: {routine} {dtype} {m}x{n}")
+    k = SLCase(call, seed=seed, null_idle=True)
+    k.run()
+    k.check_full()

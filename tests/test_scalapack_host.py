@@ -263,3 +263,65 @@ def test_full_size_scalapack_plans_stay_in_bounds(name):
     assert (src_end < sizes[x["src_buf"]]).all() and (dst_end < sizes[x["dst_buf"]]).all()
     assert (nx >= 1).all() and (ny >= 1).all() and ((ny == 1) | (x["dst_ld"] >= nx)).all()
     assert (nx * ny)[x["kind"] != PACK].sum() == st["total_elems"] == call.m * call.n
+
+
+def _mapped(rng, d, world):
+    d.world = world
+    d.rank_map = [int(x) for x in rng.permutation(world)[:d.nprow * d.npcol]]
+    return d
+
+
+def test_rank_mapped_layouts_match_oracle():
+    rng = np.random.default_rng(43)
+    for _ in range(30):
+        pr, pc = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        d = _mapped(rng, _random_desc(rng, pr, pc), int(rng.integers(pr * pc, pr * pc + 5)))
+        L = C.layout_from_spec(d)
+        O = oracle.OLayout(d)
+        assert C.costa_layout_info(L.handle)["nranks"] == d.world
+        assert [L.local_elems(q) for q in range(d.world)] == [O.local_elems(q) for q in range(d.world)]
+        _set_extents(L, d, 0, 0, d.m, d.n)
+        _window_elements_match(L, O, 0, 0)
+        m, n = int(rng.integers(0, d.m + 1)), int(rng.integers(0, d.n + 1))
+        i0, j0 = int(rng.integers(0, d.m - m + 1)), int(rng.integers(0, d.n - n + 1))
+        S = L.submatrix(i0, j0, m, n)
+        _set_extents(S, d, i0, j0, m, n)
+        _window_elements_match(S, O, i0, j0)
+
+
+def test_rank_map_errors():
+    good = [1, 0, 10, 10, 2, 2, 0, 0, 6]
+    assert _status(C.costa_layout_create_scalapack, good, 2, 2, "row", 6, [5, 0, 2, 3]) == C.SUCCESS
+    assert _status(C.costa_layout_create_scalapack, good, 2, 2, "row", 6, [5, 0, 2, 6]) == C.INVALID_VALUE
+    assert _status(C.costa_layout_create_scalapack, good, 2, 2, "row", 6, [5, 0, 5, 3]) == C.INVALID_VALUE
+    assert _status(C.costa_layout_create_scalapack, good, 2, 2, "row", 3, [0, 1, 2, 3]) == C.INVALID_VALUE
+    assert _status(C.costa_layout_create_scalapack, good, 2, 2, "row", 6) == C.INVALID_VALUE  # no map
+    one = [1, 0, 10, 10, 2, 2, 0, 0, 10]
+    bufs = [0x1000] * 6
+    # grids over different numbers of ranks
+    assert _status(C.costa_pdgemr2d, 4, 4, bufs, 1, 1, one, (1, 1, "row", 5, [0]), bufs, 1, 1, good,
+                   (2, 2, "row", 6, [0, 1, 2, 3]), stream=0) == C.SHAPE_MISMATCH
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_replay_calls_between_grids_of_different_sizes(seed):
+    """pxgemr2d / pxtran between grids of different shapes over one set of
+    ranks: scatter from one process, gather to one process, and mixed grids."""
+    rng = np.random.default_rng(300 + seed)
+    routine = ["gemr2d", "tran", "tranc", "gemr2d"][seed % 4]
+    dtype = ["f64", "c128"][(seed // 4) % 2]
+    world = int(rng.integers(4, 9))
+    pairs = [((1, 1), (2, 2)), ((2, 2), (1, 1)), ((1, 2), (2, 1)), ((2, 2), (1, 3)), ((1, 1), (1, 4))]
+    ga, gc = pairs[seed % len(pairs)]
+    dA = _mapped(rng, _random_desc(rng, *ga, maxdim=70), world)
+    dC = _mapped(rng, _random_desc(rng, *gc, maxdim=70), world)
+    tr = routine != "gemr2d"
+    mmax, nmax = min(dC.m, dA.n if tr else dA.m), min(dC.n, dA.m if tr else dA.n)
+    if mmax == 0 or nmax == 0:
+        return
+    m, n = int(rng.integers(1, mmax + 1)), int(rng.integers(1, nmax + 1))
+    ra, ca = (n, m) if tr else (m, n)
+    ia, ja = int(rng.integers(1, dA.m - ra + 2)), int(rng.integers(1, dA.n - ca + 2))
+    ic, jc = int(rng.integers(1, dC.m - m + 2)), int(rng.integers(1, dC.n - n + 2))
+    alpha, beta = (2 - 1j, 0.5) if dtype == "c128" else (2.0, 0.5)
+    _replay_call(synth.ScaLapackCall(routine, dtype, m, n, alpha, beta, dA, ia, ja, dC, ic, jc))
