@@ -325,3 +325,33 @@ def test_replay_calls_between_grids_of_different_sizes(seed):
     ic, jc = int(rng.integers(1, dC.m - m + 2)), int(rng.integers(1, dC.n - n + 2))
     alpha, beta = (2 - 1j, 0.5) if dtype == "c128" else (2.0, 0.5)
     _replay_call(synth.ScaLapackCall(routine, dtype, m, n, alpha, beta, dA, ia, ja, dC, ic, jc))
+
+
+@pytest.mark.parametrize("order", ["row", "col"])
+def test_general_window_random_grids(order):
+    """Windows of random general grids in either storage order: every element
+    of the window keeps its owner and offset (oracle storage map)."""
+    rng = np.random.default_rng(44 if order == "row" else 45)
+    for _ in range(10):
+        M, N, P = int(rng.integers(1, 80)), int(rng.integers(1, 80)), int(rng.integers(1, 6))
+        nr, nc = int(rng.integers(1, min(M, 6) + 1)), int(rng.integers(1, min(N, 6) + 1))
+        rs = [0] + sorted(rng.choice(np.arange(1, M), nr - 1, replace=False).tolist()) + [M] if nr > 1 else [0, M]
+        cs = [0] + sorted(rng.choice(np.arange(1, N), nc - 1, replace=False).tolist()) + [N] if nc > 1 else [0, N]
+        spec = synth.General(M, N, rs, cs, rng.integers(0, P, (len(rs) - 1) * (len(cs) - 1)).tolist(), P, order)
+        L = C.layout_from_spec(spec)
+        O = oracle.OLayout(spec)
+        m, n = int(rng.integers(1, M + 1)), int(rng.integers(1, N + 1))
+        i0, j0 = int(rng.integers(0, M - m + 1)), int(rng.integers(0, N - n + 1))
+        S = L.submatrix(i0, j0, m, n)
+        info = C.costa_layout_info(S.handle)
+        wr = [0] + [x - i0 for x in rs if i0 < x < i0 + m] + [m]
+        wc = [0] + [x - j0 for x in cs if j0 < x < j0 + n] + [n]
+        assert (info["nbr"], info["nbc"], info["block_order"]) == (len(wr) - 1, len(wc) - 1, order)
+        for bi in range(len(wr) - 1):
+            for bj in range(len(wc) - 1):
+                o, boff, ld = C.costa_layout_block(S.handle, bi, bj)
+                h, w = wr[bi + 1] - wr[bi], wc[bj + 1] - wc[bj]
+                ii, jj = np.meshgrid(np.arange(h), np.arange(w), indexing="ij")
+                rank, off = O.locate((ii + i0 + wr[bi]).ravel(), (jj + j0 + wc[bj]).ravel())
+                mine = boff + (ii * ld + jj if order == "row" else ii + jj * ld)
+                assert (rank == o).all() and np.array_equal(off, mine.ravel())
