@@ -19,7 +19,7 @@ LIB_PATH = os.environ.get("COSTA_LIB") or os.path.join(_HERE, "libcosta_mi355x.s
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
-                      "(python -m paper_2106_06601_amd.build)")
+                      "(or python paper_2106_06601_amd/build.py)")
 
 _lib = ctypes.CDLL(LIB_PATH)
 
