@@ -292,9 +292,11 @@ costa_status costa_plan_stats(costa_dtype dtype, int32_t n, const costa_transfor
 typedef struct {
   int32_t kind;   /* costa_kernel_kind: PACK, UNPACK or DIRECT */
   int32_t wave;   /* message round (0 for DIRECT) */
-  int64_t group;  /* workgroup of its launch that processes it */
+  int64_t group;  /* first workgroup of its launch that moves it */
   int64_t src_off, dst_off, src_ld, dst_ld;
   int32_t src_buf, dst_buf, nx, ny, item, flags;
+  int64_t ntasks; /* workgroups that move it (LDS tiles or row-walk chunks); small
+                     rectangles moved together by one workgroup report 1 each */
 } costa_piece_info;
 
 /* Writes the rectangles of the plan a transform with these arguments would

@@ -15,31 +15,10 @@
 namespace costa {
 namespace {
 
-// Work sizes (measured on MI355X): rectangles of at most 16K elements (times
-// COSTA_T_PIECE_FACTOR when transposed), and a workgroup takes consecutive
-// rectangles until it holds 512 elements, i.e. small rectangles get a
-// workgroup each; transposed 8-byte rectangles are grouped up to 4096
-// elements (four 32 x 32 tiles, pipelined across rectangles), transposed
-// 16-byte ones stay one per workgroup.
-#ifndef COSTA_MAX_PIECE_ELEMS
-#define COSTA_MAX_PIECE_ELEMS (1 << 14)
-#endif
-#ifndef COSTA_MIN_GROUP_ELEMS
-#define COSTA_MIN_GROUP_ELEMS 512
-#endif
-#ifndef COSTA_MIN_GROUP_ELEMS_T
-#define COSTA_MIN_GROUP_ELEMS_T 512
-#endif
-#ifndef COSTA_MIN_GROUP_ELEMS_T8
-#define COSTA_MIN_GROUP_ELEMS_T8 4096
-#endif
-#ifndef COSTA_T_PIECE_FACTOR
-#define COSTA_T_PIECE_FACTOR 1
-#endif
-constexpr int64_t kMaxPieceElems = COSTA_MAX_PIECE_ELEMS;
-int64_t min_group_elems(int) { return COSTA_MIN_GROUP_ELEMS; }
-constexpr int32_t kMaxGroupPieces = 64;
-constexpr int64_t kTargetGroups = 4096;
+// Rectangles are cut at 4M elements: the kernels index a rectangle's
+// elements in 32 bits and compute row and column from a float estimate of
+// the quotient, exact up to one correction step below 2^24 units.
+constexpr int64_t kMaxPieceElems = 1 << 22;
 
 int elem_size(costa_dtype d) {
   switch (d) {
@@ -63,7 +42,7 @@ struct DevicePlan {
   HostPlan host;
   int device = -1;
   Piece* d_pieces = nullptr;
-  int32_t* d_groups = nullptr;
+  int32_t* d_tasks = nullptr;
   // per-call table: buffer pointers then pair parameters
   void* d_table = nullptr;
   void* h_staging = nullptr;  // pinned
@@ -74,7 +53,7 @@ struct DevicePlan {
   bool table_pending = false;
   ~DevicePlan() {
     if (d_pieces) (void)hipFree(d_pieces);
-    if (d_groups) (void)hipFree(d_groups);
+    if (d_tasks) (void)hipFree(d_tasks);
     if (d_table) (void)hipFree(d_table);
     if (h_staging) (void)hipHostFree(h_staging);
     if (table_event) (void)hipEventDestroy(table_event);
@@ -138,11 +117,6 @@ PlanConfig make_config(int es) {
   c.elem_size = es;
   c.workspace_cap = INT64_MAX;
   c.max_piece_elems = kMaxPieceElems;
-  c.min_group_elems = min_group_elems(es);
-  c.min_group_elems_t = es == 8 ? COSTA_MIN_GROUP_ELEMS_T8 : COSTA_MIN_GROUP_ELEMS_T;
-  c.max_group_pieces = kMaxGroupPieces;
-  c.target_groups = kTargetGroups;
-  c.transpose_piece_factor = COSTA_T_PIECE_FACTOR;
   return c;
 }
 
@@ -254,7 +228,7 @@ costa_status collect_timing(State& S) {
 costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePlan& dp, const LaunchRange& lr,
                        int32_t mode, int32_t conj, void* const* d_bufs, const ItemParam* d_items, int32_t allow_wide,
                        int64_t bytes, hipStream_t stream) {
-  if (lr.ngroups == 0) return COSTA_SUCCESS;
+  if (lr.ntasks == 0) return COSTA_SUCCESS;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (S.timing) {
     if (S.pending.size() > 4096) {
@@ -267,7 +241,7 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePla
     HIP_OR_FAIL(hipEventRecord(e0, stream));
   }
   LaunchSpec spec{mode, conj, lr.has_transpose};
-  HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_groups + lr.group_begin, lr.ngroups, d_bufs, d_items,
+  HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_tasks + lr.task_begin, lr.ntasks, d_bufs, d_items,
                            allow_wide, stream));
   if (S.timing) {
     HIP_OR_FAIL(hipEventRecord(e1, stream));
@@ -349,8 +323,8 @@ costa_status get_plan(State& S, costa_dtype dt, const std::vector<ItemDesc>& ite
   if (!hp.pieces.empty()) {
     HIP_OR_FAIL(hipMalloc(&dp->d_pieces, hp.pieces.size() * sizeof(Piece)));
     HIP_OR_FAIL(hipMemcpy(dp->d_pieces, hp.pieces.data(), hp.pieces.size() * sizeof(Piece), hipMemcpyHostToDevice));
-    HIP_OR_FAIL(hipMalloc(&dp->d_groups, hp.groups.size() * sizeof(int32_t)));
-    HIP_OR_FAIL(hipMemcpy(dp->d_groups, hp.groups.data(), hp.groups.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    HIP_OR_FAIL(hipMalloc(&dp->d_tasks, hp.tasks.size() * sizeof(int32_t)));
+    HIP_OR_FAIL(hipMemcpy(dp->d_tasks, hp.tasks.data(), hp.tasks.size() * sizeof(int32_t), hipMemcpyHostToDevice));
   }
   const int32_t P = items.empty() ? 0 : items[0].A->nranks;
   dp->nbufs = (size_t)2 * items.size() * P + 1;
@@ -513,25 +487,33 @@ extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const co
   if (st != COSTA_SUCCESS) return st;
   int64_t k = 0;
   auto emit = [&](const LaunchRange& lr, costa_kernel_kind kind, int32_t wave) {
-    for (int64_t g = 0; g < lr.ngroups; ++g)
-      for (int32_t p = hp->groups[lr.group_begin + g]; p < hp->groups[lr.group_begin + g + 1]; ++p, ++k) {
-        if (k >= capacity) continue;
-        const Piece& q = hp->pieces[p];
-        costa_piece_info& o = out[k];
-        o.kind = kind;
-        o.wave = wave;
-        o.group = g;
-        o.src_off = q.src_off;
-        o.dst_off = q.dst_off;
-        o.src_ld = q.src_ld;
-        o.dst_ld = q.dst_ld;
-        o.src_buf = q.src_buf;
-        o.dst_buf = q.dst_buf;
-        o.nx = q.nx;
-        o.ny = q.ny;
-        o.item = q.item;
-        o.flags = q.flags;
-      }
+    for (int64_t i = 0; i < lr.npieces; ++i, ++k) {
+      if (k >= capacity) continue;
+      const Piece& q = hp->pieces[lr.piece_begin + i];
+      // workgroups that move it: from task0 up to the next rectangle's first
+      // one (or the launch's end); 1 for a rectangle that shares a workgroup
+      int64_t end = lr.ntasks;
+      for (int64_t j = i + 1; j < lr.npieces; ++j)
+        if (hp->pieces[lr.piece_begin + j].task0 != q.task0) {
+          end = hp->pieces[lr.piece_begin + j].task0;
+          break;
+        }
+      costa_piece_info& o = out[k];
+      o.kind = kind;
+      o.wave = wave;
+      o.group = q.task0;
+      o.src_off = q.src_off;
+      o.dst_off = q.dst_off;
+      o.src_ld = q.src_ld;
+      o.dst_ld = q.dst_ld;
+      o.src_buf = q.src_buf;
+      o.dst_buf = q.dst_buf;
+      o.nx = q.nx;
+      o.ny = q.ny;
+      o.item = q.item;
+      o.flags = q.flags;
+      o.ntasks = end - q.task0;
+    }
   };
   emit(hp->direct, COSTA_KERNEL_DIRECT, 0);
   for (size_t w = 0; w < hp->waves.size(); ++w) {

@@ -93,18 +93,20 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 // direction.  dst(x, y) = dst_off + y*dst_ld + x.  The source is
 //   src_off + y*src_ld + x   (flag TRANSPOSE clear: contiguous along x), or
 //   src_off + x*src_ld + y   (flag TRANSPOSE set: contiguous along y).
-// PIECE_NARROW_T: a transposed rectangle at most kNarrowT8 (8-byte
-// elements) or kNarrowT16 (16-byte elements) wide along the destination's
-// contiguous direction; the kernels stage it through a narrower LDS tile.
-enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_NARROW_T = 4 };
-#ifndef COSTA_NARROW_T8
-#define COSTA_NARROW_T8 16
-#endif
-#ifndef COSTA_NARROW_T16
-#define COSTA_NARROW_T16 64
-#endif
-constexpr int32_t kNarrowT8 = COSTA_NARROW_T8;
-constexpr int32_t kNarrowT16 = COSTA_NARROW_T16;
+// PIECE_WIDE: a non-transposed rectangle whose offsets, strides and width
+//   allow 16-byte vectors.
+// PIECE_TILE_MID / PIECE_TILE_NARROW: a transposed rectangle staged through
+//   the middle or the narrow LDS tile shape (tile_shape below) instead of
+//   the big one.
+// PIECE_GROUP_NEXT: the next rectangle of the launch is moved by the same
+//   workgroup (a run of small rectangles shares one workgroup).
+enum : int32_t {
+  PIECE_TRANSPOSE = 1,
+  PIECE_WIDE = 2,
+  PIECE_TILE_MID = 4,
+  PIECE_TILE_NARROW = 8,
+  PIECE_GROUP_NEXT = 16
+};
 
 struct alignas(16) Piece {
   int64_t src_off;
@@ -117,9 +119,46 @@ struct alignas(16) Piece {
   int32_t ny;
   int32_t item;     // pair of a batched call (selects alpha, beta, mode)
   int32_t flags;
-  int32_t pad[2];
+  int32_t task0;    // first workgroup of its launch that moves it
+  int32_t pad;
 };
 static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
+
+// Work of one workgroup (kThreadsPerTask lanes): one LDS tile of a
+// transposed rectangle, kThreadsPerTask units (16-byte vectors, or single
+// elements when the rectangle is not PIECE_WIDE) of a rectangle walked
+// along its rows, or a run of small rectangles moved at once.
+constexpr int32_t kThreadsPerTask = 256;
+constexpr int32_t kGroupUnitsMax = 128;  // rectangles of at most this many units may share a workgroup
+constexpr int32_t kGroupPiecesMax = 8;
+
+// Elements per 16-byte unit of a PIECE_WIDE rectangle.
+constexpr int32_t wide_elems(int32_t es) { return es >= 16 ? 1 : 16 / es; }
+
+// LDS tile of a transposed rectangle: tx elements along the destination's
+// contiguous direction (store runs), ty along the source's (load runs).
+// Class 0 (big), 1 (PIECE_TILE_MID), 2 (PIECE_TILE_NARROW); the planner picks
+// the class from the rectangle's width nx (tile_class).
+struct TileShape {
+  int32_t tx, ty;
+};
+#ifndef COSTA_C16_BIG_TX
+#define COSTA_C16_BIG_TX 256
+#endif
+constexpr TileShape tile_shape(int32_t es, int32_t cls) {
+  return es >= 16 ? (cls == 0 ? TileShape{COSTA_C16_BIG_TX, 16} : cls == 1 ? TileShape{128, 16} : TileShape{64, 16})
+       : es == 8  ? (cls == 0 ? TileShape{128, 16} : cls == 1 ? TileShape{64, 32} : TileShape{32, 32})
+                  : (cls == 0 ? TileShape{128, 32} : cls == 1 ? TileShape{64, 64} : TileShape{32, 64});
+}
+constexpr int32_t tile_class(int32_t es, int32_t nx) {
+  return nx > tile_shape(es, 1).tx ? 0 : nx > tile_shape(es, 2).tx ? 1 : 2;
+}
+constexpr int32_t tile_class_of_flags(int32_t flags) {
+  return (flags & PIECE_TILE_NARROW) ? 2 : (flags & PIECE_TILE_MID) ? 1 : 0;
+}
+constexpr int32_t tile_lds_bytes(int32_t es, int32_t cls) {
+  return tile_shape(es, cls).tx * (tile_shape(es, cls).ty + 1) * es;
+}
 
 // Per-pair parameters of a call, read by the kernels.
 enum : int32_t { MODE_COPY = 0, MODE_SCALE = 1, MODE_AXPBY = 2 };
@@ -132,10 +171,14 @@ struct alignas(16) ItemParam {
 };
 static_assert(sizeof(ItemParam) == 48, "ItemParam must be 48 bytes");
 
-// One kernel launch of a plan: a range of pieces split into workgroup groups.
+// One kernel launch of a plan: a range of rectangles and the workgroups
+// (tasks) that move them.  tasks[task_begin + b] = index into Plan::pieces of
+// the rectangle workgroup b starts with; that rectangle's task0 is the first
+// workgroup that moves it, so workgroup b takes its (b - task0)-th tile or
+// chunk.
 struct LaunchRange {
-  int64_t group_begin = 0;  // index into Plan::groups (each group: [groups[g], groups[g+1]) of pieces)
-  int64_t ngroups = 0;
+  int64_t piece_begin = 0, npieces = 0;
+  int64_t task_begin = 0, ntasks = 0;
   int64_t elems = 0;
   bool has_transpose = false;
   std::vector<int64_t> item_elems;  // elements of each pair in this launch
@@ -156,8 +199,10 @@ struct LaunchSpec {
   int32_t conj;
   bool has_transpose;
 };
+// pieces: the plan's rectangles (global indices); tasks: the launch's
+// ntasks entries.
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
-                        const int32_t* groups, int64_t ngroups, void* const* bufs, const ItemParam* items,
+                        const int32_t* tasks, int64_t ntasks, void* const* bufs, const ItemParam* items,
                         int32_t allow_wide, hipStream_t stream);
 
 struct VolumeArgs {

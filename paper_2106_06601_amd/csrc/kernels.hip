@@ -20,41 +20,8 @@ namespace costa {
 namespace {
 
 // Tuning switches (compile-time; the defaults are the measured best).
-#ifndef COSTA_UNROLL_WIDE
-#define COSTA_UNROLL_WIDE 4  // 16-byte units in flight per lane on the row walk
-#endif
-#ifndef COSTA_UNROLL_WIDE_AXPBY
-#define COSTA_UNROLL_WIDE_AXPBY 8  // ...when A is read too (beta != 0) in a launch without LDS tiles
-#endif
-#ifndef COSTA_UNROLL_NARROW16
-#define COSTA_UNROLL_NARROW16 4  // 16-byte elements in flight per lane on the row walk
-#endif
 #ifndef COSTA_XCD_REMAP
-#define COSTA_XCD_REMAP 1
-#endif
-#ifndef COSTA_TILE_X8
-#define COSTA_TILE_X8 32
-#endif
-#ifndef COSTA_TILE_Y8
-#define COSTA_TILE_Y8 32
-#endif
-#ifndef COSTA_TILE_X16
-#define COSTA_TILE_X16 128  // 16-byte elements: 2 KiB store runs
-#endif
-#ifndef COSTA_TILE_Y16
-#define COSTA_TILE_Y16 16
-#endif
-#ifndef COSTA_TILE_X16N
-#define COSTA_TILE_X16N 64  // narrow rectangles of 16-byte elements
-#endif
-#ifndef COSTA_TILE_X8N
-#define COSTA_TILE_X8N 16  // narrow rectangles of 8-byte elements
-#endif
-#ifndef COSTA_TILE_Y8N
-#define COSTA_TILE_Y8N 32
-#endif
-#ifndef COSTA_TILE_Y16N
-#define COSTA_TILE_Y16N 16
+#define COSTA_XCD_REMAP 0  // contiguous workgroup ranges per XCD (off: dispatch order is address order)
 #endif
 #ifndef COSTA_NT_LOADS
 #define COSTA_NT_LOADS 1  // row walks: each source line is read once
@@ -72,7 +39,7 @@ namespace {
 #define COSTA_NT_ALOADS 0
 #endif
 
-constexpr int kThreads = 256;
+constexpr int kThreads = kThreadsPerTask;
 
 // Workgroup b of n (dispatched round-robin over the 8 XCDs) gets the b-th
 // slot of a contiguous range per XCD, so consecutive groups share an L2.
@@ -176,267 +143,241 @@ __device__ __forceinline__ Vec<S, NU> combine(const Vec<S, NU>& b, const Vec<S, 
   return o;
 }
 
-// Rectangle whose source and destination both run along x:
-// dst[y*dst_ld + x] = f(src[y*src_ld + x]).  Units of NU scalars (one element,
-// or several when the rectangle is 16-byte aligned); lanes walk the flattened
-// (y, x) index so short rows still fill a wavefront.
-template <typename S, int NU, int NEL, bool CPLX, int MODE, bool CONJ, int UNROLL>
-__device__ __forceinline__ void move_rows(const S* __restrict__ src, S* __restrict__ dst, const Piece& p, S ar,
-                                          S ai, S br, S bi) {
-  using U = Vec<S, NU>;
-  const U* __restrict__ su = reinterpret_cast<const U*>(src) + p.src_off / NEL;
-  U* __restrict__ du = reinterpret_cast<U*>(dst) + p.dst_off / NEL;
-  const int64_t sld = p.src_ld / NEL, dld = p.dst_ld / NEL;
-  const int32_t nxu = p.nx / NEL;
-  const int32_t n = nxu * p.ny;
-  const float inv = 1.0f / (float)nxu;
-  const int32_t tid = threadIdx.x;
-  for (int32_t base = 0; base < n; base += kThreads * UNROLL) {
-    U bv[UNROLL], av[UNROLL];
-    int64_t doff[UNROLL];
-#pragma unroll
-    for (int u = 0; u < UNROLL; ++u) {
-      const int32_t e = base + u * kThreads + tid;
-      doff[u] = -1;
-      if (e < n) {
-        // y = e / nxu from a float estimate, corrected to the exact quotient
-        int32_t y = (int32_t)((float)e * inv);
-        int32_t x = e - y * nxu;
-        while (x < 0) {
-          --y;
-          x += nxu;
-        }
-        while (x >= nxu) {
-          ++y;
-          x -= nxu;
-        }
-        bv[u] = load<COSTA_NT_LOADS && (int)sizeof(S) * (CPLX ? 2 : 1) <= COSTA_NT_LOADS_MAX_ES>(su + (y * sld + x));
-        doff[u] = y * dld + x;
-        if constexpr (MODE == MODE_AXPBY) av[u] = load<COSTA_NT_ALOADS>(du + doff[u]);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < UNROLL; ++u)
-      if (doff[u] >= 0) store(du + doff[u], combine<S, NU, CPLX, MODE, CONJ>(bv[u], av[u], ar, ai, br, bi));
+template <typename S, bool CPLX>
+struct TypeTraits {
+  static constexpr int NS = CPLX ? 2 : 1;         // scalars per element
+  static constexpr int ES = (int)sizeof(S) * NS;  // bytes per element
+  static constexpr int WIDE_NEL = wide_elems(ES); // elements per 16-byte unit
+  static constexpr bool NT_WALK = COSTA_NT_LOADS && ES <= COSTA_NT_LOADS_MAX_ES;
+  static constexpr int lds_elems(int cls) { return tile_shape(ES, cls).tx * (tile_shape(ES, cls).ty + 1); }
+  static constexpr int LDS_ELEMS = lds_elems(0) > lds_elems(1) ? (lds_elems(0) > lds_elems(2) ? lds_elems(0)
+                                                                                                : lds_elems(2))
+                                                               : (lds_elems(1) > lds_elems(2) ? lds_elems(1)
+                                                                                              : lds_elems(2));
+};
+
+// y = u / n and x = u - y*n from a float estimate of the quotient, corrected
+// to the exact one (u, n < 2^24: at most one step each way).
+__device__ __forceinline__ void divmod(int32_t u, int32_t n, int32_t& y, int32_t& x) {
+  y = (int32_t)((float)u * (1.0f / (float)n));
+  x = u - y * n;
+  while (x < 0) {
+    --y;
+    x += n;
+  }
+  while (x >= n) {
+    ++y;
+    x -= n;
   }
 }
 
-template <typename S, bool CPLX>
-struct TypeTraits {
-  static constexpr int NS = CPLX ? 2 : 1;                  // scalars per element
-  static constexpr int ES = (int)sizeof(S) * NS;           // bytes per element
-  static constexpr int WIDE_NEL = ES >= 16 ? 1 : 16 / ES;  // elements per 16-byte unit
-  static constexpr int UNROLL_NARROW = ES >= 16 ? COSTA_UNROLL_NARROW16 : 8;
-  // transpose tile: TX elements along the destination's contiguous direction
-  // (store lanes), TY along the source's (load lanes).  Long store runs pay
-  // off for 16-byte elements; 8-byte elements keep 32 x 32 (occupancy, and
-  // the narrow transposed rectangles of block-cyclic layouts)
-  static constexpr int TX = ES >= 16 ? COSTA_TILE_X16 : ES == 8 ? COSTA_TILE_X8 : 64;
-  static constexpr int TY = ES >= 16 ? COSTA_TILE_Y16 : ES == 8 ? COSTA_TILE_Y8 : 64;
-  // rectangles marked PIECE_NARROW_T: a narrower tile keeps the store lanes
-  // busy
-  static constexpr int TXN = ES >= 16 ? COSTA_TILE_X16N : ES == 8 ? COSTA_TILE_X8N : TX;
-  static constexpr int TYN = ES >= 16 ? COSTA_TILE_Y16N : ES == 8 ? COSTA_TILE_Y8N : TY;
-  static constexpr int LDS_ELEMS = TX * (TY + 1) > TXN * (TYN + 1) ? TX * (TY + 1) : TXN * (TYN + 1);
-};
+// Row walk: dst[y*dst_ld + x] = f(src[y*src_ld + x]).  Workgroup chunk c
+// covers units [c*kThreads, (c+1)*kThreads) of the rectangle's flattened
+// (y, x) index, one unit per lane (a 16-byte vector for PIECE_WIDE
+// rectangles, else one element).  A run of small rectangles
+// (PIECE_GROUP_NEXT) is flattened the same way: lane l takes unit l of the
+// run.  Each lane makes one load (two when A is read) and one store.
+template <typename S, bool CPLX, int MODE, bool CONJ>
+__device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int32_t pi, int32_t c,
+                                          void* const* __restrict__ bufs, int32_t allow_wide, S ar, S ai, S br,
+                                          S bi) {
+  using TT = TypeTraits<S, CPLX>;
+  using E = Vec<S, TT::NS>;
+  constexpr int W = TT::WIDE_NEL;
+  const bool wide = (pieces[pi].flags & PIECE_WIDE) != 0;  // the same over a run
+  const int32_t epu = wide ? W : 1;                         // elements per unit
+  int32_t u = c * kThreads + (int32_t)threadIdx.x;
+  int64_t soff = -1, doff = 0;
+  int32_t sbuf = 0, dbuf = 0;
+  while (true) {
+    const Piece& p = pieces[pi];
+    const int32_t nxu = wide ? p.nx / W : p.nx;
+    const int32_t units = nxu * p.ny;
+    if (u >= 0 && u < units) {
+      int32_t y, x;
+      divmod(u, nxu, y, x);
+      soff = p.src_off + (int64_t)y * p.src_ld + (int64_t)x * epu;
+      doff = p.dst_off + (int64_t)y * p.dst_ld + (int64_t)x * epu;
+      sbuf = p.src_buf;
+      dbuf = p.dst_buf;
+    }
+    u -= units;
+    if (!(p.flags & PIECE_GROUP_NEXT)) break;
+    ++pi;
+  }
+  if (soff < 0) return;
+  const S* __restrict__ src = reinterpret_cast<const S*>(bufs[sbuf]);
+  S* __restrict__ dst = reinterpret_cast<S*>(bufs[dbuf]);
+  if (W > 1 && wide && allow_wide) {
+    using U = Vec<S, TT::NS * W>;
+    const U* su = reinterpret_cast<const U*>(src + soff * TT::NS);
+    U* du = reinterpret_cast<U*>(dst + doff * TT::NS);
+    const U bv = load<TT::NT_WALK>(su);
+    U av;
+    if constexpr (MODE == MODE_AXPBY) av = load<COSTA_NT_ALOADS>(du);
+    store(du, combine<S, TT::NS * W, CPLX, MODE, CONJ>(bv, av, ar, ai, br, bi));
+  } else {
+    // one element at a time (epu of them: a PIECE_WIDE rectangle in a call
+    // whose buffers are not 16-byte aligned)
+    const E* se = reinterpret_cast<const E*>(src) + soff;
+    E* de = reinterpret_cast<E*>(dst) + doff;
+    E bv[W], av[W];
+#pragma unroll
+    for (int k = 0; k < W; ++k)
+      if (k < epu) {
+        bv[k] = load<TT::NT_WALK>(se + k);
+        if constexpr (MODE == MODE_AXPBY) av[k] = load<COSTA_NT_ALOADS>(de + k);
+      }
+#pragma unroll
+    for (int k = 0; k < W; ++k)
+      if (k < epu) store(de + k, combine<S, TT::NS, CPLX, MODE, CONJ>(bv[k], av[k], ar, ai, br, bi));
+  }
+}
 
-// Rectangles whose source runs along y while the destination runs along x:
-// staged through an LDS tile of TX x TY elements (one padding column against
-// bank conflicts).  Loads are coalesced along the source, stores along the
-// destination.  The workgroup walks the tiles of the consecutive transposed
-// rectangles [pi, p1) as one sequence, software pipelined across rectangle
-// boundaries: the loads of the next tile (of this rectangle or of the next
-// one) are in flight while the current tile is written out.  Returns the
-// index of the first rectangle it did not process (the run stops at a
-// rectangle that is not transposed or takes the other tile shape).  MODE_ANY
-// callers pass p1 = pi + 1.
+// One TX x TY tile of a rectangle whose source runs along y while the
+// destination runs along x, staged through LDS (one padding column against
+// bank conflicts).  Loads are coalesced along the source (runs of TY
+// elements), stores along the destination (runs of TX elements).  Tile c of
+// the rectangle; tiles are numbered along x first.
 template <typename S, bool CPLX, int MODE, bool CONJ, int TX, int TY>
-__device__ __forceinline__ int32_t move_transposed_run(const Piece* __restrict__ pieces, int32_t pi, int32_t p1,
-                                                       void* const* __restrict__ bufs,
-                                                       const ItemParam* __restrict__ items,
-                                                       Vec<S, CPLX ? 2 : 1>* lds) {
+__device__ __forceinline__ void move_tile(const Piece* __restrict__ pieces, int32_t pi, int32_t c,
+                                          void* const* __restrict__ bufs, Vec<S, CPLX ? 2 : 1>* lds, S ar, S ai,
+                                          S br, S bi) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
   E (*tile)[TY + 1] = reinterpret_cast<E (*)[TY + 1]>(lds);
   constexpr int LROWS = kThreads / TY;  // x rows per load pass
   constexpr int SROWS = kThreads / TX;  // y rows per store pass
-  constexpr int NL = TX / LROWS;        // loads per thread per tile
+  constexpr int NL = TX / LROWS;        // loads per lane
   static_assert(kThreads % TX == 0 && kThreads % TY == 0 && TX % LROWS == 0 && TY % SROWS == 0,
                 "the load and store passes must cover the tile exactly");
+  static_assert(TX * (TY + 1) <= TT::LDS_ELEMS, "tile larger than the launch's LDS");
+  const Piece& p = pieces[pi];
   const int32_t tid = threadIdx.x;
-  const int32_t ly0 = tid % TY, lx0 = tid / TY;  // load mapping
-  const int32_t sx0 = tid % TX, sy0 = tid / TX;  // store mapping
-  auto tiles_x = [](const Piece& p) { return (p.nx + TX - 1) / TX; };
-  auto tiles_of = [&](const Piece& p) { return tiles_x(p) * ((p.ny + TY - 1) / TY); };
-  auto fetch = [&](const Piece& p, int32_t t, E (&b)[NL]) {
-    const E* __restrict__ se = reinterpret_cast<const E*>(bufs[p.src_buf]) + p.src_off;
-    const int32_t ntx = tiles_x(p);
-    const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
-    const int32_t y = ty + ly0;
+  const int32_t ntx = (p.nx + TX - 1) / TX;
+  const int32_t tx = (c % ntx) * TX, ty = (c / ntx) * TY;
+  const int32_t ly = tid % TY, lx0 = tid / TY;  // load mapping
+  const E* __restrict__ se = reinterpret_cast<const E*>(bufs[p.src_buf]) + p.src_off;
+  E v[NL];
+  const bool yin = ty + ly < p.ny;
 #pragma unroll
-    for (int k = 0; k < NL; ++k) {
-      const int32_t x = tx + lx0 + k * LROWS;
-      if (x < p.nx && y < p.ny) b[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)x * p.src_ld + y));
-    }
-  };
-  Piece cur = pieces[pi];
-  int32_t ntiles = tiles_of(cur);
-  E b[NL];
-  fetch(cur, 0, b);
-  int32_t t = 0;
-  while (true) {
-    const int32_t ntx = tiles_x(cur);
-    const int32_t tx = (t % ntx) * TX, ty = (t / ntx) * TY;
-    // registers -> LDS
+  for (int k = 0; k < NL; ++k) {
+    const int32_t x = tx + lx0 + k * LROWS;
+    if (x < p.nx && yin) v[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)x * p.src_ld + (ty + ly)));
+  }
 #pragma unroll
-    for (int k = 0; k < NL; ++k) {
-      const int32_t lx = lx0 + k * LROWS;
-      if (tx + lx < cur.nx && ty + ly0 < cur.ny) tile[lx][ly0] = b[k];
-    }
-    __syncthreads();
-    // the next tile: of this rectangle, else the first of the next one if it
-    // is transposed too; its loads go out before this tile is stored
-    Piece nxt = cur;
-    int32_t nt = t + 1;
-    bool more = nt < ntiles;
-    if (!more && pi + 1 < p1) {
-      nxt = pieces[pi + 1];
-      constexpr int32_t kClass = PIECE_TRANSPOSE | PIECE_NARROW_T;  // same tile shape
-      more = (nxt.flags & kClass) == (cur.flags & kClass);
-      nt = 0;
-    }
-    if (more) fetch(nxt, nt, b);
-    // LDS -> destination
-    E* __restrict__ de = reinterpret_cast<E*>(bufs[cur.dst_buf]) + cur.dst_off;
-    S ar = S(0), ai = S(0), br = S(0), bi = S(0);
-    if constexpr (MODE != MODE_COPY) {
-      const ItemParam& ip = items[cur.item];
-      ar = (S)ip.alpha[0];
-      ai = (S)ip.alpha[1];
-      br = (S)ip.beta[0];
-      bi = (S)ip.beta[1];
-    }
-    const int32_t x = tx + sx0;
+  for (int k = 0; k < NL; ++k) {
+    const int32_t lx = lx0 + k * LROWS;
+    if (tx + lx < p.nx && yin) tile[lx][ly] = v[k];
+  }
+  __syncthreads();
+  E* __restrict__ de = reinterpret_cast<E*>(bufs[p.dst_buf]) + p.dst_off;
+  const int32_t sx = tid % TX, sy0 = tid / TX;  // store mapping
+  const int32_t x = tx + sx;
+  if (x >= p.nx) return;
 #pragma unroll
-    for (int k = 0; k < TY / SROWS; ++k) {
-      const int32_t ly = sy0 + k * SROWS;
-      const int32_t yy = ty + ly;
-      if (x < cur.nx && yy < cur.ny) {
-        E* o = de + ((int64_t)yy * cur.dst_ld + x);
-        E a;
-        if constexpr (MODE == MODE_AXPBY) a = load<COSTA_NT_ALOADS>(o);
-        store(o, combine<S, TT::NS, CPLX, MODE, CONJ>(tile[sx0][ly], a, ar, ai, br, bi));
-      }
+  for (int k = 0; k < TY / SROWS; ++k) {
+    const int32_t ly2 = sy0 + k * SROWS;
+    const int32_t yy = ty + ly2;
+    if (yy < p.ny) {
+      E* o = de + ((int64_t)yy * p.dst_ld + x);
+      E a;
+      if constexpr (MODE == MODE_AXPBY) a = load<COSTA_NT_ALOADS>(o);
+      store(o, combine<S, TT::NS, CPLX, MODE, CONJ>(tile[sx][ly2], a, ar, ai, br, bi));
     }
-    __syncthreads();
-    if (!more) return pi + 1;
-    if (nt == 0) {
-      ++pi;
-      cur = nxt;
-      ntiles = tiles_of(cur);
-    }
-    t = nt;
   }
 }
 
-// A rectangle whose source and destination run the same way.  A launch that
-// also holds transposed rectangles (HAS_T) keeps the shallower unroll: the
-// register budget of its tile path sets the launch's occupancy.
+// The work of one workgroup for a fixed arithmetic mode.
 template <typename S, bool CPLX, int MODE, bool CONJ, bool HAS_T>
-__device__ __forceinline__ void move_piece(const S* src, S* dst, const Piece& p, bool wide, S ar, S ai, S br, S bi) {
+__device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int32_t pi, int32_t flags, int32_t c,
+                                          void* const* __restrict__ bufs, const ItemParam* __restrict__ ip,
+                                          int32_t allow_wide, Vec<S, CPLX ? 2 : 1>* lds) {
   using TT = TypeTraits<S, CPLX>;
-  if (wide && TT::WIDE_NEL > 1) {
-    constexpr int U = MODE == MODE_AXPBY && !HAS_T ? COSTA_UNROLL_WIDE_AXPBY : COSTA_UNROLL_WIDE;
-    move_rows<S, TT::NS * TT::WIDE_NEL, TT::WIDE_NEL, CPLX, MODE, CONJ, U>(src, dst, p, ar, ai, br, bi);
-  } else {
-    move_rows<S, TT::NS, 1, CPLX, MODE, CONJ, TT::UNROLL_NARROW>(src, dst, p, ar, ai, br, bi);
+  S ar = S(0), ai = S(0), br = S(0), bi = S(0);
+  if constexpr (MODE != MODE_COPY) {
+    ar = (S)ip->alpha[0];
+    ai = (S)ip->alpha[1];
+    br = (S)ip->beta[0];
+    bi = (S)ip->beta[1];
   }
+  if constexpr (HAS_T) {
+    if (flags & PIECE_TRANSPOSE) {
+      constexpr TileShape t0 = tile_shape(TT::ES, 0), t1 = tile_shape(TT::ES, 1), t2 = tile_shape(TT::ES, 2);
+      const int32_t cls = tile_class_of_flags(flags);
+      if (cls == 0) move_tile<S, CPLX, MODE, CONJ, t0.tx, t0.ty>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
+      else if (cls == 1) move_tile<S, CPLX, MODE, CONJ, t1.tx, t1.ty>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
+      else move_tile<S, CPLX, MODE, CONJ, t2.tx, t2.ty>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
+      return;
+    }
+  }
+  move_walk<S, CPLX, MODE, CONJ>(pieces, pi, c, bufs, allow_wide, ar, ai, br, bi);
 }
 
 constexpr int MODE_ANY = 3;
 
-// One launch over groups of rectangles.
+// One launch: workgroup b moves task task_off + b of the launch's task table.
 //   KIND: pack (bitwise copy into message buffers, never transposed),
 //         unpack-transform, or direct.
 //   MODE: the arithmetic of every pair of the call, or MODE_ANY to read it
-//         per rectangle (batches that mix modes); CONJ likewise.
-//   HAS_T: whether the launch contains transposed rectangles (LDS tile).
+//         per workgroup (batches that mix modes; a workgroup's rectangles
+//         belong to one pair); CONJ likewise.
+//   HAS_T: whether the launch contains transposed rectangles (LDS tiles).
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
-costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ groups, int32_t ngroups,
-            void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide) {
+__device__ __forceinline__ void mover_body(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks,
+                                           int32_t task_off, void* const* __restrict__ bufs,
+                                           const ItemParam* __restrict__ items, int32_t allow_wide) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
   __shared__ E lds[HAS_T ? TT::LDS_ELEMS : 1];
-  const int32_t g = xcd_remap((int32_t)blockIdx.x, ngroups);
-  const int32_t p0 = groups[g], p1 = groups[g + 1];
-  int32_t pi = p0;
-  Piece ahead = pieces[p0];  // the next rectangle's descriptor, fetched while the current one moves
-  int32_t ahead_i = p0;
-  while (pi < p1) {
-    const Piece p = ahead_i == pi ? ahead : pieces[pi];
-    if (pi + 1 < p1) {
-      ahead = pieces[pi + 1];
-      ahead_i = pi + 1;
-    }
-    if constexpr (KIND == KIND_PACK) {
-      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
-      move_piece<S, CPLX, MODE_COPY, false, false>(reinterpret_cast<const S*>(bufs[p.src_buf]),
-                                            reinterpret_cast<S*>(bufs[p.dst_buf]), p, wide, S(0), S(0), S(0), S(0));
-      ++pi;
-      continue;
+  const int32_t b = task_off + (COSTA_XCD_REMAP ? xcd_remap((int32_t)blockIdx.x, (int32_t)gridDim.x)
+                                                : (int32_t)blockIdx.x);
+  const int32_t pi = tasks[b];
+  const int32_t c = b - pieces[pi].task0;
+  if constexpr (KIND == KIND_PACK) {
+    move_walk<S, CPLX, MODE_COPY, false>(pieces, pi, c, bufs, allow_wide, S(0), S(0), S(0), S(0));
+  } else {
+    const int32_t flags = pieces[pi].flags;
+    const ItemParam* ip = items + pieces[pi].item;
+    if constexpr (MODE != MODE_ANY) {
+      move_task<S, CPLX, MODE, CONJ, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
     } else {
-      const ItemParam& ip = items[p.item];
-      if constexpr (HAS_T) {
-        if (p.flags & PIECE_TRANSPOSE) {
-          if constexpr (MODE != MODE_ANY) {
-            if (TT::TXN != TT::TX && (p.flags & PIECE_NARROW_T))
-              pi = move_transposed_run<S, CPLX, MODE, CONJ, TT::TXN, TT::TYN>(pieces, pi, p1, bufs, items, lds);
-            else
-              pi = move_transposed_run<S, CPLX, MODE, CONJ, TT::TX, TT::TY>(pieces, pi, p1, bufs, items, lds);
-          } else {
-            // mixed batches: one rectangle at a time, the big tile
-            const bool conj = CPLX && ip.conj;
-            constexpr int X = TT::TX, Y = TT::TY;
-            if (ip.mode == MODE_COPY)
-              pi = conj ? move_transposed_run<S, CPLX, MODE_COPY, true, X, Y>(pieces, pi, pi + 1, bufs, items, lds)
-                        : move_transposed_run<S, CPLX, MODE_COPY, false, X, Y>(pieces, pi, pi + 1, bufs, items, lds);
-            else if (ip.mode == MODE_SCALE)
-              pi = conj ? move_transposed_run<S, CPLX, MODE_SCALE, true, X, Y>(pieces, pi, pi + 1, bufs, items, lds)
-                        : move_transposed_run<S, CPLX, MODE_SCALE, false, X, Y>(pieces, pi, pi + 1, bufs, items, lds);
-            else
-              pi = conj ? move_transposed_run<S, CPLX, MODE_AXPBY, true, X, Y>(pieces, pi, pi + 1, bufs, items, lds)
-                        : move_transposed_run<S, CPLX, MODE_AXPBY, false, X, Y>(pieces, pi, pi + 1, bufs, items, lds);
-          }
-          continue;
-        }
-      }
-      const S* src = reinterpret_cast<const S*>(bufs[p.src_buf]);
-      S* dst = reinterpret_cast<S*>(bufs[p.dst_buf]);
-      const bool wide = allow_wide && (p.flags & PIECE_WIDE);
-      const S ar = (S)ip.alpha[0], ai = (S)ip.alpha[1], br = (S)ip.beta[0], bi = (S)ip.beta[1];
-      if constexpr (MODE != MODE_ANY) {
-        move_piece<S, CPLX, MODE, CONJ, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
+      const bool conj = CPLX && ip->conj;
+      const int32_t mode = ip->mode;
+      if (mode == MODE_COPY) {
+        if (conj) move_task<S, CPLX, MODE_COPY, CPLX, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+        else move_task<S, CPLX, MODE_COPY, false, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+      } else if (mode == MODE_SCALE) {
+        if (conj) move_task<S, CPLX, MODE_SCALE, CPLX, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+        else move_task<S, CPLX, MODE_SCALE, false, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
       } else {
-        const bool conj = CPLX && ip.conj;
-        switch (ip.mode) {
-          case MODE_COPY:
-            if (conj) move_piece<S, CPLX, MODE_COPY, true, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_COPY, false, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
-            break;
-          case MODE_SCALE:
-            if (conj) move_piece<S, CPLX, MODE_SCALE, true, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_SCALE, false, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
-            break;
-          default:
-            if (conj) move_piece<S, CPLX, MODE_AXPBY, true, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
-            else move_piece<S, CPLX, MODE_AXPBY, false, HAS_T>(src, dst, p, wide, ar, ai, br, bi);
-            break;
-        }
+        if (conj) move_task<S, CPLX, MODE_AXPBY, CPLX, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+        else move_task<S, CPLX, MODE_AXPBY, false, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
       }
-      ++pi;
     }
   }
+}
+
+// Tile sizes that leave room for at least four workgroups per CU (160 KiB of
+// LDS) are compiled for at least four waves per SIMD; larger tiles (the big
+// complex128 tile) for two.
+template <typename S, bool CPLX, bool HAS_T>
+constexpr bool big_lds() {
+  return HAS_T && TypeTraits<S, CPLX>::LDS_ELEMS * TypeTraits<S, CPLX>::ES > 40 * 1024;
+}
+
+template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
+costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
+            void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide);
+}
+
+template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+costa_mover_lds(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
+                void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide);
 }
 
 // Volume of the grid overlay: every overlay block (k, l) adds its element
@@ -472,8 +413,8 @@ struct Launch {
   dim3 grid, block;
   hipStream_t stream;
   const Piece* pieces;
-  const int32_t* groups;
-  int32_t ngroups;
+  const int32_t* tasks;
+  int32_t task_off;
   void* const* bufs;
   const ItemParam* items;
   int32_t allow_wide;
@@ -513,8 +454,12 @@ __global__ void __launch_bounds__(kThreads) costa_volume_outer(SeparableArgs a) 
 
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 hipError_t go(const Launch& l) {
-  hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
-                     l.groups, l.ngroups, l.bufs, l.items, l.allow_wide);
+  if constexpr (big_lds<S, CPLX, HAS_T>())
+    hipLaunchKernelGGL((costa_mover_lds<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
+                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide);
+  else
+    hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
+                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide);
   return hipGetLastError();
 }
 
@@ -548,19 +493,25 @@ hipError_t launch_typed(MoverKind kind, const LaunchSpec& spec, const Launch& l)
 }  // namespace
 
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
-                        const int32_t* groups, int64_t ngroups, void* const* bufs, const ItemParam* items,
+                        const int32_t* tasks, int64_t ntasks, void* const* bufs, const ItemParam* items,
                         int32_t allow_wide, hipStream_t stream) {
-  if (ngroups <= 0) return hipSuccess;
-  if (ngroups > INT32_MAX) return hipErrorInvalidValue;
-  Launch l{dim3((unsigned)ngroups), dim3(kThreads), stream, pieces, groups, (int32_t)ngroups, bufs, items,
-           allow_wide};
-  switch (dtype) {
-    case COSTA_R64: return launch_typed<double, false>(kind, spec, l);
-    case COSTA_C128: return launch_typed<double, true>(kind, spec, l);
-    case COSTA_R32: return launch_typed<float, false>(kind, spec, l);
-    case COSTA_C64: return launch_typed<float, true>(kind, spec, l);
+  if (ntasks <= 0) return hipSuccess;
+  if (ntasks > INT32_MAX) return hipErrorInvalidValue;
+  // one workgroup per task, in slices that keep the grid below 2^32 work-items
+  constexpr int64_t kSlice = 1 << 23;
+  for (int64_t off = 0; off < ntasks; off += kSlice) {
+    const int64_t n = ntasks - off < kSlice ? ntasks - off : kSlice;
+    Launch l{dim3((unsigned)n), dim3(kThreads), stream, pieces, tasks, (int32_t)off, bufs, items, allow_wide};
+    hipError_t e = hipErrorInvalidValue;
+    switch (dtype) {
+      case COSTA_R64: e = launch_typed<double, false>(kind, spec, l); break;
+      case COSTA_C128: e = launch_typed<double, true>(kind, spec, l); break;
+      case COSTA_R32: e = launch_typed<float, false>(kind, spec, l); break;
+      case COSTA_C64: e = launch_typed<float, true>(kind, spec, l); break;
+    }
+    if (e != hipSuccess) return e;
   }
-  return hipErrorInvalidValue;
+  return hipSuccess;
 }
 
 hipError_t launch_volume_separable(const SeparableArgs& a, hipStream_t stream) {

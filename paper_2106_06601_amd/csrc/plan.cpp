@@ -10,10 +10,13 @@
 //
 // Adjacent overlay blocks that are also adjacent in both the source and the
 // destination storage (for instance the blocks of one process row of a 1 x P
-// grid) are merged into one rectangle, large rectangles are split for load
-// balance, and runs of small rectangles are grouped per workgroup.
+// grid) are merged into one rectangle.  Each launch's rectangles are then cut
+// into workgroup tasks of equal size (an LDS tile of a transposed rectangle,
+// or a few KiB of a row walk), and runs of small rectangles share one
+// workgroup.
 #include <algorithm>
 #include <chrono>
+#include <new>
 #include <numeric>
 
 #include "plan.hpp"
@@ -22,10 +25,6 @@
 // of their own.
 #ifndef COSTA_MERGE_DIRECT
 #define COSTA_MERGE_DIRECT 1
-#endif
-// Cut transposed rectangles into tile-aligned near-square pieces.
-#ifndef COSTA_SPLIT_SQUARE
-#define COSTA_SPLIT_SQUARE 1
 #endif
 
 namespace costa {
@@ -128,7 +127,8 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
       p.dst_buf = item * P + r;
       p.src_buf = nitems * P + item * P + s;
       p.item = item;
-      p.pad[0] = p.pad[1] = 0;
+      p.task0 = 0;
+      p.pad = 0;
       c.kx0 = kx;
       c.kx1 = kx + 1;
       c.ly_end = ly + 1;
@@ -171,38 +171,32 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
   for (Cand& c : all) (c.s == c.r ? local : remote).push_back(c);
 }
 
-// Cuts of a rectangle larger than max_nt elements (t_factor times that when
-// transposed): (x0, y0, nx, ny) of each sub-rectangle.  Row walks keep whole
-// rows (long contiguous runs); transposed rectangles are cut into
-// near-square pieces whose sides are multiples of the 32-element LDS tile,
-// so that no piece is a thin strip that leaves most of a tile idle.
+// Cuts of a rectangle larger than max_elems elements: (x0, y0, nx, ny) of
+// each sub-rectangle.  Row walks are cut into strips of whole rows where a row
+// fits; transposed rectangles into strips whose width is a multiple of 128 and
+// whose height is a multiple of 32 where possible, so that their LDS tiles
+// stay full.
 struct Cut {
   int64_t x0, y0, nx, ny;
 };
-void cuts_of(const Piece& p, int64_t max_nt, int64_t t_factor, std::vector<Cut>& out) {
+void cuts_of(const Piece& p, int64_t max_elems, std::vector<Cut>& out) {
   out.clear();
-  const int64_t TS = 32;
-  const bool T = p.flags & PIECE_TRANSPOSE;
-  const int64_t max_elems = T ? max_nt * t_factor : max_nt;
   if ((int64_t)p.nx * p.ny <= max_elems) {
     out.push_back(Cut{0, 0, p.nx, p.ny});
     return;
   }
+  const bool T = p.flags & PIECE_TRANSPOSE;
   int64_t cx, cy;
-  if (T && COSTA_SPLIT_SQUARE) {
-    int64_t side = TS;
-    while ((2 * side) * (2 * side) <= max_elems) side *= 2;  // largest power-of-two square that fits
-    cx = std::min<int64_t>(p.nx, side);
-    cy = std::max<int64_t>(TS, max_elems / cx);
-    cy = std::min<int64_t>(p.ny, cy - cy % TS);
-    if (cx < side) {  // narrow in x: give the room to y
-      cy = std::max<int64_t>(TS, max_elems / cx);
-      cy = std::min<int64_t>(p.ny, cy - cy % TS);
-    }
+  if (T) {
+    cx = std::min<int64_t>(p.nx, std::max<int64_t>(128, max_elems / 32));
+    if (cx < p.nx && cx >= 128) cx -= cx % 128;
+    cy = std::max<int64_t>(1, max_elems / cx);
+    if (cy > 32) cy -= cy % 32;
   } else {
     cx = std::min<int64_t>(p.nx, max_elems);
     cy = std::max<int64_t>(1, max_elems / cx);
   }
+  cy = std::min<int64_t>(cy, p.ny);
   for (int64_t y0 = 0; y0 < p.ny; y0 += cy)
     for (int64_t x0 = 0; x0 < p.nx; x0 += cx)
       out.push_back(Cut{x0, y0, std::min<int64_t>(cx, p.nx - x0), std::min<int64_t>(cy, p.ny - y0)});
@@ -219,13 +213,16 @@ Piece sub_piece(const Piece& p, const Cut& c) {
   return d;
 }
 
-// Splits rectangles larger than max_nt elements (see cuts_of).
-void split_pieces(std::vector<Cand>& v, int64_t max_nt, int64_t t_factor) {
+// Splits rectangles larger than max_elems elements (see cuts_of).
+void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
+  bool any = false;
+  for (const Cand& c : v) any = any || (int64_t)c.p.nx * c.p.ny > max_elems;
+  if (!any) return;
   std::vector<Cand> out;
   out.reserve(v.size());
   std::vector<Cut> cs;
   for (const Cand& c : v) {
-    cuts_of(c.p, max_nt, t_factor, cs);
+    cuts_of(c.p, max_elems, cs);
     for (const Cut& k : cs) {
       Cand d = c;
       d.p = sub_piece(c.p, k);
@@ -235,53 +232,93 @@ void split_pieces(std::vector<Cand>& v, int64_t max_nt, int64_t t_factor) {
   v.swap(out);
 }
 
-// Marks rectangles whose non-transposed walk can use 16-byte vectors, and
-// narrow transposed rectangles of 16-byte elements.
+// Sets the flags the kernels read: 16-byte vectors for row walks, the LDS
+// tile class of transposed rectangles.
 void finish_piece(Piece& p, int elem_size) {
-  p.flags &= ~(PIECE_WIDE | PIECE_NARROW_T);
-  if ((p.flags & PIECE_TRANSPOSE) &&
-      ((elem_size == 16 && p.nx <= kNarrowT16) || (elem_size == 8 && p.nx <= kNarrowT8)))
-    p.flags |= PIECE_NARROW_T;
-  if (!(p.flags & PIECE_TRANSPOSE)) {
-    int64_t want = elem_size >= 16 ? 1 : 16 / elem_size;
-    if (want > 1 && p.nx % want == 0 && p.src_off % want == 0 && p.dst_off % want == 0 &&
-        (p.ny == 1 || (p.src_ld % want == 0 && p.dst_ld % want == 0)))
-      p.flags |= PIECE_WIDE;
+  p.flags &= ~(PIECE_WIDE | PIECE_TILE_MID | PIECE_TILE_NARROW | PIECE_GROUP_NEXT);
+  p.task0 = 0;
+  p.pad = 0;
+  if (p.flags & PIECE_TRANSPOSE) {
+    const int32_t cls = tile_class(elem_size, p.nx);
+    if (cls == 1) p.flags |= PIECE_TILE_MID;
+    if (cls == 2) p.flags |= PIECE_TILE_NARROW;
+    return;
   }
+  const int64_t want = wide_elems(elem_size);
+  if (want > 1 && p.nx % want == 0 && p.src_off % want == 0 && p.dst_off % want == 0 &&
+      (p.ny == 1 || (p.src_ld % want == 0 && p.dst_ld % want == 0)))
+    p.flags |= PIECE_WIDE;
 }
 
-// Appends one launch: groups of consecutive rectangles.
-LaunchRange add_launch(HostPlan& hp, const std::vector<Piece>& ps, const PlanConfig& cfg, int32_t nitems) {
+// Appends one launch: its rectangles and the workgroups that move them, in
+// rectangle order.  A transposed rectangle gets one workgroup per LDS tile
+// (tiles along x first); a row walk one per kThreadsPerTask units; runs of
+// small row walks of the same pair and vector width share one workgroup.
+LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nitems) {
   LaunchRange lr;
   lr.item_elems.assign(nitems, 0);
-  lr.group_begin = (int64_t)hp.groups.size();
+  lr.piece_begin = (int64_t)hp.pieces.size();
+  lr.npieces = (int64_t)ps.size();
+  lr.task_begin = (int64_t)hp.tasks.size();
+  if (hp.pieces.size() + ps.size() > (size_t)INT32_MAX) throw std::bad_alloc();
   const int32_t base = (int32_t)hp.pieces.size();
-  int64_t acc = 0;
-  int32_t cnt = 0;
+  int64_t b = 0;
+  int64_t g_task = -1;  // workgroup of the open run of small rectangles
+  int64_t g_units = 0;
+  int32_t g_count = 0;
+  size_t g_last = 0;
+  bool g_wide = false;
+  int32_t g_item = 0;
   for (size_t k = 0; k < ps.size(); ++k) {
-    if (cnt == 0) hp.groups.push_back(base + (int32_t)k);
-    acc += (int64_t)ps[k].nx * ps[k].ny;
-    lr.elems += (int64_t)ps[k].nx * ps[k].ny;
-    lr.item_elems[ps[k].item] += (int64_t)ps[k].nx * ps[k].ny;
-    if (ps[k].flags & PIECE_TRANSPOSE) lr.has_transpose = true;
-    ++cnt;
-    const int64_t enough = (ps[k].flags & PIECE_TRANSPOSE) ? cfg.min_group_elems_t : cfg.min_group_elems;
-    if (acc >= enough || cnt >= cfg.max_group_pieces) {
-      acc = 0;
-      cnt = 0;
+    Piece& p = ps[k];
+    const int64_t ne = (int64_t)p.nx * p.ny;
+    lr.elems += ne;
+    lr.item_elems[p.item] += ne;
+    const int32_t pi = base + (int32_t)k;
+    if (p.flags & PIECE_TRANSPOSE) {
+      lr.has_transpose = true;
+      const TileShape ts = tile_shape(es, tile_class_of_flags(p.flags));
+      const int64_t n = (int64_t)((p.nx + ts.tx - 1) / ts.tx) * ((p.ny + ts.ty - 1) / ts.ty);
+      p.task0 = (int32_t)b;
+      hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+      b += n;
+      g_task = -1;
+      continue;
+    }
+    const bool wide = p.flags & PIECE_WIDE;
+    const int64_t units = wide ? ne / wide_elems(es) : ne;
+    if (units <= kGroupUnitsMax && g_task >= 0 && wide == g_wide && p.item == g_item &&
+        g_units + units <= kThreadsPerTask && g_count < kGroupPiecesMax) {
+      ps[g_last].flags |= PIECE_GROUP_NEXT;
+      p.task0 = (int32_t)g_task;
+      g_units += units;
+      ++g_count;
+      g_last = k;
+      continue;
+    }
+    const int64_t n = (units + kThreadsPerTask - 1) / kThreadsPerTask;
+    p.task0 = (int32_t)b;
+    hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+    b += n;
+    if (units <= kGroupUnitsMax) {
+      g_task = b - 1;
+      g_units = units;
+      g_count = 1;
+      g_last = k;
+      g_wide = wide;
+      g_item = p.item;
+    } else {
+      g_task = -1;
     }
   }
-  lr.ngroups = (int64_t)hp.groups.size() - lr.group_begin;
-  hp.groups.push_back(base + (int32_t)ps.size());  // end sentinel
+  if (b > INT32_MAX) throw std::bad_alloc();
+  lr.ntasks = b;
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
 }
 
 #ifndef COSTA_PACK_BY_SOURCE
 #define COSTA_PACK_BY_SOURCE 1
-#endif
-#ifndef COSTA_PACK_CHUNK_FACTOR
-#define COSTA_PACK_CHUNK_FACTOR 2
 #endif
 
 bool by_dst(const Piece& a, const Piece& b) {
@@ -305,35 +342,8 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     hp.item_total[k] = items[k].A->nrows * items[k].A->ncols;
     plan_pair(k, n, items[k], sigma, local, remote, hp.overlay_blocks, hp.item_local[k], hp.item_remote[k]);
   }
-  // a launch should offer the chip a few thousand workgroups: small launches
-  // get smaller rectangles and groups
-  auto total_of = [](const std::vector<Cand>& v) {
-    int64_t t = 0;
-    for (const Cand& c : v) t += (int64_t)c.p.nx * c.p.ny;
-    return t;
-  };
-  const int64_t local_total = total_of(local), remote_total = total_of(remote);
-  auto piece_cap = [&](int64_t total) {
-    return std::max<int64_t>(4096, std::min<int64_t>(cfg.max_piece_elems, total / cfg.target_groups));
-  };
-  split_pieces(local, piece_cap(local_total), cfg.transpose_piece_factor);
-  // transposed remote rectangles of 8-byte elements become message chunks of
-  // up to COSTA_PACK_CHUNK_FACTOR times the rectangle size, the extra room
-  // going along the source's contiguous direction: the pack copies a chunk as
-  // one rectangle (longer source runs), the unpack cuts it into rectangles of
-  // the usual size.  (Measured: +3.7% on transposed tall-skinny fp64; row
-  // walks only gain rows that way, and complex128 chunks lost 2%.)
-  const int64_t unpack_cap = piece_cap(remote_total);
-  split_pieces(remote, unpack_cap, cfg.transpose_piece_factor * (es <= 8 ? COSTA_PACK_CHUNK_FACTOR : 1));
-  auto group_cfg = [&](int64_t total) {
-    PlanConfig g = cfg;
-    g.min_group_elems = std::max<int64_t>(std::min<int64_t>(1024, cfg.min_group_elems),
-                                          std::min<int64_t>(cfg.min_group_elems, total / cfg.target_groups));
-    g.min_group_elems_t = std::max<int64_t>(std::min<int64_t>(1024, cfg.min_group_elems_t),
-                                            std::min<int64_t>(cfg.min_group_elems_t, total / cfg.target_groups));
-    return g;
-  };
-  const PlanConfig cfg_local = group_cfg(local_total), cfg_remote = group_cfg(remote_total);
+  split_pieces(local, cfg.max_piece_elems);
+  split_pieces(remote, cfg.max_piece_elems);
 
   // direct path, in destination order
   std::vector<Piece> direct;
@@ -347,25 +357,33 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
 
   // messages: packages ordered by sender, then receiver (each sender's send
   // buffer holds one contiguous package per receiver); blocks in source order
-  std::sort(remote.begin(), remote.end(), [](const Cand& a, const Cand& b) {
+  auto by_package = [](const Cand& a, const Cand& b) {
     if (a.s != b.s) return a.s < b.s;
     if (a.r != b.r) return a.r < b.r;
     if (a.p.src_buf != b.p.src_buf) return a.p.src_buf < b.p.src_buf;
     return a.p.src_off < b.p.src_off;
-  });
+  };
+  std::sort(remote.begin(), remote.end(), by_package);
   auto chunk_bytes = [&](const Piece& p) {
     int64_t b = (int64_t)p.nx * p.ny * es;
     return (b + 255) / 256 * 256;  // every message block starts 256-byte aligned
   };
-  int64_t total_msg = 0;
-  for (const Cand& c : remote) total_msg += chunk_bytes(c.p);
+  int64_t total_msg = 0, biggest = 0;
+  for (const Cand& c : remote) {
+    total_msg += chunk_bytes(c.p);
+    biggest = std::max(biggest, chunk_bytes(c.p));
+  }
   int64_t cap = choose_cap ? choose_cap(total_msg) : cfg.workspace_cap;
-  int64_t biggest = 0;
-  for (const Cand& c : remote) biggest = std::max(biggest, chunk_bytes(c.p));
+  if (biggest > cap) {
+    // a small workspace: cut the blocks so that each fits one wave
+    split_pieces(remote, std::max<int64_t>(1, (cap - 255) / es));
+    std::sort(remote.begin(), remote.end(), by_package);
+    biggest = 0;
+    for (const Cand& c : remote) biggest = std::max(biggest, chunk_bytes(c.p));
+  }
   cap = std::max(cap, biggest);
 
   const int32_t msg_buf = 2 * n * (items.empty() ? 0 : items[0].A->nranks);
-  std::vector<Cut> chunk_cuts;
   size_t k = 0;
   while (k < remote.size()) {
     std::vector<Piece> pack, unpack;
@@ -384,18 +402,14 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
       pk.dst_ld = pk.nx;
       finish_piece(pk, es);
       pack.push_back(pk);
-      // unpack-transform: message -> A, in rectangles of the usual size cut
-      // from the chunk (stored in the source's orientation)
+      // unpack-transform: message -> A, the block read back in the source's
+      // orientation
       Piece up = q;
       up.src_buf = msg_buf;
       up.src_off = off / es;
       up.src_ld = T ? q.ny : q.nx;
-      cuts_of(q, unpack_cap, cfg.transpose_piece_factor, chunk_cuts);
-      for (const Cut& c : chunk_cuts) {
-        Piece u = sub_piece(up, c);
-        finish_piece(u, es);
-        unpack.push_back(u);
-      }
+      finish_piece(up, es);
+      unpack.push_back(up);
       off += chunk_bytes(q);
       ++k;
     }
@@ -428,13 +442,12 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     std::sort(unpack.begin(), unpack.end(), by_dst);
     Wave w;
     w.msg_bytes = off;
-    w.pack = add_launch(hp, pack, cfg_remote, n);
-    w.unpack = add_launch(hp, unpack, last && COSTA_MERGE_DIRECT ? group_cfg(remote_total + local_total)
-                                                                 : cfg_remote, n);
+    w.pack = add_launch(hp, pack, es, n);
+    w.unpack = add_launch(hp, unpack, es, n);
     hp.workspace_bytes = std::max(hp.workspace_bytes, off);
     hp.waves.push_back(w);
   }
-  hp.direct = add_launch(hp, direct, cfg_local, n);  // empty when merged above
+  hp.direct = add_launch(hp, direct, es, n);  // empty when merged above
   hp.plan_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
 }
 

@@ -18,17 +18,12 @@ struct ItemDesc {
 struct PlanConfig {
   int elem_size;           // bytes per element
   int64_t workspace_cap;   // max message bytes per wave (>= 1)
-  int64_t max_piece_elems; // split rectangles larger than this
-  int64_t min_group_elems; // a workgroup takes consecutive rectangles up to this many elements
-  int64_t min_group_elems_t;  // ...while they are transposed (their tiles are pipelined across rectangles)
-  int32_t max_group_pieces;
-  int64_t target_groups;   // aim for at least this many workgroups per launch
-  int64_t transpose_piece_factor;  // transposed rectangles may be this many times larger
+  int64_t max_piece_elems; // split rectangles larger than this (keeps per-rectangle indices in 32 bits)
 };
 
 struct HostPlan {
   std::vector<Piece> pieces;    // every launch's rectangles, concatenated
-  std::vector<int32_t> groups;  // per launch: ngroups+1 start indices into `pieces`
+  std::vector<int32_t> tasks;   // every launch's workgroups: index of the rectangle each starts with
   LaunchRange direct;
   std::vector<Wave> waves;
   int64_t workspace_bytes = 0;  // max message bytes of a wave

@@ -18,6 +18,54 @@ C = pytest.importorskip("paper_2106_06601_amd")
 
 PACK, UNPACK, DIRECT = 0, 1, 2
 
+# The task contract of the kernels: a transposed rectangle (flag 1) is moved
+# by one workgroup per LDS tile of its class (flags 4: middle, 8: narrow,
+# else big), tiles of (tx, ty) elements; a row walk by one workgroup per 256
+# units (16-byte vectors when flag 2 is set, else elements); a run of small
+# row walks (each but the last flagged 16) by one workgroup for all of them.
+TILES = {4: [(128, 32), (64, 64), (32, 64)], 8: [(128, 16), (64, 32), (32, 32)],
+         16: [(256, 16), (128, 16), (64, 16)]}
+LANES, GROUP_UNITS, GROUP_PIECES = 256, 128, 8
+
+
+def check_tasks(pieces, es):
+    """Every launch's workgroups are handed out in rectangle order without gaps
+    or overlaps, each rectangle gets the number its tiles or units need, and
+    runs of small rectangles fit one workgroup."""
+    launches = {}
+    for i, p in enumerate(pieces):
+        launches.setdefault((int(p["kind"]), int(p["wave"])), []).append(p)
+    for ps in launches.values():
+        nxt = 0
+        run = None  # (units so far, rectangles so far, item, vector width) of an open run
+        for p in ps:
+            nx, ny, fl = int(p["nx"]), int(p["ny"]), int(p["flags"])
+            if run is not None:  # continues the run of the previous rectangle
+                assert not fl & 1 and int(p["group"]) == nxt - 1 and int(p["ntasks"]) == 1
+                units = nx * ny // (16 // es if fl & 2 and es < 16 else 1)
+                assert units <= GROUP_UNITS and int(p["item"]) == run[2] and (fl & 2) == run[3]
+                run = (run[0] + units, run[1] + 1, run[2], run[3])
+                assert run[0] <= LANES and run[1] <= GROUP_PIECES
+                if not fl & 16:
+                    run = None
+                continue
+            assert int(p["group"]) == nxt, "workgroups of a launch are not handed out in order"
+            if fl & 1:
+                cls = 2 if fl & 8 else 1 if fl & 4 else 0
+                tx, ty = TILES[es][cls]
+                assert cls == (0 if nx > TILES[es][1][0] else 1 if nx > TILES[es][2][0] else 2)
+                need = -(-nx // tx) * -(-ny // ty)
+                assert not fl & 16
+            else:
+                units = nx * ny // (16 // es if fl & 2 and es < 16 else 1)
+                need = -(-units // LANES)
+                if fl & 16:
+                    assert units <= GROUP_UNITS and need == 1
+                    run = (units, 1, int(p["item"]), fl & 2)
+            assert int(p["ntasks"]) == need, f"{p} needs {need} workgroups"
+            nxt += need
+        assert run is None, "a run of small rectangles ends with the launch's last rectangle flagged"
+
 
 def _descs(w):
     keep, descs = [], []
@@ -40,6 +88,7 @@ def replay(w, sigma=None, limit=None):
             C.costa_set_workspace_limit(0)
     n, P = len(w.items), w.items[0].A.nranks
     es = synth.ITEMSIZE[w.dtype]
+    check_tasks(pieces, es)
     npt = oracle.NUMPY[w.dtype]
     sg = list(range(P)) if sigma is None else list(sigma)
     inv = [0] * P
@@ -169,7 +218,8 @@ def test_full_size_plans_stay_in_bounds(name):
     assert (x["src_off"] >= 0).all() and (x["dst_off"] >= 0).all()
     assert (src_end < sizes[x["src_buf"]]).all()
     assert (dst_end < sizes[x["dst_buf"]]).all()
-    assert (nx >= 1).all() and (ny >= 1).all() and (nx * ny <= 1 << 16).all()
+    assert (nx >= 1).all() and (ny >= 1).all() and (nx * ny <= 1 << 22).all()
+    check_tasks(x, es)
     # rows of a rectangle do not wrap into each other
     assert ((ny == 1) | (x["dst_ld"] >= nx)).all()
     written = (nx * ny)[x["kind"] != PACK].sum()
