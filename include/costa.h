@@ -297,6 +297,7 @@ typedef struct {
   int32_t src_buf, dst_buf, nx, ny, item, flags;
   int64_t ntasks; /* workgroups that move it (LDS tiles or row-walk chunks); small
                      rectangles moved together by one workgroup report 1 each */
+  int32_t tile_x, tile_y; /* LDS tile of a transposed rectangle (0 otherwise) */
 } costa_piece_info;
 
 /* Writes the rectangles of the plan a transform with these arguments would

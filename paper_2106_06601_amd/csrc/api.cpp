@@ -242,7 +242,7 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePla
   }
   LaunchSpec spec{mode, conj, lr.has_transpose};
   HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_tasks + lr.task_begin, lr.ntasks, d_bufs, d_items,
-                           allow_wide, stream));
+                           allow_wide, lr.xcd_remap, stream));
   if (S.timing) {
     HIP_OR_FAIL(hipEventRecord(e1, stream));
     costa_kernel_kind kk = kind == KIND_PACK ? COSTA_KERNEL_PACK
@@ -513,6 +513,9 @@ extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const co
       o.item = q.item;
       o.flags = q.flags;
       o.ntasks = end - q.task0;
+      o.tile_x = tile_x_of(q.tile);
+      o.tile_y = tile_y_of(q.tile);
+
     }
   };
   emit(hp->direct, COSTA_KERNEL_DIRECT, 0);

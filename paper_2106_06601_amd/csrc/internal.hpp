@@ -95,18 +95,12 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 //   src_off + x*src_ld + y   (flag TRANSPOSE set: contiguous along y).
 // PIECE_WIDE: a non-transposed rectangle whose offsets, strides and width
 //   allow 16-byte vectors.
-// PIECE_TILE_MID / PIECE_TILE_NARROW: a transposed rectangle staged through
-//   the middle or the narrow LDS tile shape (tile_shape below) instead of
-//   the big one.
 // PIECE_GROUP_NEXT: the next rectangle of the launch is moved by the same
 //   workgroup (a run of small rectangles shares one workgroup).
-enum : int32_t {
-  PIECE_TRANSPOSE = 1,
-  PIECE_WIDE = 2,
-  PIECE_TILE_MID = 4,
-  PIECE_TILE_NARROW = 8,
-  PIECE_GROUP_NEXT = 16
-};
+// A transposed rectangle is moved in LDS tiles of tile_x x tile_y elements
+// (tile_x along the destination's contiguous direction; choose_tile below),
+// packed into `tile` with tile_pack.
+enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_GROUP_NEXT = 16 };
 
 struct alignas(16) Piece {
   int64_t src_off;
@@ -120,7 +114,7 @@ struct alignas(16) Piece {
   int32_t item;     // pair of a batched call (selects alpha, beta, mode)
   int32_t flags;
   int32_t task0;    // first workgroup of its launch that moves it
-  int32_t pad;
+  int32_t tile;     // transposed rectangles: tile_pack(tile_x, tile_y)
 };
 static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
 
@@ -135,29 +129,32 @@ constexpr int32_t kGroupPiecesMax = 8;
 // Elements per 16-byte unit of a PIECE_WIDE rectangle.
 constexpr int32_t wide_elems(int32_t es) { return es >= 16 ? 1 : 16 / es; }
 
-// LDS tile of a transposed rectangle: tx elements along the destination's
-// contiguous direction (store runs), ty along the source's (load runs).
-// Class 0 (big), 1 (PIECE_TILE_MID), 2 (PIECE_TILE_NARROW); the planner picks
-// the class from the rectangle's width nx (tile_class).
-struct TileShape {
-  int32_t tx, ty;
-};
-#ifndef COSTA_C16_BIG_TX
-#define COSTA_C16_BIG_TX 256
-#endif
-constexpr TileShape tile_shape(int32_t es, int32_t cls) {
-  return es >= 16 ? (cls == 0 ? TileShape{COSTA_C16_BIG_TX, 16} : cls == 1 ? TileShape{128, 16} : TileShape{64, 16})
-       : es == 8  ? (cls == 0 ? TileShape{128, 16} : cls == 1 ? TileShape{64, 32} : TileShape{32, 32})
-                  : (cls == 0 ? TileShape{128, 32} : cls == 1 ? TileShape{64, 64} : TileShape{32, 64});
-}
-constexpr int32_t tile_class(int32_t es, int32_t nx) {
-  return nx > tile_shape(es, 1).tx ? 0 : nx > tile_shape(es, 2).tx ? 1 : 2;
-}
-constexpr int32_t tile_class_of_flags(int32_t flags) {
-  return (flags & PIECE_TILE_NARROW) ? 2 : (flags & PIECE_TILE_MID) ? 1 : 0;
-}
-constexpr int32_t tile_lds_bytes(int32_t es, int32_t cls) {
-  return tile_shape(es, cls).tx * (tile_shape(es, cls).ty + 1) * es;
+// LDS tiles of transposed rectangles.  A tile holds at most
+// tile_budget(es) elements and is at most tile_max_x(es) wide; its rows (one
+// per x) take tile_y | 1 elements in LDS, an odd stride, so that lanes
+// reading one LDS row element each (consecutive x) hit distinct banks.
+// Small rectangles are one tile; larger ones are cut into tiles of equal
+// width (at most tile_max_x) and equal height (as many rows as the budget
+// allows), so that every lane of a workgroup has an element.
+constexpr int32_t tile_budget(int32_t es) { return es >= 16 ? 4096 : es == 8 ? 2048 : 4096; }
+constexpr int32_t tile_max_x(int32_t es) { return es >= 16 ? 256 : 128; }
+constexpr int32_t tile_lds_elems(int32_t es) { return tile_budget(es) + tile_max_x(es); }
+constexpr int32_t tile_pack(int32_t tx, int32_t ty) { return tx | ty << 16; }
+constexpr int32_t tile_x_of(int32_t t) { return t & 0xffff; }
+constexpr int32_t tile_y_of(int32_t t) { return t >> 16; }
+inline void choose_tile(int32_t es, int32_t nx, int32_t ny, int32_t& tx, int32_t& ty) {
+  const int32_t budget = tile_budget(es), maxx = tile_max_x(es);
+  if (nx <= maxx && (int64_t)nx * ny <= budget) {
+    tx = nx;
+    ty = ny;
+    return;
+  }
+  const int32_t ntx = (nx + maxx - 1) / maxx;
+  tx = (nx + ntx - 1) / ntx;
+  ty = budget / tx;
+  if (ty > ny) ty = ny;
+  const int32_t nty = (ny + ty - 1) / ty;
+  ty = (ny + nty - 1) / nty;
 }
 
 // Per-pair parameters of a call, read by the kernels.
@@ -181,6 +178,7 @@ struct LaunchRange {
   int64_t task_begin = 0, ntasks = 0;
   int64_t elems = 0;
   bool has_transpose = false;
+  int32_t xcd_remap = 0;  // workgroup order: 0 dispatch order, -1 one range per XCD, K > 0 runs of K per XCD
   std::vector<int64_t> item_elems;  // elements of each pair in this launch
 };
 
@@ -201,9 +199,13 @@ struct LaunchSpec {
 };
 // pieces: the plan's rectangles (global indices); tasks: the launch's
 // ntasks entries.
+// xcd_remap (workgroups are dispatched round-robin over the 8 XCDs): 0 runs
+// task b in workgroup b; -1 hands each XCD one contiguous range of the
+// launch slice; K > 0 hands each XCD runs of K consecutive tasks, the XCDs
+// advancing through the launch side by side.
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
                         const int32_t* tasks, int64_t ntasks, void* const* bufs, const ItemParam* items,
-                        int32_t allow_wide, hipStream_t stream);
+                        int32_t allow_wide, int32_t xcd_remap, hipStream_t stream);
 
 struct VolumeArgs {
   const Interval* rows;

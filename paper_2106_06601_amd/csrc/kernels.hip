@@ -20,9 +20,6 @@ namespace costa {
 namespace {
 
 // Tuning switches (compile-time; the defaults are the measured best).
-#ifndef COSTA_XCD_REMAP
-#define COSTA_XCD_REMAP 0  // contiguous workgroup ranges per XCD (off: dispatch order is address order)
-#endif
 #ifndef COSTA_NT_LOADS
 #define COSTA_NT_LOADS 1  // row walks: each source line is read once
 #endif
@@ -41,15 +38,24 @@ namespace {
 
 constexpr int kThreads = kThreadsPerTask;
 
-// Workgroup b of n (dispatched round-robin over the 8 XCDs) gets the b-th
-// slot of a contiguous range per XCD, so consecutive groups share an L2.
-__device__ __forceinline__ int32_t xcd_remap(int32_t b, int32_t n) {
-  if (!COSTA_XCD_REMAP) return b;
+// The task of workgroup b of n (workgroups are dispatched round-robin over
+// the 8 XCDs, b % 8 being b's XCD).  remap 0: task b.  remap -1: the b/8-th
+// task of a contiguous range per XCD.  remap K > 0: each block of 8K
+// workgroups takes a block of 8K tasks, XCD x its K consecutive tasks from
+// x*K (the tail that fills no block keeps dispatch order).
+__device__ __forceinline__ int32_t xcd_order(int32_t b, int32_t n, int32_t remap) {
   constexpr int32_t X = 8;
-  const int32_t q = n / X, r = n % X;
-  const int32_t xcd = b % X, idx = b / X;
-  const int32_t start = xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q;
-  return start + idx;
+  if (remap == 0) return b;
+  if (remap < 0) {
+    const int32_t q = n / X, r = n % X;
+    const int32_t xcd = b % X, idx = b / X;
+    const int32_t start = xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q;
+    return start + idx;
+  }
+  const int32_t blk = X * remap;
+  if (b >= n - n % blk) return b;
+  const int32_t j = b % blk;
+  return b - j + (j % X) * remap + j / X;
 }
 
 template <typename S, int N>
@@ -149,11 +155,8 @@ struct TypeTraits {
   static constexpr int ES = (int)sizeof(S) * NS;  // bytes per element
   static constexpr int WIDE_NEL = wide_elems(ES); // elements per 16-byte unit
   static constexpr bool NT_WALK = COSTA_NT_LOADS && ES <= COSTA_NT_LOADS_MAX_ES;
-  static constexpr int lds_elems(int cls) { return tile_shape(ES, cls).tx * (tile_shape(ES, cls).ty + 1); }
-  static constexpr int LDS_ELEMS = lds_elems(0) > lds_elems(1) ? (lds_elems(0) > lds_elems(2) ? lds_elems(0)
-                                                                                                : lds_elems(2))
-                                                               : (lds_elems(1) > lds_elems(2) ? lds_elems(1)
-                                                                                              : lds_elems(2));
+  static constexpr int LDS_ELEMS = tile_lds_elems(ES);
+  static constexpr int TILE_PASSES = tile_budget(ES) / kThreads;  // elements per lane of a full tile
 };
 
 // y = u / n and x = u - y*n from a float estimate of the quotient, corrected
@@ -234,56 +237,75 @@ __device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int3
   }
 }
 
-// One TX x TY tile of a rectangle whose source runs along y while the
-// destination runs along x, staged through LDS (one padding column against
-// bank conflicts).  Loads are coalesced along the source (runs of TY
-// elements), stores along the destination (runs of TX elements).  Tile c of
-// the rectangle; tiles are numbered along x first.
-template <typename S, bool CPLX, int MODE, bool CONJ, int TX, int TY>
+// One LDS tile of a rectangle whose source runs along y while the
+// destination runs along x: tile c (tiles numbered along x first) of
+// tile_x x tile_y elements, cut at the rectangle's edges to w x h.  Loads
+// take the tile's elements in source order (y fastest: runs of h elements),
+// stores in destination order (x fastest: runs of w elements); lanes walk
+// the flattened tile, so every lane has work whatever its shape.  In LDS
+// element (x, y) sits at x * (tile_y | 1) + y.  When A is read (beta != 0)
+// its elements are loaded together with the source, before the barrier:
+// loads issued between the stores could not be moved ahead of them (the
+// compiler cannot tell that they touch other elements) and would each wait
+// for a full memory round trip.
+template <typename S, bool CPLX, int MODE, bool CONJ>
 __device__ __forceinline__ void move_tile(const Piece* __restrict__ pieces, int32_t pi, int32_t c,
                                           void* const* __restrict__ bufs, Vec<S, CPLX ? 2 : 1>* lds, S ar, S ai,
                                           S br, S bi) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
-  E (*tile)[TY + 1] = reinterpret_cast<E (*)[TY + 1]>(lds);
-  constexpr int LROWS = kThreads / TY;  // x rows per load pass
-  constexpr int SROWS = kThreads / TX;  // y rows per store pass
-  constexpr int NL = TX / LROWS;        // loads per lane
-  static_assert(kThreads % TX == 0 && kThreads % TY == 0 && TX % LROWS == 0 && TY % SROWS == 0,
-                "the load and store passes must cover the tile exactly");
-  static_assert(TX * (TY + 1) <= TT::LDS_ELEMS, "tile larger than the launch's LDS");
+  constexpr int NP = TT::TILE_PASSES;
   const Piece& p = pieces[pi];
   const int32_t tid = threadIdx.x;
-  const int32_t ntx = (p.nx + TX - 1) / TX;
-  const int32_t tx = (c % ntx) * TX, ty = (c / ntx) * TY;
-  const int32_t ly = tid % TY, lx0 = tid / TY;  // load mapping
-  const E* __restrict__ se = reinterpret_cast<const E*>(bufs[p.src_buf]) + p.src_off;
-  E v[NL];
-  const bool yin = ty + ly < p.ny;
+  const int32_t tx = tile_x_of(p.tile), ty = tile_y_of(p.tile);
+  const int32_t stride = ty | 1;
+  const int32_t ntx = (p.nx + tx - 1) / tx;
+  const int32_t x0 = (c % ntx) * tx, y0 = (c / ntx) * ty;
+  const int32_t w = min(tx, p.nx - x0), h = min(ty, p.ny - y0);
+  const int32_t n = w * h;
+  const E* __restrict__ se = reinterpret_cast<const E*>(bufs[p.src_buf]) + p.src_off + (int64_t)x0 * p.src_ld + y0;
+  E* __restrict__ de = reinterpret_cast<E*>(bufs[p.dst_buf]) + p.dst_off + (int64_t)y0 * p.dst_ld + x0;
+  E v[NP];
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int32_t x = tx + lx0 + k * LROWS;
-    if (x < p.nx && yin) v[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)x * p.src_ld + (ty + ly)));
+  for (int k = 0; k < NP; ++k) {
+    const int32_t i = k * kThreads + tid;
+    if (i < n) {
+      int32_t xl, yl;
+      divmod(i, h, xl, yl);
+      v[k] = load<COSTA_NT_TILE_LOADS>(se + ((int64_t)xl * p.src_ld + yl));
+    }
+  }
+  E a[MODE == MODE_AXPBY ? NP : 1];
+  if constexpr (MODE == MODE_AXPBY) {
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+      const int32_t i = k * kThreads + tid;
+      if (i < n) {
+        int32_t yl, xl;
+        divmod(i, w, yl, xl);
+        a[k] = load<COSTA_NT_ALOADS>(de + ((int64_t)yl * p.dst_ld + xl));
+      }
+    }
   }
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    const int32_t lx = lx0 + k * LROWS;
-    if (tx + lx < p.nx && yin) tile[lx][ly] = v[k];
+  for (int k = 0; k < NP; ++k) {
+    const int32_t i = k * kThreads + tid;
+    if (i < n) {
+      int32_t xl, yl;
+      divmod(i, h, xl, yl);
+      lds[xl * stride + yl] = v[k];
+    }
   }
   __syncthreads();
-  E* __restrict__ de = reinterpret_cast<E*>(bufs[p.dst_buf]) + p.dst_off;
-  const int32_t sx = tid % TX, sy0 = tid / TX;  // store mapping
-  const int32_t x = tx + sx;
-  if (x >= p.nx) return;
 #pragma unroll
-  for (int k = 0; k < TY / SROWS; ++k) {
-    const int32_t ly2 = sy0 + k * SROWS;
-    const int32_t yy = ty + ly2;
-    if (yy < p.ny) {
-      E* o = de + ((int64_t)yy * p.dst_ld + x);
-      E a;
-      if constexpr (MODE == MODE_AXPBY) a = load<COSTA_NT_ALOADS>(o);
-      store(o, combine<S, TT::NS, CPLX, MODE, CONJ>(tile[sx][ly2], a, ar, ai, br, bi));
+  for (int k = 0; k < NP; ++k) {
+    const int32_t i = k * kThreads + tid;
+    if (i < n) {
+      int32_t yl, xl;
+      divmod(i, w, yl, xl);
+      store(de + ((int64_t)yl * p.dst_ld + xl),
+            combine<S, TT::NS, CPLX, MODE, CONJ>(lds[xl * stride + yl], a[MODE == MODE_AXPBY ? k : 0], ar, ai, br,
+                                                 bi));
     }
   }
 }
@@ -293,7 +315,6 @@ template <typename S, bool CPLX, int MODE, bool CONJ, bool HAS_T>
 __device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int32_t pi, int32_t flags, int32_t c,
                                           void* const* __restrict__ bufs, const ItemParam* __restrict__ ip,
                                           int32_t allow_wide, Vec<S, CPLX ? 2 : 1>* lds) {
-  using TT = TypeTraits<S, CPLX>;
   S ar = S(0), ai = S(0), br = S(0), bi = S(0);
   if constexpr (MODE != MODE_COPY) {
     ar = (S)ip->alpha[0];
@@ -303,11 +324,7 @@ __device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int3
   }
   if constexpr (HAS_T) {
     if (flags & PIECE_TRANSPOSE) {
-      constexpr TileShape t0 = tile_shape(TT::ES, 0), t1 = tile_shape(TT::ES, 1), t2 = tile_shape(TT::ES, 2);
-      const int32_t cls = tile_class_of_flags(flags);
-      if (cls == 0) move_tile<S, CPLX, MODE, CONJ, t0.tx, t0.ty>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
-      else if (cls == 1) move_tile<S, CPLX, MODE, CONJ, t1.tx, t1.ty>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
-      else move_tile<S, CPLX, MODE, CONJ, t2.tx, t2.ty>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
+      move_tile<S, CPLX, MODE, CONJ>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
       return;
     }
   }
@@ -326,12 +343,12 @@ constexpr int MODE_ANY = 3;
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __device__ __forceinline__ void mover_body(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks,
                                            int32_t task_off, void* const* __restrict__ bufs,
-                                           const ItemParam* __restrict__ items, int32_t allow_wide) {
+                                           const ItemParam* __restrict__ items, int32_t allow_wide,
+                                           int32_t remap) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
   __shared__ E lds[HAS_T ? TT::LDS_ELEMS : 1];
-  const int32_t b = task_off + (COSTA_XCD_REMAP ? xcd_remap((int32_t)blockIdx.x, (int32_t)gridDim.x)
-                                                : (int32_t)blockIdx.x);
+  const int32_t b = task_off + xcd_order((int32_t)blockIdx.x, (int32_t)gridDim.x, remap);
   const int32_t pi = tasks[b];
   const int32_t c = b - pieces[pi].task0;
   if constexpr (KIND == KIND_PACK) {
@@ -369,15 +386,17 @@ constexpr bool big_lds() {
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
 costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
-            void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide) {
-  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide);
+            void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
+            int32_t remap) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide, remap);
 }
 
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 costa_mover_lds(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
-                void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide) {
-  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide);
+                void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
+            int32_t remap) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide, remap);
 }
 
 // Volume of the grid overlay: every overlay block (k, l) adds its element
@@ -418,6 +437,7 @@ struct Launch {
   void* const* bufs;
   const ItemParam* items;
   int32_t allow_wide;
+  int32_t remap;
 };
 
 // Separable volume, step 1: histogram of overlay interval lengths by (class
@@ -456,10 +476,10 @@ template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 hipError_t go(const Launch& l) {
   if constexpr (big_lds<S, CPLX, HAS_T>())
     hipLaunchKernelGGL((costa_mover_lds<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
-                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide);
+                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide, l.remap);
   else
     hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
-                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide);
+                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide, l.remap);
   return hipGetLastError();
 }
 
@@ -494,14 +514,15 @@ hipError_t launch_typed(MoverKind kind, const LaunchSpec& spec, const Launch& l)
 
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
                         const int32_t* tasks, int64_t ntasks, void* const* bufs, const ItemParam* items,
-                        int32_t allow_wide, hipStream_t stream) {
+                        int32_t allow_wide, int32_t xcd_remap, hipStream_t stream) {
   if (ntasks <= 0) return hipSuccess;
   if (ntasks > INT32_MAX) return hipErrorInvalidValue;
   // one workgroup per task, in slices that keep the grid below 2^32 work-items
   constexpr int64_t kSlice = 1 << 23;
   for (int64_t off = 0; off < ntasks; off += kSlice) {
     const int64_t n = ntasks - off < kSlice ? ntasks - off : kSlice;
-    Launch l{dim3((unsigned)n), dim3(kThreads), stream, pieces, tasks, (int32_t)off, bufs, items, allow_wide};
+    Launch l{dim3((unsigned)n), dim3(kThreads), stream, pieces, tasks, (int32_t)off, bufs, items, allow_wide,
+             xcd_remap};
     hipError_t e = hipErrorInvalidValue;
     switch (dtype) {
       case COSTA_R64: e = launch_typed<double, false>(kind, spec, l); break;

@@ -128,7 +128,7 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
       p.src_buf = nitems * P + item * P + s;
       p.item = item;
       p.task0 = 0;
-      p.pad = 0;
+      p.tile = 0;
       c.kx0 = kx;
       c.kx1 = kx + 1;
       c.ly_end = ly + 1;
@@ -235,19 +235,46 @@ void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
 // Sets the flags the kernels read: 16-byte vectors for row walks, the LDS
 // tile class of transposed rectangles.
 void finish_piece(Piece& p, int elem_size) {
-  p.flags &= ~(PIECE_WIDE | PIECE_TILE_MID | PIECE_TILE_NARROW | PIECE_GROUP_NEXT);
+  p.flags &= ~(PIECE_WIDE | PIECE_GROUP_NEXT);
   p.task0 = 0;
-  p.pad = 0;
+  p.tile = 0;
   if (p.flags & PIECE_TRANSPOSE) {
-    const int32_t cls = tile_class(elem_size, p.nx);
-    if (cls == 1) p.flags |= PIECE_TILE_MID;
-    if (cls == 2) p.flags |= PIECE_TILE_NARROW;
+    int32_t tx, ty;
+    choose_tile(elem_size, p.nx, p.ny, tx, ty);
+    p.tile = tile_pack(tx, ty);
     return;
   }
   const int64_t want = wide_elems(elem_size);
   if (want > 1 && p.nx % want == 0 && p.src_off % want == 0 && p.dst_off % want == 0 &&
       (p.ny == 1 || (p.src_ld % want == 0 && p.dst_ld % want == 0)))
     p.flags |= PIECE_WIDE;
+}
+
+// Workgroup order per launch: 0 = dispatch order, 1 = runs of
+// COSTA_XCD_CHUNK tasks per XCD, 2 = one contiguous range per XCD when the
+// launch's tasks are all of one kind (all row-walk chunks or all LDS tiles,
+// so that equal ranges are equal work) and nearly all of its elements lie in
+// rectangles whose runs start and end on 128-byte lines.  Measured on MI355X:
+// +5 to +8% on such launches; -5 to -8% on launches of short runs that share
+// lines with their neighbours; -40% on a launch whose first half is row
+// walks and second half LDS tiles (four XCDs idle while four finish the
+// tiles).
+#ifndef COSTA_XCD_POLICY
+#define COSTA_XCD_POLICY 2
+#endif
+#ifndef COSTA_XCD_CHUNK
+#define COSTA_XCD_CHUNK 64
+#endif
+
+// Whether every run of the rectangle (its rows in the source and in the
+// destination) starts and ends on a 128-byte line.
+bool line_aligned(const Piece& p, int es) {
+  auto al = [&](int64_t v) { return v * es % 128 == 0; };
+  const bool T = p.flags & PIECE_TRANSPOSE;
+  const int64_t srun = T ? p.ny : p.nx;  // source run length
+  const int64_t sstep = T ? p.nx : p.ny;  // number of source runs
+  return al(p.dst_off) && al(p.nx) && (p.ny == 1 || al(p.dst_ld)) && al(p.src_off) && al(srun) &&
+         (sstep == 1 || al(p.src_ld));
 }
 
 // Appends one launch: its rectangles and the workgroups that move them, in
@@ -263,7 +290,8 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   if (hp.pieces.size() + ps.size() > (size_t)INT32_MAX) throw std::bad_alloc();
   const int32_t base = (int32_t)hp.pieces.size();
   int64_t b = 0;
-  int64_t g_task = -1;  // workgroup of the open run of small rectangles
+  // the open run of small row walks
+  int64_t g_task = -1;
   int64_t g_units = 0;
   int32_t g_count = 0;
   size_t g_last = 0;
@@ -277,12 +305,12 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     const int32_t pi = base + (int32_t)k;
     if (p.flags & PIECE_TRANSPOSE) {
       lr.has_transpose = true;
-      const TileShape ts = tile_shape(es, tile_class_of_flags(p.flags));
-      const int64_t n = (int64_t)((p.nx + ts.tx - 1) / ts.tx) * ((p.ny + ts.ty - 1) / ts.ty);
+      g_task = -1;
+      const int32_t tx = tile_x_of(p.tile), ty = tile_y_of(p.tile);
+      const int64_t n = (int64_t)((p.nx + tx - 1) / tx) * ((p.ny + ty - 1) / ty);
       p.task0 = (int32_t)b;
       hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
       b += n;
-      g_task = -1;
       continue;
     }
     const bool wide = p.flags & PIECE_WIDE;
@@ -313,6 +341,15 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   }
   if (b > INT32_MAX) throw std::bad_alloc();
   lr.ntasks = b;
+  int64_t aligned = 0, transposed = 0;
+  for (const Piece& p : ps) {
+    if (line_aligned(p, es)) aligned += (int64_t)p.nx * p.ny;
+    if (p.flags & PIECE_TRANSPOSE) transposed += (int64_t)p.nx * p.ny;
+  }
+  const bool one_kind = transposed == 0 || transposed == lr.elems;
+  lr.xcd_remap = COSTA_XCD_POLICY == 1 ? COSTA_XCD_CHUNK
+                 : COSTA_XCD_POLICY == 2 && one_kind && lr.elems > 0 && 10 * aligned >= 9 * lr.elems ? -1
+                                                                                                      : 0;
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
 }

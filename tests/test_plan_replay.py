@@ -19,12 +19,14 @@ C = pytest.importorskip("paper_2106_06601_amd")
 PACK, UNPACK, DIRECT = 0, 1, 2
 
 # The task contract of the kernels: a transposed rectangle (flag 1) is moved
-# by one workgroup per LDS tile of its class (flags 4: middle, 8: narrow,
-# else big), tiles of (tx, ty) elements; a row walk by one workgroup per 256
-# units (16-byte vectors when flag 2 is set, else elements); a run of small
-# row walks (each but the last flagged 16) by one workgroup for all of them.
-TILES = {4: [(128, 32), (64, 64), (32, 64)], 8: [(128, 16), (64, 32), (32, 32)],
-         16: [(256, 16), (128, 16), (64, 16)]}
+# by one workgroup per LDS tile (tile_x x tile_y elements, tiles of at most
+# BUDGET[es] elements and MAXX[es] wide; a rectangle that fits is one tile,
+# wider ones use as few tile columns as MAXX allows); a row walk by one
+# workgroup per 256 units (16-byte vectors when flag 2 is set, else
+# elements); a run of small row walks (each but the last flagged 16) by one
+# workgroup for all of them.
+BUDGET = {4: 4096, 8: 2048, 16: 4096}
+MAXX = {4: 128, 8: 128, 16: 256}
 LANES, GROUP_UNITS, GROUP_PIECES = 256, 128, 8
 
 
@@ -51,9 +53,13 @@ def check_tasks(pieces, es):
                 continue
             assert int(p["group"]) == nxt, "workgroups of a launch are not handed out in order"
             if fl & 1:
-                cls = 2 if fl & 8 else 1 if fl & 4 else 0
-                tx, ty = TILES[es][cls]
-                assert cls == (0 if nx > TILES[es][1][0] else 1 if nx > TILES[es][2][0] else 2)
+                tx, ty = int(p["tile_x"]), int(p["tile_y"])
+                assert 1 <= tx <= min(nx, MAXX[es]) and 1 <= ty <= ny and tx * ty <= BUDGET[es]
+                if nx <= MAXX[es] and nx * ny <= BUDGET[es]:
+                    assert (tx, ty) == (nx, ny), "a rectangle that fits a tile is one tile"
+                else:
+                    assert -(-nx // tx) == -(-nx // MAXX[es]), "more tile columns than needed"
+                    assert 2 * tx * (ty + 1) > BUDGET[es] or ty == ny, "tiles far below the budget"
                 need = -(-nx // tx) * -(-ny // ty)
                 assert not fl & 16
             else:
