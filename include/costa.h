@@ -298,10 +298,14 @@ typedef struct {
   int64_t ntasks; /* workgroups that move it (LDS tiles or row-walk chunks); small
                      rectangles moved together by one workgroup report 1 each */
   int32_t tile_x, tile_y; /* LDS tile of a transposed rectangle (0 otherwise) */
+  int32_t launch;         /* index of its kernel launch in the plan's launch order */
+  int32_t reserved;
 } costa_piece_info;
 
 /* Writes the rectangles of the plan a transform with these arguments would
- * use, in launch order (DIRECT, then PACK and UNPACK of each wave), into
+ * use, in launch order (DIRECT, then PACK and UNPACK of each wave; a DIRECT
+ * or UNPACK step that holds both transposed and other rectangles is two
+ * launches, the transposed ones first), into
  * out[0..capacity); *count = their total number (call with capacity 0 to
  * size the array).  Host only; no device work. */
 costa_status costa_plan_export(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,

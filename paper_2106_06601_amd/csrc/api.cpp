@@ -403,17 +403,21 @@ costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_des
   int32_t mode = ipar[0].mode, conj = ipar[0].conj;
   for (int32_t k = 1; k < n; ++k)
     if (ipar[k].mode != mode || ipar[k].conj != conj) mode = -1;
-  st = run_range(S, KIND_DIRECT, dt, *dp, hp.direct, mode, conj, d_bufs, d_items, wide,
-                 range_bytes(hp.direct, es, reads_a), stream);
-  if (st != COSTA_SUCCESS) return st;
+  for (const LaunchRange& lr : hp.direct) {
+    st = run_range(S, KIND_DIRECT, dt, *dp, lr, mode, conj, d_bufs, d_items, wide, range_bytes(lr, es, reads_a),
+                   stream);
+    if (st != COSTA_SUCCESS) return st;
+  }
   std::vector<char> no_read(n, 0);
   for (const Wave& w : hp.waves) {
     st = run_range(S, KIND_PACK, dt, *dp, w.pack, MODE_COPY, 0, d_bufs, d_items, wide,
                    range_bytes(w.pack, es, no_read), stream);
     if (st != COSTA_SUCCESS) return st;
-    st = run_range(S, KIND_UNPACK, dt, *dp, w.unpack, mode, conj, d_bufs, d_items, wide,
-                   range_bytes(w.unpack, es, reads_a), stream);
-    if (st != COSTA_SUCCESS) return st;
+    for (const LaunchRange& lr : w.unpack) {
+      st = run_range(S, KIND_UNPACK, dt, *dp, lr, mode, conj, d_bufs, d_items, wide, range_bytes(lr, es, reads_a),
+                     stream);
+      if (st != COSTA_SUCCESS) return st;
+    }
   }
   if (ws->last_use) {
     HIP_OR_FAIL(hipEventRecord(ws->last_use, stream));
@@ -486,6 +490,7 @@ extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const co
   costa_status st = host_plan(dtype, n, desc, sigma, hp);
   if (st != COSTA_SUCCESS) return st;
   int64_t k = 0;
+  int32_t launch = 0;
   auto emit = [&](const LaunchRange& lr, costa_kernel_kind kind, int32_t wave) {
     for (int64_t i = 0; i < lr.npieces; ++i, ++k) {
       if (k >= capacity) continue;
@@ -515,13 +520,16 @@ extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const co
       o.ntasks = end - q.task0;
       o.tile_x = tile_x_of(q.tile);
       o.tile_y = tile_y_of(q.tile);
+      o.launch = launch;
+      o.reserved = 0;
 
     }
+    ++launch;
   };
-  emit(hp->direct, COSTA_KERNEL_DIRECT, 0);
+  for (const LaunchRange& lr : hp->direct) emit(lr, COSTA_KERNEL_DIRECT, 0);
   for (size_t w = 0; w < hp->waves.size(); ++w) {
     emit(hp->waves[w].pack, COSTA_KERNEL_PACK, (int32_t)w);
-    emit(hp->waves[w].unpack, COSTA_KERNEL_UNPACK, (int32_t)w);
+    for (const LaunchRange& lr : hp->waves[w].unpack) emit(lr, COSTA_KERNEL_UNPACK, (int32_t)w);
   }
   *count = k;
   return COSTA_SUCCESS;

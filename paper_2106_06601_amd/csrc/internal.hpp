@@ -136,8 +136,14 @@ constexpr int32_t wide_elems(int32_t es) { return es >= 16 ? 1 : 16 / es; }
 // Small rectangles are one tile; larger ones are cut into tiles of equal
 // width (at most tile_max_x) and equal height (as many rows as the budget
 // allows), so that every lane of a workgroup has an element.
-constexpr int32_t tile_budget(int32_t es) { return es >= 16 ? 4096 : es == 8 ? 2048 : 4096; }
-constexpr int32_t tile_max_x(int32_t es) { return es >= 16 ? 256 : 128; }
+#ifndef COSTA_TILE_BUDGET16
+#define COSTA_TILE_BUDGET16 3072  // three workgroups per CU (4096: two, -1 to -9%; 2048: four, shorter tiles)
+#endif
+#ifndef COSTA_TILE_MAXX16
+#define COSTA_TILE_MAXX16 256
+#endif
+constexpr int32_t tile_budget(int32_t es) { return es >= 16 ? COSTA_TILE_BUDGET16 : es == 8 ? 2048 : 4096; }
+constexpr int32_t tile_max_x(int32_t es) { return es >= 16 ? COSTA_TILE_MAXX16 : 128; }
 constexpr int32_t tile_lds_elems(int32_t es) { return tile_budget(es) + tile_max_x(es); }
 constexpr int32_t tile_pack(int32_t tx, int32_t ty) { return tx | ty << 16; }
 constexpr int32_t tile_x_of(int32_t t) { return t & 0xffff; }
@@ -182,8 +188,11 @@ struct LaunchRange {
   std::vector<int64_t> item_elems;  // elements of each pair in this launch
 };
 
+// A pack and its unpack-transform; the unpack is two launches when it holds
+// both row walks and LDS tiles (each launch of one kind, see plan.cpp).
 struct Wave {
-  LaunchRange pack, unpack;
+  LaunchRange pack;
+  std::vector<LaunchRange> unpack;
   int64_t msg_bytes = 0;
 };
 

@@ -357,6 +357,31 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
 #ifndef COSTA_PACK_BY_SOURCE
 #define COSTA_PACK_BY_SOURCE 1
 #endif
+// Split an unpack or direct launch that holds both row walks and LDS tiles
+// into one launch of each kind (tiles first), so that each can take the
+// per-XCD workgroup ranges (measured on MI355X: tall-skinny batch of 4
+// identity + 4 transposed pairs: unpack +8%, whole step +4%).
+#ifndef COSTA_SPLIT_KINDS
+#define COSTA_SPLIT_KINDS 1
+#endif
+
+// The launches of one kernel kind over `ps` (sorted): one, or a tile launch
+// and a row-walk launch.
+std::vector<LaunchRange> add_launches(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nitems) {
+  std::vector<LaunchRange> out;
+  if (ps.empty()) return out;
+  std::vector<Piece> tiles, walks;
+  if (COSTA_SPLIT_KINDS) {
+    for (const Piece& p : ps) ((p.flags & PIECE_TRANSPOSE) ? tiles : walks).push_back(p);
+  }
+  if (tiles.empty() || walks.empty()) {
+    out.push_back(add_launch(hp, ps, es, nitems));
+  } else {
+    out.push_back(add_launch(hp, tiles, es, nitems));
+    out.push_back(add_launch(hp, walks, es, nitems));
+  }
+  return out;
+}
 
 bool by_dst(const Piece& a, const Piece& b) {
   if (a.dst_buf != b.dst_buf) return a.dst_buf < b.dst_buf;
@@ -480,11 +505,11 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     Wave w;
     w.msg_bytes = off;
     w.pack = add_launch(hp, pack, es, n);
-    w.unpack = add_launch(hp, unpack, es, n);
+    w.unpack = add_launches(hp, unpack, es, n);
     hp.workspace_bytes = std::max(hp.workspace_bytes, off);
     hp.waves.push_back(w);
   }
-  hp.direct = add_launch(hp, direct, es, n);  // empty when merged above
+  hp.direct = add_launches(hp, direct, es, n);  // empty when merged above
   hp.plan_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
 }
 

@@ -24,7 +24,7 @@ struct PlanConfig {
 struct HostPlan {
   std::vector<Piece> pieces;    // every launch's rectangles, concatenated
   std::vector<int32_t> tasks;   // every launch's workgroups: index of the rectangle each starts with
-  LaunchRange direct;
+  std::vector<LaunchRange> direct;  // empty when the direct rectangles join the last unpack
   std::vector<Wave> waves;
   int64_t workspace_bytes = 0;  // max message bytes of a wave
   // per pair: elements on each path

@@ -25,7 +25,7 @@ PACK, UNPACK, DIRECT = 0, 1, 2
 # workgroup per 256 units (16-byte vectors when flag 2 is set, else
 # elements); a run of small row walks (each but the last flagged 16) by one
 # workgroup for all of them.
-BUDGET = {4: 4096, 8: 2048, 16: 4096}
+BUDGET = {4: 4096, 8: 2048, 16: 3072}
 MAXX = {4: 128, 8: 128, 16: 256}
 LANES, GROUP_UNITS, GROUP_PIECES = 256, 128, 8
 
@@ -36,7 +36,13 @@ def check_tasks(pieces, es):
     runs of small rectangles fit one workgroup."""
     launches = {}
     for i, p in enumerate(pieces):
-        launches.setdefault((int(p["kind"]), int(p["wave"])), []).append(p)
+        launches.setdefault((int(p["kind"]), int(p["launch"])), []).append(p)
+    order = [int(p["launch"]) for p in pieces]
+    assert order == sorted(order), "rectangles are exported in launch order"
+    for (kind, _), ps in launches.items():
+        assert len({int(p["wave"]) for p in ps}) == 1 and len({int(p["kind"]) for p in ps}) == 1
+        T = {bool(int(p["flags"]) & 1) for p in ps}
+        assert kind == PACK and T == {False} or len(T) == 1, "a launch holds tiles or row walks, not both"
     for ps in launches.values():
         nxt = 0
         run = None  # (units so far, rectangles so far, item, vector width) of an open run
