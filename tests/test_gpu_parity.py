@@ -187,6 +187,34 @@ def test_random_batched_full_compare():
         case.check_full()
 
 
+@pytest.mark.parametrize("dtype", ["f64", "c128", "f32", "c64"])
+def test_transposed_rectangles_around_the_tile_limits(dtype):
+    """Transposed rectangles whose width and height sit on both sides of every
+    LDS tile limit (one tile per rectangle, balanced tile columns, ragged edge
+    tiles): W x H rectangles on the direct path (one rank) and through
+    messages (two ranks that swap their blocks), with and without beta."""
+    widths = [1, 2, 15, 16, 17, 63, 64, 65, 127, 128, 129, 200, 255, 256, 257, 300, 513]
+    heights = [1, 3, 16, 17, 33, 129]
+    sc = CSCALARS if dtype in ("c128", "c64") else SCALARS
+    k = 0
+    for W in widths:
+        for H in heights:
+            op = "C" if dtype in ("c128", "c64") and k % 2 else "T"
+            alpha, beta = sc[k % len(sc)]
+            if k % 2:
+                A = GEN(W, H, [0, W], [0, H], [0], 1, "col")
+                B = GEN(H, W, [0, H], [0, W], [0], 1, "col")
+            else:
+                A = GEN(W, 2 * H, [0, W], [0, H, 2 * H], [0, 1], 2, "col")
+                B = GEN(2 * H, W, [0, H, 2 * H], [0, W], [1, 0], 2, "col")
+            _say(f"tile limits {dtype} W={W} H={H} op={op} alpha={alpha} beta={beta} ranks={A.nranks}")
+            w = synth.Workload(f"tiles{k}", dtype, [synth.Item(A, B, op, alpha, beta)], False, seed=300 + k)
+            case = Case(w)
+            case.run()
+            case.check_full()
+            k += 1
+
+
 # ---------------------------------------------------------------------------
 # edge cases
 # ---------------------------------------------------------------------------
