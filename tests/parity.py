@@ -188,3 +188,4 @@ class Case:
     def free(self):
         self.A = self.B = None
         torch.cuda.synchronize()
+        torch.cuda.empty_cache()  # hand the memory back, so later tests see it as free

@@ -117,6 +117,32 @@ def test_workload_rpa_full_size_sampled():
     case.free()
 
 
+def test_launches_beyond_one_slice():
+    """A launch of more than 2^23 workgroups runs in slices: two ranks swap the
+    halves of a 69632^2 fp64 matrix (38.8 GB, 4.85e9 elements, every element
+    remote: about 9.5 million workgroups per pack and unpack launch)."""
+    M = N = 69632
+    need = 3 * M * N * 8
+    torch.cuda.empty_cache()
+    free, total = torch.cuda.mem_get_info()
+    if free < need + (8 << 30):
+        pytest.skip(f"needs {need / 2**30:.0f} GiB; {free / 2**30:.0f} GiB free")
+    A = GEN(M, N, [0, M], [0, N // 2, N], [0, 1], 2, "col")
+    B = GEN(M, N, [0, M], [0, N // 2, N], [1, 0], 2, "col")
+    w = synth.Workload("slices", "f64", [synth.Item(A, B, "N", 1.0, 0.0)], False, seed=77)
+    descs = [dict(op="N", alpha=1.0, beta=0.0, A=C.layout_from_spec(A), B=C.layout_from_spec(B))]
+    x = C.costa_plan_export("f64", descs)
+    for kind in (0, 1):  # pack, unpack
+        sel = x[x["kind"] == kind]
+        assert int(sel["group"].max()) + 1 > 1 << 23
+    _say("transform 69632^2 swap, two launch slices")
+    case = Case(w, a_init="nan")
+    case.run()
+    assert case.check_sampled(n_random=100000, n_corners=100000) > 100000
+    case.check_all_written()
+    case.free()
+
+
 # ---------------------------------------------------------------------------
 # random layouts, every op / order / type / scalar combination
 # ---------------------------------------------------------------------------
