@@ -300,6 +300,10 @@ typedef struct {
   int32_t tile_x, tile_y; /* LDS tile of a transposed rectangle (0 otherwise) */
   int32_t launch;         /* index of its kernel launch in the plan's launch order */
   int32_t reserved;
+  int64_t wide_group;     /* launches of row walks only (else -1): its first task in the
+                             launch's wide task table (tasks of 512 units, which the
+                             launches that copy use) */
+  int64_t wide_ntasks;    /* tasks of the wide table that move it (0 if none) */
 } costa_piece_info;
 
 /* Writes the rectangles of the plan a transform with these arguments would

@@ -50,7 +50,8 @@ class CostaPieceInfo(ctypes.Structure):
     _fields_ = [("kind", _i32), ("wave", _i32), ("group", _i64), ("src_off", _i64), ("dst_off", _i64),
                 ("src_ld", _i64), ("dst_ld", _i64), ("src_buf", _i32), ("dst_buf", _i32), ("nx", _i32),
                 ("ny", _i32), ("item", _i32), ("flags", _i32), ("ntasks", _i64),
-                ("tile_x", _i32), ("tile_y", _i32), ("launch", _i32), ("reserved", _i32)]
+                ("tile_x", _i32), ("tile_y", _i32), ("launch", _i32), ("reserved", _i32),
+                ("wide_group", _i64), ("wide_ntasks", _i64)]
 
 
 class CostaGrid(ctypes.Structure):

@@ -43,6 +43,7 @@ struct DevicePlan {
   int device = -1;
   Piece* d_pieces = nullptr;
   int32_t* d_tasks = nullptr;
+  int32_t* d_wide = nullptr;
   // per-call table: buffer pointers then pair parameters
   void* d_table = nullptr;
   void* h_staging = nullptr;  // pinned
@@ -54,6 +55,7 @@ struct DevicePlan {
   ~DevicePlan() {
     if (d_pieces) (void)hipFree(d_pieces);
     if (d_tasks) (void)hipFree(d_tasks);
+    if (d_wide) (void)hipFree(d_wide);
     if (d_table) (void)hipFree(d_table);
     if (h_staging) (void)hipHostFree(h_staging);
     if (table_event) (void)hipEventDestroy(table_event);
@@ -241,8 +243,9 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePla
     HIP_OR_FAIL(hipEventRecord(e0, stream));
   }
   LaunchSpec spec{mode, conj, lr.has_transpose};
-  HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_tasks + lr.task_begin, lr.ntasks, d_bufs, d_items,
-                           allow_wide, lr.xcd_remap, stream));
+  HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_tasks + lr.task_begin, lr.ntasks,
+                           lr.nwide ? dp.d_wide + lr.wide_begin : nullptr, lr.nwide, d_bufs, d_items, allow_wide,
+                           lr.xcd_remap, stream));
   if (S.timing) {
     HIP_OR_FAIL(hipEventRecord(e1, stream));
     costa_kernel_kind kk = kind == KIND_PACK ? COSTA_KERNEL_PACK
@@ -325,6 +328,11 @@ costa_status get_plan(State& S, costa_dtype dt, const std::vector<ItemDesc>& ite
     HIP_OR_FAIL(hipMemcpy(dp->d_pieces, hp.pieces.data(), hp.pieces.size() * sizeof(Piece), hipMemcpyHostToDevice));
     HIP_OR_FAIL(hipMalloc(&dp->d_tasks, hp.tasks.size() * sizeof(int32_t)));
     HIP_OR_FAIL(hipMemcpy(dp->d_tasks, hp.tasks.data(), hp.tasks.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    if (!hp.wide_tasks.empty()) {
+      HIP_OR_FAIL(hipMalloc(&dp->d_wide, hp.wide_tasks.size() * sizeof(int32_t)));
+      HIP_OR_FAIL(hipMemcpy(dp->d_wide, hp.wide_tasks.data(), hp.wide_tasks.size() * sizeof(int32_t),
+                            hipMemcpyHostToDevice));
+    }
   }
   const int32_t P = items.empty() ? 0 : items[0].A->nranks;
   dp->nbufs = (size_t)2 * items.size() * P + 1;
@@ -518,8 +526,18 @@ extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const co
       o.item = q.item;
       o.flags = q.flags;
       o.ntasks = end - q.task0;
-      o.tile_x = tile_x_of(q.tile);
-      o.tile_y = tile_y_of(q.tile);
+      const bool T = q.flags & PIECE_TRANSPOSE;
+      o.tile_x = T ? tile_x_of(q.aux) : 0;
+      o.tile_y = T ? tile_y_of(q.aux) : 0;
+      // its first task and task count in the wide table (launches without tiles)
+      o.wide_group = lr.nwide ? q.aux : -1;
+      int64_t wend = lr.nwide;
+      for (int64_t j = i + 1; lr.nwide && j < lr.npieces; ++j)
+        if (hp->pieces[lr.piece_begin + j].aux != q.aux) {
+          wend = hp->pieces[lr.piece_begin + j].aux;
+          break;
+        }
+      o.wide_ntasks = lr.nwide ? wend - q.aux : 0;
       o.launch = launch;
       o.reserved = 0;
 

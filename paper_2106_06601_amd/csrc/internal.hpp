@@ -99,7 +99,7 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 //   workgroup (a run of small rectangles shares one workgroup).
 // A transposed rectangle is moved in LDS tiles of tile_x x tile_y elements
 // (tile_x along the destination's contiguous direction; choose_tile below),
-// packed into `tile` with tile_pack.
+// packed into `aux` with tile_pack.
 enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_GROUP_NEXT = 16 };
 
 struct alignas(16) Piece {
@@ -114,15 +114,19 @@ struct alignas(16) Piece {
   int32_t item;     // pair of a batched call (selects alpha, beta, mode)
   int32_t flags;
   int32_t task0;    // first workgroup of its launch that moves it
-  int32_t tile;     // transposed rectangles: tile_pack(tile_x, tile_y)
+  int32_t aux;      // transposed rectangles: tile_pack(tile_x, tile_y); row walks in a
+                    // launch without tiles: its first task in the launch's wide task table
 };
 static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
 
 // Work of one workgroup (kThreadsPerTask lanes): one LDS tile of a
 // transposed rectangle, kThreadsPerTask units (16-byte vectors, or single
-// elements when the rectangle is not PIECE_WIDE) of a rectangle walked
-// along its rows, or a run of small rectangles moved at once.
+// elements when the rectangle is not PIECE_WIDE) of a rectangle walked along
+// its rows, or a run of small rectangles moved at once.  A launch of row
+// walks also has a wide task table whose tasks are kWideTaskUnits units (a
+// run still one task); launches that copy use it, two units per lane.
 constexpr int32_t kThreadsPerTask = 256;
+constexpr int32_t kWideTaskUnits = 2 * kThreadsPerTask;
 constexpr int32_t kGroupUnitsMax = 128;  // rectangles of at most this many units may share a workgroup
 constexpr int32_t kGroupPiecesMax = 8;
 
@@ -176,12 +180,13 @@ static_assert(sizeof(ItemParam) == 48, "ItemParam must be 48 bytes");
 
 // One kernel launch of a plan: a range of rectangles and the workgroups
 // (tasks) that move them.  tasks[task_begin + b] = index into Plan::pieces of
-// the rectangle workgroup b starts with; that rectangle's task0 is the first
-// workgroup that moves it, so workgroup b takes its (b - task0)-th tile or
-// chunk.
+// the rectangle task b starts with; that rectangle's task0 is the first task
+// that moves it, so task b takes its (b - task0)-th tile or chunk.  The wide
+// table works the same way with the rectangle's aux in place of task0.
 struct LaunchRange {
   int64_t piece_begin = 0, npieces = 0;
   int64_t task_begin = 0, ntasks = 0;
+  int64_t wide_begin = 0, nwide = 0;  // wide task table (launches without tiles; 0 tasks otherwise)
   int64_t elems = 0;
   bool has_transpose = false;
   int32_t xcd_remap = 0;  // workgroup order: 0 dispatch order, -1 one range per XCD, K > 0 runs of K per XCD
@@ -207,14 +212,15 @@ struct LaunchSpec {
   bool has_transpose;
 };
 // pieces: the plan's rectangles (global indices); tasks: the launch's
-// ntasks entries.
+// ntasks entries, wide: its wide task table (nwide entries, 0 in launches
+// with tiles).
 // xcd_remap (workgroups are dispatched round-robin over the 8 XCDs): 0 runs
 // task b in workgroup b; -1 hands each XCD one contiguous range of the
 // launch slice; K > 0 hands each XCD runs of K consecutive tasks, the XCDs
 // advancing through the launch side by side.
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
-                        const int32_t* tasks, int64_t ntasks, void* const* bufs, const ItemParam* items,
-                        int32_t allow_wide, int32_t xcd_remap, hipStream_t stream);
+                        const int32_t* tasks, int64_t ntasks, const int32_t* wide, int64_t nwide, void* const* bufs,
+                        const ItemParam* items, int32_t allow_wide, int32_t xcd_remap, hipStream_t stream);
 
 struct VolumeArgs {
   const Interval* rows;

@@ -3,11 +3,13 @@
 //
 // All of them are bound by HBM bandwidth: per element they read at most two
 // values and write one, with at most a few flops (Section 5 eq:costa).  The
-// design goals are therefore coalesced 64-lane accesses, 16-byte vectors
-// where the rectangle allows them, many independent loads in flight per lane,
-// an LDS tile for the rectangles whose source and destination run in
-// different directions, and a workgroup order that keeps neighbouring work on
-// one XCD (one L2).
+// movers are therefore built from one-shot workgroups: each takes one task
+// from the plan's task table -- 256 or 512 consecutive 16-byte units (or
+// elements) of a rectangle walked along its rows, or one LDS tile of a
+// rectangle whose source and destination run in different directions --
+// moves it with coalesced 64-lane accesses and exits, so the workgroups in
+// flight sweep the buffers in task order.  A launch whose tasks are all
+// alike may hand each XCD (one L2) a contiguous range of them.
 #include <hip/hip_runtime.h>
 
 #include "internal.hpp"
@@ -34,6 +36,9 @@ namespace {
 #endif
 #ifndef COSTA_NT_ALOADS
 #define COSTA_NT_ALOADS 0
+#endif
+#ifndef COSTA_COPY_UNITS
+#define COSTA_COPY_UNITS 2  // units per lane in launches of row walks that copy (1: no wide table use)
 #endif
 
 constexpr int kThreads = kThreadsPerTask;
@@ -174,13 +179,14 @@ __device__ __forceinline__ void divmod(int32_t u, int32_t n, int32_t& y, int32_t
   }
 }
 
-// Row walk: dst[y*dst_ld + x] = f(src[y*src_ld + x]).  Workgroup chunk c
-// covers units [c*kThreads, (c+1)*kThreads) of the rectangle's flattened
-// (y, x) index, one unit per lane (a 16-byte vector for PIECE_WIDE
-// rectangles, else one element).  A run of small rectangles
-// (PIECE_GROUP_NEXT) is flattened the same way: lane l takes unit l of the
-// run.  Each lane makes one load (two when A is read) and one store.
-template <typename S, bool CPLX, int MODE, bool CONJ>
+// Row walk: dst[y*dst_ld + x] = f(src[y*src_ld + x]).  Task c of the
+// rectangle covers units [c*UL*kThreads, (c+1)*UL*kThreads) of its
+// flattened (y, x) index (a unit is a 16-byte vector for PIECE_WIDE
+// rectangles, else one element); lane l takes units l + k*kThreads, k < UL.
+// A run of small rectangles (PIECE_GROUP_NEXT) is flattened the same way:
+// lane l takes unit l of the run.  A lane issues all its loads (and those of
+// A when it is read) before its stores.
+template <typename S, bool CPLX, int MODE, bool CONJ, int UL>
 __device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int32_t pi, int32_t c,
                                           void* const* __restrict__ bufs, int32_t allow_wide, S ar, S ai, S br,
                                           S bi) {
@@ -189,51 +195,74 @@ __device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int3
   constexpr int W = TT::WIDE_NEL;
   const bool wide = (pieces[pi].flags & PIECE_WIDE) != 0;  // the same over a run
   const int32_t epu = wide ? W : 1;                         // elements per unit
-  int32_t u = c * kThreads + (int32_t)threadIdx.x;
-  int64_t soff = -1, doff = 0;
-  int32_t sbuf = 0, dbuf = 0;
-  while (true) {
-    const Piece& p = pieces[pi];
-    const int32_t nxu = wide ? p.nx / W : p.nx;
-    const int32_t units = nxu * p.ny;
-    if (u >= 0 && u < units) {
-      int32_t y, x;
-      divmod(u, nxu, y, x);
-      soff = p.src_off + (int64_t)y * p.src_ld + (int64_t)x * epu;
-      doff = p.dst_off + (int64_t)y * p.dst_ld + (int64_t)x * epu;
-      sbuf = p.src_buf;
-      dbuf = p.dst_buf;
+  const S* __restrict__ srcs[UL];
+  S* __restrict__ dsts[UL];
+  int64_t soffs[UL], doffs[UL];
+#pragma unroll
+  for (int k = 0; k < UL; ++k) {
+    int32_t u = c * (UL * kThreads) + k * kThreads + (int32_t)threadIdx.x;
+    int64_t soff = -1, doff = 0;
+    int32_t sbuf = 0, dbuf = 0;
+    int32_t q = pi;
+    while (true) {
+      const Piece& p = pieces[q];
+      const int32_t nxu = wide ? p.nx / W : p.nx;
+      const int32_t units = nxu * p.ny;
+      if (u >= 0 && u < units) {
+        int32_t y, x;
+        divmod(u, nxu, y, x);
+        soff = p.src_off + (int64_t)y * p.src_ld + (int64_t)x * epu;
+        doff = p.dst_off + (int64_t)y * p.dst_ld + (int64_t)x * epu;
+        sbuf = p.src_buf;
+        dbuf = p.dst_buf;
+      }
+      u -= units;
+      if (!(p.flags & PIECE_GROUP_NEXT)) break;
+      ++q;
     }
-    u -= units;
-    if (!(p.flags & PIECE_GROUP_NEXT)) break;
-    ++pi;
+    soffs[k] = soff;
+    doffs[k] = doff;
+    srcs[k] = reinterpret_cast<const S*>(bufs[sbuf]);
+    dsts[k] = reinterpret_cast<S*>(bufs[dbuf]);
   }
-  if (soff < 0) return;
-  const S* __restrict__ src = reinterpret_cast<const S*>(bufs[sbuf]);
-  S* __restrict__ dst = reinterpret_cast<S*>(bufs[dbuf]);
   if (W > 1 && wide && allow_wide) {
     using U = Vec<S, TT::NS * W>;
-    const U* su = reinterpret_cast<const U*>(src + soff * TT::NS);
-    U* du = reinterpret_cast<U*>(dst + doff * TT::NS);
-    const U bv = load<TT::NT_WALK>(su);
-    U av;
-    if constexpr (MODE == MODE_AXPBY) av = load<COSTA_NT_ALOADS>(du);
-    store(du, combine<S, TT::NS * W, CPLX, MODE, CONJ>(bv, av, ar, ai, br, bi));
+    U bv[UL], av[UL];
+#pragma unroll
+    for (int k = 0; k < UL; ++k)
+      if (soffs[k] >= 0) {
+        bv[k] = load<TT::NT_WALK>(reinterpret_cast<const U*>(srcs[k] + soffs[k] * TT::NS));
+        if constexpr (MODE == MODE_AXPBY) av[k] = load<COSTA_NT_ALOADS>(reinterpret_cast<U*>(dsts[k] + doffs[k] * TT::NS));
+      }
+#pragma unroll
+    for (int k = 0; k < UL; ++k)
+      if (soffs[k] >= 0)
+        store(reinterpret_cast<U*>(dsts[k] + doffs[k] * TT::NS),
+              combine<S, TT::NS * W, CPLX, MODE, CONJ>(bv[k], av[k], ar, ai, br, bi));
   } else {
     // one element at a time (epu of them: a PIECE_WIDE rectangle in a call
     // whose buffers are not 16-byte aligned)
-    const E* se = reinterpret_cast<const E*>(src) + soff;
-    E* de = reinterpret_cast<E*>(dst) + doff;
-    E bv[W], av[W];
+    E bv[UL][W], av[UL][W];
 #pragma unroll
-    for (int k = 0; k < W; ++k)
-      if (k < epu) {
-        bv[k] = load<TT::NT_WALK>(se + k);
-        if constexpr (MODE == MODE_AXPBY) av[k] = load<COSTA_NT_ALOADS>(de + k);
+    for (int k = 0; k < UL; ++k)
+      if (soffs[k] >= 0) {
+        const E* se = reinterpret_cast<const E*>(srcs[k]) + soffs[k];
+        E* de = reinterpret_cast<E*>(dsts[k]) + doffs[k];
+#pragma unroll
+        for (int j = 0; j < W; ++j)
+          if (j < epu) {
+            bv[k][j] = load<TT::NT_WALK>(se + j);
+            if constexpr (MODE == MODE_AXPBY) av[k][j] = load<COSTA_NT_ALOADS>(de + j);
+          }
       }
 #pragma unroll
-    for (int k = 0; k < W; ++k)
-      if (k < epu) store(de + k, combine<S, TT::NS, CPLX, MODE, CONJ>(bv[k], av[k], ar, ai, br, bi));
+    for (int k = 0; k < UL; ++k)
+      if (soffs[k] >= 0) {
+        E* de = reinterpret_cast<E*>(dsts[k]) + doffs[k];
+#pragma unroll
+        for (int j = 0; j < W; ++j)
+          if (j < epu) store(de + j, combine<S, TT::NS, CPLX, MODE, CONJ>(bv[k][j], av[k][j], ar, ai, br, bi));
+      }
   }
 }
 
@@ -257,7 +286,7 @@ __device__ __forceinline__ void move_tile(const Piece* __restrict__ pieces, int3
   constexpr int NP = TT::TILE_PASSES;
   const Piece& p = pieces[pi];
   const int32_t tid = threadIdx.x;
-  const int32_t tx = tile_x_of(p.tile), ty = tile_y_of(p.tile);
+  const int32_t tx = tile_x_of(p.aux), ty = tile_y_of(p.aux);
   const int32_t stride = ty | 1;
   const int32_t ntx = (p.nx + tx - 1) / tx;
   const int32_t x0 = (c % ntx) * tx, y0 = (c / ntx) * ty;
@@ -311,7 +340,7 @@ __device__ __forceinline__ void move_tile(const Piece* __restrict__ pieces, int3
 }
 
 // The work of one workgroup for a fixed arithmetic mode.
-template <typename S, bool CPLX, int MODE, bool CONJ, bool HAS_T>
+template <typename S, bool CPLX, int MODE, bool CONJ, bool HAS_T, int UL>
 __device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int32_t pi, int32_t flags, int32_t c,
                                           void* const* __restrict__ bufs, const ItemParam* __restrict__ ip,
                                           int32_t allow_wide, Vec<S, CPLX ? 2 : 1>* lds) {
@@ -328,7 +357,7 @@ __device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int3
       return;
     }
   }
-  move_walk<S, CPLX, MODE, CONJ>(pieces, pi, c, bufs, allow_wide, ar, ai, br, bi);
+  move_walk<S, CPLX, MODE, CONJ, UL>(pieces, pi, c, bufs, allow_wide, ar, ai, br, bi);
 }
 
 constexpr int MODE_ANY = 3;
@@ -340,7 +369,9 @@ constexpr int MODE_ANY = 3;
 //         per workgroup (batches that mix modes; a workgroup's rectangles
 //         belong to one pair); CONJ likewise.
 //   HAS_T: whether the launch contains transposed rectangles (LDS tiles).
-template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
+// UL = 2: the launch runs on its wide task table (task0 of a rectangle in
+// aux), two units per lane.
+template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T, int UL>
 __device__ __forceinline__ void mover_body(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks,
                                            int32_t task_off, void* const* __restrict__ bufs,
                                            const ItemParam* __restrict__ items, int32_t allow_wide,
@@ -350,27 +381,29 @@ __device__ __forceinline__ void mover_body(const Piece* __restrict__ pieces, con
   __shared__ E lds[HAS_T ? TT::LDS_ELEMS : 1];
   const int32_t b = task_off + xcd_order((int32_t)blockIdx.x, (int32_t)gridDim.x, remap);
   const int32_t pi = tasks[b];
-  const int32_t c = b - pieces[pi].task0;
+  const int32_t c = b - (UL == 1 ? pieces[pi].task0 : pieces[pi].aux);
   if constexpr (KIND == KIND_PACK) {
-    move_walk<S, CPLX, MODE_COPY, false>(pieces, pi, c, bufs, allow_wide, S(0), S(0), S(0), S(0));
+    move_walk<S, CPLX, MODE_COPY, false, UL>(pieces, pi, c, bufs, allow_wide, S(0), S(0), S(0), S(0));
   } else {
     const int32_t flags = pieces[pi].flags;
     const ItemParam* ip = items + pieces[pi].item;
     if constexpr (MODE != MODE_ANY) {
-      move_task<S, CPLX, MODE, CONJ, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+      move_task<S, CPLX, MODE, CONJ, HAS_T, UL>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
     } else {
       const bool conj = CPLX && ip->conj;
       const int32_t mode = ip->mode;
+#define COSTA_TASK(M, CJ) move_task<S, CPLX, M, CJ, HAS_T, UL>(pieces, pi, flags, c, bufs, ip, allow_wide, lds)
       if (mode == MODE_COPY) {
-        if (conj) move_task<S, CPLX, MODE_COPY, CPLX, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
-        else move_task<S, CPLX, MODE_COPY, false, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+        if (conj) COSTA_TASK(MODE_COPY, CPLX);
+        else COSTA_TASK(MODE_COPY, false);
       } else if (mode == MODE_SCALE) {
-        if (conj) move_task<S, CPLX, MODE_SCALE, CPLX, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
-        else move_task<S, CPLX, MODE_SCALE, false, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+        if (conj) COSTA_TASK(MODE_SCALE, CPLX);
+        else COSTA_TASK(MODE_SCALE, false);
       } else {
-        if (conj) move_task<S, CPLX, MODE_AXPBY, CPLX, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
-        else move_task<S, CPLX, MODE_AXPBY, false, HAS_T>(pieces, pi, flags, c, bufs, ip, allow_wide, lds);
+        if (conj) COSTA_TASK(MODE_AXPBY, CPLX);
+        else COSTA_TASK(MODE_AXPBY, false);
       }
+#undef COSTA_TASK
     }
   }
 }
@@ -383,20 +416,30 @@ constexpr bool big_lds() {
   return HAS_T && TypeTraits<S, CPLX>::LDS_ELEMS * TypeTraits<S, CPLX>::ES > 40 * 1024;
 }
 
+// Units per lane of a launch: two (the wide task table) in launches of row
+// walks that copy -- the pack, and unpack/direct launches with alpha = 1,
+// beta = 0 -- one otherwise.  Measured on MI355X: two units per lane +2 to
+// +11% on copies; on an axpby walk of short misaligned rows -19%.
+template <int KIND, int MODE, bool HAS_T>
+constexpr int units_per_lane() {
+  return !HAS_T && (KIND == KIND_PACK || MODE == MODE_COPY) ? COSTA_COPY_UNITS : 1;
+}
+
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
 costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
             void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
             int32_t remap) {
-  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide, remap);
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, units_per_lane<KIND, MODE, HAS_T>()>(pieces, tasks, task_off, bufs,
+                                                                                   items, allow_wide, remap);
 }
 
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 costa_mover_lds(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
                 void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
-            int32_t remap) {
-  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T>(pieces, tasks, task_off, bufs, items, allow_wide, remap);
+                int32_t remap) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, 1>(pieces, tasks, task_off, bufs, items, allow_wide, remap);
 }
 
 // Volume of the grid overlay: every overlay block (k, l) adds its element
@@ -429,11 +472,12 @@ __global__ void __launch_bounds__(kThreads) costa_volume(VolumeArgs a, int32_t u
 }
 
 struct Launch {
-  dim3 grid, block;
   hipStream_t stream;
   const Piece* pieces;
-  const int32_t* tasks;
-  int32_t task_off;
+  const int32_t* tasks;  // the launch's task table
+  int64_t ntasks;
+  const int32_t* wide;   // its wide task table (launches of row walks)
+  int64_t nwide;
   void* const* bufs;
   const ItemParam* items;
   int32_t allow_wide;
@@ -472,15 +516,27 @@ __global__ void __launch_bounds__(kThreads) costa_volume_outer(SeparableArgs a) 
   }
 }
 
+// One workgroup per task of the table the launch runs on, in slices that
+// keep the grid below 2^32 work-items.
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 hipError_t go(const Launch& l) {
-  if constexpr (big_lds<S, CPLX, HAS_T>())
-    hipLaunchKernelGGL((costa_mover_lds<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
-                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide, l.remap);
-  else
-    hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), l.grid, l.block, 0, l.stream, l.pieces,
-                       l.tasks, l.task_off, l.bufs, l.items, l.allow_wide, l.remap);
-  return hipGetLastError();
+  constexpr bool WIDE = units_per_lane<KIND, MODE, HAS_T>() > 1;
+  const int32_t* tasks = WIDE ? l.wide : l.tasks;
+  const int64_t ntasks = WIDE ? l.nwide : l.ntasks;
+  if (ntasks > INT32_MAX) return hipErrorInvalidValue;
+  constexpr int64_t kSlice = (int64_t)1 << 23;
+  for (int64_t off = 0; off < ntasks; off += kSlice) {
+    const unsigned n = (unsigned)(ntasks - off < kSlice ? ntasks - off : kSlice);
+    if constexpr (big_lds<S, CPLX, HAS_T>())
+      hipLaunchKernelGGL((costa_mover_lds<S, CPLX, KIND, MODE, CONJ, HAS_T>), dim3(n), dim3(kThreads), 0, l.stream,
+                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.remap);
+    else
+      hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), dim3(n), dim3(kThreads), 0, l.stream,
+                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.remap);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 template <typename S, bool CPLX, int KIND, bool HAS_T>
@@ -513,26 +569,18 @@ hipError_t launch_typed(MoverKind kind, const LaunchSpec& spec, const Launch& l)
 }  // namespace
 
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
-                        const int32_t* tasks, int64_t ntasks, void* const* bufs, const ItemParam* items,
-                        int32_t allow_wide, int32_t xcd_remap, hipStream_t stream) {
+                        const int32_t* tasks, int64_t ntasks, const int32_t* wide, int64_t nwide, void* const* bufs,
+                        const ItemParam* items, int32_t allow_wide, int32_t xcd_remap, hipStream_t stream) {
   if (ntasks <= 0) return hipSuccess;
-  if (ntasks > INT32_MAX) return hipErrorInvalidValue;
-  // one workgroup per task, in slices that keep the grid below 2^32 work-items
-  constexpr int64_t kSlice = 1 << 23;
-  for (int64_t off = 0; off < ntasks; off += kSlice) {
-    const int64_t n = ntasks - off < kSlice ? ntasks - off : kSlice;
-    Launch l{dim3((unsigned)n), dim3(kThreads), stream, pieces, tasks, (int32_t)off, bufs, items, allow_wide,
-             xcd_remap};
-    hipError_t e = hipErrorInvalidValue;
-    switch (dtype) {
-      case COSTA_R64: e = launch_typed<double, false>(kind, spec, l); break;
-      case COSTA_C128: e = launch_typed<double, true>(kind, spec, l); break;
-      case COSTA_R32: e = launch_typed<float, false>(kind, spec, l); break;
-      case COSTA_C64: e = launch_typed<float, true>(kind, spec, l); break;
-    }
-    if (e != hipSuccess) return e;
+  if (!spec.has_transpose && nwide <= 0) return hipErrorInvalidValue;  // a launch of row walks has both tables
+  Launch l{stream, pieces, tasks, ntasks, wide, nwide, bufs, items, allow_wide, xcd_remap};
+  switch (dtype) {
+    case COSTA_R64: return launch_typed<double, false>(kind, spec, l);
+    case COSTA_C128: return launch_typed<double, true>(kind, spec, l);
+    case COSTA_R32: return launch_typed<float, false>(kind, spec, l);
+    case COSTA_C64: return launch_typed<float, true>(kind, spec, l);
   }
-  return hipSuccess;
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_volume_separable(const SeparableArgs& a, hipStream_t stream) {

@@ -128,7 +128,7 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
       p.src_buf = nitems * P + item * P + s;
       p.item = item;
       p.task0 = 0;
-      p.tile = 0;
+      p.aux = 0;
       c.kx0 = kx;
       c.kx1 = kx + 1;
       c.ly_end = ly + 1;
@@ -237,11 +237,11 @@ void split_pieces(std::vector<Cand>& v, int64_t max_elems) {
 void finish_piece(Piece& p, int elem_size) {
   p.flags &= ~(PIECE_WIDE | PIECE_GROUP_NEXT);
   p.task0 = 0;
-  p.tile = 0;
+  p.aux = 0;
   if (p.flags & PIECE_TRANSPOSE) {
     int32_t tx, ty;
     choose_tile(elem_size, p.nx, p.ny, tx, ty);
-    p.tile = tile_pack(tx, ty);
+    p.aux = tile_pack(tx, ty);
     return;
   }
   const int64_t want = wide_elems(elem_size);
@@ -306,7 +306,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     if (p.flags & PIECE_TRANSPOSE) {
       lr.has_transpose = true;
       g_task = -1;
-      const int32_t tx = tile_x_of(p.tile), ty = tile_y_of(p.tile);
+      const int32_t tx = tile_x_of(p.aux), ty = tile_y_of(p.aux);
       const int64_t n = (int64_t)((p.nx + tx - 1) / tx) * ((p.ny + ty - 1) / ty);
       p.task0 = (int32_t)b;
       hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
@@ -341,6 +341,26 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   }
   if (b > INT32_MAX) throw std::bad_alloc();
   lr.ntasks = b;
+  // the wide task table of a launch of row walks: kWideTaskUnits units per
+  // task, a run of small rectangles still one task
+  lr.wide_begin = (int64_t)hp.wide_tasks.size();
+  if (!lr.has_transpose) {
+    int64_t b2 = 0;
+    for (size_t k = 0; k < ps.size(); ++k) {
+      Piece& p = ps[k];
+      if (k > 0 && (ps[k - 1].flags & PIECE_GROUP_NEXT)) {
+        p.aux = ps[k - 1].aux;
+        continue;
+      }
+      const int64_t ne = (int64_t)p.nx * p.ny;
+      const int64_t units = (p.flags & PIECE_WIDE) ? ne / wide_elems(es) : ne;
+      const int64_t n = (p.flags & PIECE_GROUP_NEXT) ? 1 : (units + kWideTaskUnits - 1) / kWideTaskUnits;
+      p.aux = (int32_t)b2;
+      hp.wide_tasks.insert(hp.wide_tasks.end(), (size_t)n, base + (int32_t)k);
+      b2 += n;
+    }
+    lr.nwide = b2;
+  }
   int64_t aligned = 0, transposed = 0;
   for (const Piece& p : ps) {
     if (line_aligned(p, es)) aligned += (int64_t)p.nx * p.ny;

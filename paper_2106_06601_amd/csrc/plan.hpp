@@ -24,6 +24,7 @@ struct PlanConfig {
 struct HostPlan {
   std::vector<Piece> pieces;    // every launch's rectangles, concatenated
   std::vector<int32_t> tasks;   // every launch's workgroups: index of the rectangle each starts with
+  std::vector<int32_t> wide_tasks;  // the wide task tables of the launches without tiles
   std::vector<LaunchRange> direct;  // empty when the direct rectangles join the last unpack
   std::vector<Wave> waves;
   int64_t workspace_bytes = 0;  // max message bytes of a wave

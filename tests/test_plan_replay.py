@@ -77,6 +77,24 @@ def check_tasks(pieces, es):
             assert int(p["ntasks"]) == need, f"{p} needs {need} workgroups"
             nxt += need
         assert run is None, "a run of small rectangles ends with the launch's last rectangle flagged"
+        # the wide task table of a launch of row walks: tasks of 2 * LANES
+        # units, a run of small rectangles one task; none in launches with tiles
+        if any(int(p["flags"]) & 1 for p in ps):
+            assert all(int(p["wide_group"]) == -1 and int(p["wide_ntasks"]) == 0 for p in ps)
+            continue
+        nxt, in_run = 0, False
+        for p in ps:
+            nx, ny, fl = int(p["nx"]), int(p["ny"]), int(p["flags"])
+            if in_run:
+                assert int(p["wide_group"]) == nxt - 1 and int(p["wide_ntasks"]) == 1
+                in_run = bool(fl & 16)
+                continue
+            assert int(p["wide_group"]) == nxt, "wide tasks of a launch are not handed out in order"
+            units = nx * ny // (16 // es if fl & 2 and es < 16 else 1)
+            need = 1 if fl & 16 else -(-units // (2 * LANES))
+            assert int(p["wide_ntasks"]) == need
+            in_run = bool(fl & 16)
+            nxt += need
 
 
 def _descs(w):
