@@ -126,7 +126,10 @@ static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
 // walks also has a wide task table whose tasks are kWideTaskUnits units (a
 // run still one task); launches that copy use it, two units per lane.
 constexpr int32_t kThreadsPerTask = 256;
-constexpr int32_t kWideTaskUnits = 2 * kThreadsPerTask;
+#ifndef COSTA_COPY_UNITS
+#define COSTA_COPY_UNITS 2  // units per lane in launches of row walks that copy
+#endif
+constexpr int32_t kWideTaskUnits = (COSTA_COPY_UNITS > 1 ? COSTA_COPY_UNITS : 2) * kThreadsPerTask;
 constexpr int32_t kGroupUnitsMax = 128;  // rectangles of at most this many units may share a workgroup
 constexpr int32_t kGroupPiecesMax = 8;
 

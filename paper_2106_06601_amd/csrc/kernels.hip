@@ -37,9 +37,6 @@ namespace {
 #ifndef COSTA_NT_ALOADS
 #define COSTA_NT_ALOADS 0
 #endif
-#ifndef COSTA_COPY_UNITS
-#define COSTA_COPY_UNITS 2  // units per lane in launches of row walks that copy (1: no wide table use)
-#endif
 
 constexpr int kThreads = kThreadsPerTask;
 

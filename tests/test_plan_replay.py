@@ -27,7 +27,7 @@ PACK, UNPACK, DIRECT = 0, 1, 2
 # workgroup for all of them.
 BUDGET = {4: 4096, 8: 2048, 16: 3072}
 MAXX = {4: 128, 8: 128, 16: 256}
-LANES, GROUP_UNITS, GROUP_PIECES = 256, 128, 8
+LANES, GROUP_UNITS, GROUP_PIECES, WIDE_UNITS = 256, 128, 8, 512
 
 
 def check_tasks(pieces, es):
@@ -77,7 +77,7 @@ def check_tasks(pieces, es):
             assert int(p["ntasks"]) == need, f"{p} needs {need} workgroups"
             nxt += need
         assert run is None, "a run of small rectangles ends with the launch's last rectangle flagged"
-        # the wide task table of a launch of row walks: tasks of 2 * LANES
+        # the wide task table of a launch of row walks: tasks of WIDE_UNITS
         # units, a run of small rectangles one task; none in launches with tiles
         if any(int(p["flags"]) & 1 for p in ps):
             assert all(int(p["wide_group"]) == -1 and int(p["wide_ntasks"]) == 0 for p in ps)
@@ -91,7 +91,7 @@ def check_tasks(pieces, es):
                 continue
             assert int(p["wide_group"]) == nxt, "wide tasks of a launch are not handed out in order"
             units = nx * ny // (16 // es if fl & 2 and es < 16 else 1)
-            need = 1 if fl & 16 else -(-units // (2 * LANES))
+            need = 1 if fl & 16 else -(-units // WIDE_UNITS)
             assert int(p["wide_ntasks"]) == need
             in_run = bool(fl & 16)
             nxt += need
