@@ -245,7 +245,7 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePla
   LaunchSpec spec{mode, conj, lr.has_transpose};
   HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_tasks + lr.task_begin, lr.ntasks,
                            lr.nwide ? dp.d_wide + lr.wide_begin : nullptr, lr.nwide, d_bufs, d_items, allow_wide,
-                           lr.xcd_remap, stream));
+                           lr.xcd_ranges, stream));
   if (S.timing) {
     HIP_OR_FAIL(hipEventRecord(e1, stream));
     costa_kernel_kind kk = kind == KIND_PACK ? COSTA_KERNEL_PACK

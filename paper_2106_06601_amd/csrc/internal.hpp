@@ -192,7 +192,7 @@ struct LaunchRange {
   int64_t wide_begin = 0, nwide = 0;  // wide task table (launches without tiles; 0 tasks otherwise)
   int64_t elems = 0;
   bool has_transpose = false;
-  int32_t xcd_remap = 0;  // workgroup order: 0 dispatch order, -1 one range per XCD, K > 0 runs of K per XCD
+  int32_t xcd_ranges = 0;  // 1: each XCD takes one contiguous range of the launch's tasks
   std::vector<int64_t> item_elems;  // elements of each pair in this launch
 };
 
@@ -217,13 +217,12 @@ struct LaunchSpec {
 // pieces: the plan's rectangles (global indices); tasks: the launch's
 // ntasks entries, wide: its wide task table (nwide entries, 0 in launches
 // with tiles).
-// xcd_remap (workgroups are dispatched round-robin over the 8 XCDs): 0 runs
-// task b in workgroup b; -1 hands each XCD one contiguous range of the
-// launch slice; K > 0 hands each XCD runs of K consecutive tasks, the XCDs
-// advancing through the launch side by side.
+// xcd_ranges: 0 runs task b in workgroup b (workgroups are dispatched
+// round-robin over the 8 XCDs); 1 hands each XCD one contiguous range of the
+// tasks of each launch slice.
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
                         const int32_t* tasks, int64_t ntasks, const int32_t* wide, int64_t nwide, void* const* bufs,
-                        const ItemParam* items, int32_t allow_wide, int32_t xcd_remap, hipStream_t stream);
+                        const ItemParam* items, int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream);
 
 struct VolumeArgs {
   const Interval* rows;

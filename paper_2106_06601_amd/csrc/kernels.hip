@@ -40,24 +40,17 @@ namespace {
 
 constexpr int kThreads = kThreadsPerTask;
 
-// The task of workgroup b of n (workgroups are dispatched round-robin over
-// the 8 XCDs, b % 8 being b's XCD).  remap 0: task b.  remap -1: the b/8-th
-// task of a contiguous range per XCD.  remap K > 0: each block of 8K
-// workgroups takes a block of 8K tasks, XCD x its K consecutive tasks from
-// x*K (the tail that fills no block keeps dispatch order).
-__device__ __forceinline__ int32_t xcd_order(int32_t b, int32_t n, int32_t remap) {
+// The task of workgroup b of n.  Workgroups are dispatched round-robin over
+// the 8 XCDs (b % 8 is b's XCD).  ranges 0: task b.  ranges 1: XCD x takes
+// the x-th of 8 contiguous ranges of tasks, workgroup b the (b/8)-th task of
+// its XCD's range.
+__device__ __forceinline__ int32_t xcd_order(int32_t b, int32_t n, int32_t ranges) {
   constexpr int32_t X = 8;
-  if (remap == 0) return b;
-  if (remap < 0) {
-    const int32_t q = n / X, r = n % X;
-    const int32_t xcd = b % X, idx = b / X;
-    const int32_t start = xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q;
-    return start + idx;
-  }
-  const int32_t blk = X * remap;
-  if (b >= n - n % blk) return b;
-  const int32_t j = b % blk;
-  return b - j + (j % X) * remap + j / X;
+  if (!ranges) return b;
+  const int32_t q = n / X, r = n % X;
+  const int32_t xcd = b % X, idx = b / X;
+  const int32_t start = xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q;
+  return start + idx;
 }
 
 template <typename S, int N>
@@ -359,24 +352,25 @@ __device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int3
 
 constexpr int MODE_ANY = 3;
 
-// One launch: workgroup b moves task task_off + b of the launch's task table.
+// One launch slice: workgroup b moves task task_off + xcd_order(b) of the
+// launch's task table.
 //   KIND: pack (bitwise copy into message buffers, never transposed),
 //         unpack-transform, or direct.
 //   MODE: the arithmetic of every pair of the call, or MODE_ANY to read it
 //         per workgroup (batches that mix modes; a workgroup's rectangles
 //         belong to one pair); CONJ likewise.
 //   HAS_T: whether the launch contains transposed rectangles (LDS tiles).
-// UL = 2: the launch runs on its wide task table (task0 of a rectangle in
-// aux), two units per lane.
+//   UL: units per lane of its row walks; with UL = 2 the table is the
+//       launch's wide task table, whose first task of a rectangle is in aux.
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T, int UL>
 __device__ __forceinline__ void mover_body(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks,
                                            int32_t task_off, void* const* __restrict__ bufs,
                                            const ItemParam* __restrict__ items, int32_t allow_wide,
-                                           int32_t remap) {
+                                           int32_t ranges) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
   __shared__ E lds[HAS_T ? TT::LDS_ELEMS : 1];
-  const int32_t b = task_off + xcd_order((int32_t)blockIdx.x, (int32_t)gridDim.x, remap);
+  const int32_t b = task_off + xcd_order((int32_t)blockIdx.x, (int32_t)gridDim.x, ranges);
   const int32_t pi = tasks[b];
   const int32_t c = b - (UL == 1 ? pieces[pi].task0 : pieces[pi].aux);
   if constexpr (KIND == KIND_PACK) {
@@ -426,17 +420,17 @@ template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
 costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
             void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
-            int32_t remap) {
+            int32_t ranges) {
   mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, units_per_lane<KIND, MODE, HAS_T>()>(pieces, tasks, task_off, bufs,
-                                                                                   items, allow_wide, remap);
+                                                                                   items, allow_wide, ranges);
 }
 
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 costa_mover_lds(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
                 void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
-                int32_t remap) {
-  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, 1>(pieces, tasks, task_off, bufs, items, allow_wide, remap);
+                int32_t ranges) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, 1>(pieces, tasks, task_off, bufs, items, allow_wide, ranges);
 }
 
 // Volume of the grid overlay: every overlay block (k, l) adds its element
@@ -478,7 +472,7 @@ struct Launch {
   void* const* bufs;
   const ItemParam* items;
   int32_t allow_wide;
-  int32_t remap;
+  int32_t ranges;
 };
 
 // Separable volume, step 1: histogram of overlay interval lengths by (class
@@ -526,10 +520,10 @@ hipError_t go(const Launch& l) {
     const unsigned n = (unsigned)(ntasks - off < kSlice ? ntasks - off : kSlice);
     if constexpr (big_lds<S, CPLX, HAS_T>())
       hipLaunchKernelGGL((costa_mover_lds<S, CPLX, KIND, MODE, CONJ, HAS_T>), dim3(n), dim3(kThreads), 0, l.stream,
-                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.remap);
+                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.ranges);
     else
       hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), dim3(n), dim3(kThreads), 0, l.stream,
-                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.remap);
+                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.ranges);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -567,10 +561,10 @@ hipError_t launch_typed(MoverKind kind, const LaunchSpec& spec, const Launch& l)
 
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
                         const int32_t* tasks, int64_t ntasks, const int32_t* wide, int64_t nwide, void* const* bufs,
-                        const ItemParam* items, int32_t allow_wide, int32_t xcd_remap, hipStream_t stream) {
+                        const ItemParam* items, int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream) {
   if (ntasks <= 0) return hipSuccess;
   if (!spec.has_transpose && nwide <= 0) return hipErrorInvalidValue;  // a launch of row walks has both tables
-  Launch l{stream, pieces, tasks, ntasks, wide, nwide, bufs, items, allow_wide, xcd_remap};
+  Launch l{stream, pieces, tasks, ntasks, wide, nwide, bufs, items, allow_wide, xcd_ranges};
   switch (dtype) {
     case COSTA_R64: return launch_typed<double, false>(kind, spec, l);
     case COSTA_C128: return launch_typed<double, true>(kind, spec, l);

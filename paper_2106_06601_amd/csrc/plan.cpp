@@ -250,20 +250,16 @@ void finish_piece(Piece& p, int elem_size) {
     p.flags |= PIECE_WIDE;
 }
 
-// Workgroup order per launch: 0 = dispatch order, 1 = runs of
-// COSTA_XCD_CHUNK tasks per XCD, 2 = one contiguous range per XCD when the
-// launch's tasks are all of one kind (all row-walk chunks or all LDS tiles,
-// so that equal ranges are equal work) and nearly all of its elements lie in
-// rectangles whose runs start and end on 128-byte lines.  Measured on MI355X:
-// +5 to +8% on such launches; -5 to -8% on launches of short runs that share
-// lines with their neighbours; -40% on a launch whose first half is row
-// walks and second half LDS tiles (four XCDs idle while four finish the
-// tiles).
-#ifndef COSTA_XCD_POLICY
-#define COSTA_XCD_POLICY 2
-#endif
-#ifndef COSTA_XCD_CHUNK
-#define COSTA_XCD_CHUNK 64
+// Workgroup order per launch: one contiguous range of tasks per XCD when the
+// launch's tasks are all of one kind (all row-walk chunks or all tiles, so
+// that equal ranges are equal work) and nearly all of its elements lie in
+// rectangles whose runs start and end on 128-byte lines; dispatch order
+// otherwise.  Measured on MI355X: +5 to +8% on such launches; -5 to -8% on
+// launches of short runs that share lines with their neighbours; -40% on a
+// launch whose first half is row walks and second half LDS tiles (four XCDs
+// idle while four finish the tiles).  COSTA_XCD_RANGES=0 turns it off.
+#ifndef COSTA_XCD_RANGES
+#define COSTA_XCD_RANGES 1
 #endif
 
 // Whether every run of the rectangle (its rows in the source and in the
@@ -367,9 +363,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     if (p.flags & PIECE_TRANSPOSE) transposed += (int64_t)p.nx * p.ny;
   }
   const bool one_kind = transposed == 0 || transposed == lr.elems;
-  lr.xcd_remap = COSTA_XCD_POLICY == 1 ? COSTA_XCD_CHUNK
-                 : COSTA_XCD_POLICY == 2 && one_kind && lr.elems > 0 && 10 * aligned >= 9 * lr.elems ? -1
-                                                                                                      : 0;
+  lr.xcd_ranges = COSTA_XCD_RANGES && one_kind && lr.elems > 0 && 10 * aligned >= 9 * lr.elems ? 1 : 0;
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
 }
