@@ -62,13 +62,17 @@ typedef enum {
 } costa_status;
 
 /* op of equation (eq:costa); for real types C equals T. */
-typedef enum { COSTA_OP_N = 0, COSTA_OP_T = 1, COSTA_OP_C = 2 } costa_op;
+/* The enumerations a caller passes in end with an *_INT32 member that no call
+ * accepts: it makes every int32 value a value of the type, so an unknown value
+ * passed through the ABI is reported as COSTA_ERROR_INVALID_VALUE rather than
+ * being undefined. */
+typedef enum { COSTA_OP_N = 0, COSTA_OP_T = 1, COSTA_OP_C = 2, COSTA_OP_INT32 = 0x7fffffff } costa_op;
 
 /* Storage order of blocks (Figure 1 "ordering"), or rank order of a process grid. */
-typedef enum { COSTA_COL_MAJOR = 0, COSTA_ROW_MAJOR = 1 } costa_order;
+typedef enum { COSTA_COL_MAJOR = 0, COSTA_ROW_MAJOR = 1, COSTA_ORDER_INT32 = 0x7fffffff } costa_order;
 
 /* Element type (Section 6: arbitrary types through templates). */
-typedef enum { COSTA_R64 = 0, COSTA_C128 = 1, COSTA_R32 = 2, COSTA_C64 = 3 } costa_dtype;
+typedef enum { COSTA_R64 = 0, COSTA_C128 = 1, COSTA_R32 = 2, COSTA_C64 = 3, COSTA_DTYPE_INT32 = 0x7fffffff } costa_dtype;
 
 /* Opaque, immutable layout L(A) = (Grid_A, P, Owners_A) plus the local view. */
 typedef struct costa_layout_s* costa_layout;
@@ -192,9 +196,10 @@ costa_status costa_relabel(int32_t P, const int64_t* V_host, int32_t* sigma, int
 /* Matching used for the relabeling (Section 4.3, Algorithm 1 "MWBPM"). */
 typedef enum {
   COSTA_RELABEL_EXACT = 0,  /* Hungarian method: an optimal relabeling */
-  COSTA_RELABEL_GREEDY = 1  /* the paper's greedy 2-approximation (Section 6): edges of G_delta
+  COSTA_RELABEL_GREEDY = 1, /* the paper's greedy 2-approximation (Section 6): edges of G_delta
                                by decreasing gain (ties: smaller label, then smaller rank) are
                                taken while both ends are free */
+  COSTA_RELABEL_INT32 = 0x7fffffff
 } costa_relabel_method;
 
 /* Relabeling under a general communication cost (Section 3): a package s of

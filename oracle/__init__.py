@@ -40,19 +40,23 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "costa_oracle.c")
-LIB_PATH = os.path.join(HERE, "liboracle.so")
+# COSTA_ORACLE_LIB: load another build of the same source (the tests'
+# sanitizer run builds one)
+LIB_PATH = os.environ.get("COSTA_ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
 
 OPS = {"N": 0, "T": 1, "C": 2}
 DTYPES = {"f64": 0, "c128": 1, "f32": 2, "c64": 3}
 NUMPY = {"f64": np.float64, "c128": np.complex128, "f32": np.float32, "c64": np.complex64}
 
 
-def build() -> str:
-    """Compile the oracle with gcc (no contraction of a*b+c into FMA)."""
-    cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
-           "-o", LIB_PATH, SRC]
+def build(out=None, cc="gcc", extra=()) -> str:
+    """Compile the oracle (no contraction of a*b+c into FMA); by default with
+    gcc into oracle/liboracle.so."""
+    out = out or LIB_PATH
+    cmd = [cc, "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", *extra,
+           "-o", out, SRC]
     subprocess.run(cmd, check=True)
-    return LIB_PATH
+    return out
 
 
 class _OLayout(ctypes.Structure):

@@ -36,8 +36,26 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False, defines=(), out=None, build_dir=None, synth=True) -> str:
-    """defines: extra -D flags (tuning experiments); out: library path."""
+# Host-side sanitizers (AddressSanitizer + UndefinedBehaviorSanitizer) for the
+# library's host code only: each flag is scoped to the host pass, the device
+# code is compiled as usual.
+SANITIZE_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=undefined"]
+
+
+def sanitizer_runtime() -> str:
+    """The AddressSanitizer runtime of the compiler that builds the library
+    (to be preloaded into an uninstrumented host process)."""
+    import glob
+    found = sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    if not found:
+        raise RuntimeError("libclang_rt.asan-x86_64.so not found under /opt/rocm/llvm")
+    return found[-1]
+
+
+def build(verbose: bool = False, defines=(), out=None, build_dir=None, synth=True, sanitize=False) -> str:
+    """defines: extra -D flags (tuning experiments); out: library path;
+    sanitize: instrument the host code with ASan and UBSan."""
     lib = out or LIB
     bdir = build_dir or BUILD_DIR
     os.makedirs(bdir, exist_ok=True)
@@ -48,8 +66,8 @@ def build(verbose: bool = False, defines=(), out=None, build_dir=None, synth=Tru
         obj = os.path.join(bdir, src + ".o")
         objs.append(obj)
         lang = ["-x", "hip"]
-        jobs.append([HIPCC, f"--offload-arch={ARCH}", *COMMON, *[f"-D{d}" for d in defines], *lang, "-c", path,
-                     "-o", obj])
+        jobs.append([HIPCC, f"--offload-arch={ARCH}", *COMMON, *(SANITIZE_HOST if sanitize else []),
+                     *[f"-D{d}" for d in defines], *lang, "-c", path, "-o", obj])
     with ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         outs = list(ex.map(_run, jobs))
     if verbose:
@@ -57,7 +75,8 @@ def build(verbose: bool = False, defines=(), out=None, build_dir=None, synth=Tru
             if o.strip():
                 print(o)
     tmp = lib + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    link_san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-shared-libsan"]
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *(link_san if sanitize else []), "-o", tmp, *objs])
     os.replace(tmp, lib)
     if not synth:
         return lib

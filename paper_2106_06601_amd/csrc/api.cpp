@@ -26,8 +26,8 @@ int elem_size(costa_dtype d) {
     case COSTA_C128: return 16;
     case COSTA_R32: return 4;
     case COSTA_C64: return 8;
+    default: return 0;  // not an element type
   }
-  return 0;
 }
 bool is_complex(costa_dtype d) { return d == COSTA_C128 || d == COSTA_C64; }
 

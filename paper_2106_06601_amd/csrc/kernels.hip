@@ -570,8 +570,8 @@ hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spe
     case COSTA_C128: return launch_typed<double, true>(kind, spec, l);
     case COSTA_R32: return launch_typed<float, false>(kind, spec, l);
     case COSTA_C64: return launch_typed<float, true>(kind, spec, l);
+    default: return hipErrorInvalidValue;
   }
-  return hipErrorInvalidValue;
 }
 
 hipError_t launch_volume_separable(const SeparableArgs& a, hipStream_t stream) {
