@@ -192,6 +192,41 @@ def test_random_layouts_full_compare(dtype):
         case.check_full()
 
 
+@pytest.mark.parametrize("dtype", ["f64", "c128"])
+def test_random_larger_layouts_full_compare(dtype):
+    """Random layouts large enough that rectangles span many tasks, several
+    tile rows and columns, wide tasks and per-XCD ranges (up to 3000 x 3000,
+    up to 16 ranks, block sizes 1-300), every element compared."""
+    rng = np.random.default_rng({"f64": 21, "c128": 22}[dtype])
+    for case_no in range(8):
+        P = int(rng.integers(1, 17))
+        M, N = int(rng.integers(500, 3001)), int(rng.integers(500, 3001))
+        op = ["N", "T", "C"][case_no % 3]
+        oa = "col" if rng.random() < 0.5 else "row"
+        ob = "col" if rng.random() < 0.5 else "row"
+
+        def lay(m, n, order):
+            if rng.random() < 0.7:
+                divs = [d for d in range(1, P + 1) if P % d == 0]
+                pr = divs[int(rng.integers(0, len(divs)))]
+                return BC(m, n, int(rng.integers(1, 301)), int(rng.integers(1, 301)), pr, P // pr,
+                          "row" if rng.random() < 0.5 else "col", order)
+            return _random_general(rng, m, n, P, order)
+
+        A = lay(M, N, oa)
+        B = lay(M if op == "N" else N, N if op == "N" else M, ob)
+        sc = CSCALARS if dtype == "c128" else SCALARS
+        alpha, beta = sc[case_no % len(sc)]
+        sigma = rng.permutation(P).tolist() if rng.random() < 0.5 else None
+        w = synth.Workload(f"larger{case_no}", dtype, [synth.Item(A, B, op, alpha, beta)], False, seed=case_no + 70)
+        _say(f"larger random {dtype} case {case_no}: P={P} {M}x{N} op={op} A={A.kind}/{oa} B={B.kind}/{ob} "
+             f"alpha={alpha} beta={beta} sigma={sigma}")
+        case = Case(w, sigma=sigma)
+        case.run()
+        case.check_full()
+        case.free()
+
+
 def test_random_batched_full_compare():
     rng = np.random.default_rng(11)
     for case_no in range(6):
