@@ -311,6 +311,7 @@ def main():
         "waves": m["kernels"].get("pack", {}).get("launches_per_step", 0), "plan_s": round(t_setup + m["first_step_s"], 3),
         "kernels": m["kernels"],
         "roofline": m["roofline"],
+        "copy_ceiling": m["copy_ceiling"],
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -371,8 +372,33 @@ def measure(step, stats: dict, workload: str, args) -> dict:
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
             "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
     return {"value": round(value, 1), "ms_per_step": round(ms_per_step, 4), "kernels": per_kernel,
-            "roofline": roof, "first_step_s": first_step_s,
+            "roofline": roof, "first_step_s": first_step_s, "copy_ceiling": copy_ceiling(dev, stream),
             "ms_per_step_median": round(per_step[len(per_step) // 2], 4), "ms_per_step_min": round(per_step[0], 4)}
+
+
+def copy_ceiling(dev, stream, mib: int = 1024, reps: int = 10):
+    """Context beside the 8 TB/s peak (not a target): a plain device-to-device
+    copy of `mib` MiB (torch's copy_), read + write bytes over its event time,
+    after the timed steps.  None when the memory is not free."""
+    import torch
+    nbytes = mib << 20
+    if torch.cuda.mem_get_info(dev)[0] < 2 * nbytes + (256 << 20):
+        return None
+    src = torch.ones(nbytes // 8, dtype=torch.float64, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"GB_s": round(2 * nbytes / (ms * 1e-3) / 1e9, 1), "bytes_per_copy": 2 * nbytes,
+            "kind": f"device copy of {mib} MiB (torch copy_), read + write bytes"}
 
 
 def scalapack_bench(name: str, args) -> dict:
