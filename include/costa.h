@@ -198,7 +198,8 @@ typedef enum {
   COSTA_RELABEL_EXACT = 0,  /* Hungarian method: an optimal relabeling */
   COSTA_RELABEL_GREEDY = 1, /* the paper's greedy 2-approximation (Section 6): edges of G_delta
                                by decreasing gain (ties: smaller label, then smaller rank) are
-                               taken while both ends are free */
+                               taken while both ends are free; the identity when that perfect
+                               matching's total gain is negative (gains can be) */
   COSTA_RELABEL_INT32 = 0x7fffffff
 } costa_relabel_method;
 

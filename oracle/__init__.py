@@ -405,7 +405,13 @@ def relabel_greedy(V: np.ndarray, w=w_locally_free) -> List[int]:
     """Algorithm 1 with the matching the paper's implementation uses (Section 6:
     a simple greedy 2-approximation): weights[i][j] = delta(p_i, p_j), edges
     taken by decreasing weight (ties: smaller i, then smaller j) while both ends
-    are free; sigma[i] = j for every matched (p_i, p_j)."""
+    are free; sigma[i] = j for every matched (p_i, p_j).
+
+    The gains can be negative, and completing the greedy matching to a perfect
+    one can then give a total gain below zero, below the identity's (always a
+    perfect matching, with gain 0, as the proof of Theorem 2 in Section 4.2
+    notes), which no 2-approximation of a maximum >= 0 can return.  The
+    identity is kept in that case."""
     P = V.shape[0]
     weights = [[gain(V, i, j, w) for j in range(P)] for i in range(P)]
     edges = sorted(((i, j) for i in range(P) for j in range(P)), key=lambda e: (-weights[e[0]][e[1]], e[0], e[1]))
@@ -415,6 +421,8 @@ def relabel_greedy(V: np.ndarray, w=w_locally_free) -> List[int]:
         if sigma[i] < 0 and not used[j]:
             sigma[i] = j
             used[j] = True
+    if sum(weights[i][sigma[i]] for i in range(P)) < 0:
+        return list(range(P))
     return sigma
 
 

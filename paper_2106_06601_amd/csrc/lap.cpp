@@ -154,7 +154,11 @@ namespace {
 
 // The paper's greedy matching (Section 6): edges by decreasing weight, ties
 // by smaller row then smaller column; an edge is taken while both ends are
-// free.  weight[x*n + y]; returns rowcol[x] = y.
+// free.  weight[x*n + y]; returns rowcol[x] = y.  The weights (gains) can be
+// negative: when the completed perfect matching has a total weight below
+// zero, the identity (weight 0, always a perfect matching of the complete
+// graph G_delta, Theorem 2) is returned instead, since a 2-approximation of a
+// maximum that is >= 0 cannot be negative.
 template <typename T>
 void greedy_matching(int n, const std::vector<T>& weight, std::vector<int>& rowcol) {
   std::vector<int64_t> order((size_t)n * n);
@@ -170,6 +174,10 @@ void greedy_matching(int n, const std::vector<T>& weight, std::vector<int>& rowc
     rowcol[x] = y;
     if (++taken == n) break;
   }
+  T total = 0;
+  for (int x = 0; x < n; ++x) total += weight[(size_t)x * n + rowcol[x]];
+  if (total < 0)
+    for (int x = 0; x < n; ++x) rowcol[x] = x;
 }
 
 }  // namespace

@@ -262,6 +262,86 @@ def test_remark_gain_closed_form():
             assert oracle.gain(V, x, y) == int(V[y, x]) - int(V[x, x])
 
 
+def test_topology_cost_hand_example():
+    """P = 2 under the latency-bandwidth cost of Section 3: rank 0 sends 5
+    elements to label 1, rank 1 sends 3 to label 0, latency 2 and 1 unit per
+    byte between the two ranks, nothing within a rank.  By hand: identity
+    W = (2 + 5) + (2 + 3) = 12; swapping the labels makes both packages
+    local, W = 0; delta(p_0, p_1) = w(1,0,3) - w(1,1,3) = 5 and
+    delta(p_1, p_0) = w(0,1,5) - w(0,0,5) = 7 (eq:delta)."""
+    V = np.array([[0, 5], [3, 0]], np.int64)
+    w = oracle.w_topology(np.array([[0.0, 2.0], [2.0, 0.0]]), np.array([[0.0, 1.0], [1.0, 0.0]]), 1.0)
+    assert oracle.total_cost(V, [0, 1], w) == 12 and oracle.total_cost(V, [1, 0], w) == 0
+    assert oracle.gain(V, 0, 1, w) == 5 and oracle.gain(V, 1, 0, w) == 7
+    assert oracle.relabel_bruteforce_cost(V, w) == [1, 0]
+    assert oracle.relabel_greedy(V, w) == [1, 0]
+    # asymmetric links: only the bandwidth term of the used direction counts
+    w2 = oracle.w_topology(np.zeros((2, 2)), np.array([[0.0, 1.0], [10.0, 0.0]]), 2.0)
+    assert oracle.total_cost(V, [0, 1], w2) == 5 * 2 * 1.0 + 3 * 2 * 10.0
+
+
+def test_greedy_hand_example_is_suboptimal():
+    """Locally-free cost, P = 3, by hand: label 0 receives 5 from rank 1 and
+    4 from rank 2; label 2 receives 4 from rank 1.  The gains are
+    delta(p_x, p_y) = V[y][x] - V[x][x]: the heaviest edge (0 -> 1, gain 5)
+    is taken first and blocks both edges of gain 4, so the greedy matching
+    keeps 5 elements local (sigma = [1, 0, 2], W = 13 - 5 = 8) while the
+    optimum keeps 8 (sigma = [2, 0, 1], W = 5) -- within the factor 2 of a
+    greedy matching."""
+    V = np.array([[0, 0, 0], [5, 0, 4], [4, 0, 0]], np.int64)
+    assert oracle.total_cost(V, [0, 1, 2]) == 13
+    g = oracle.relabel_greedy(V)
+    assert g == [1, 0, 2]
+    assert oracle.retained(V, g) == 5 and oracle.total_cost(V, g) == 8
+    opt = oracle.relabel_bruteforce(V)
+    assert opt == [2, 0, 1]
+    assert oracle.retained(V, opt) == 8 and oracle.total_cost(V, opt) == 5
+
+
+def test_greedy_keeps_the_identity_when_its_matching_loses():
+    """Locally-free cost, P = 2, by hand: V = [[7, 2], [0, 0]].  Gains
+    delta(p_x, p_y) = V[y][x] - V[x][x]: delta(p_1, p_0) = 2 is the only
+    positive edge; taking it leaves (p_0, p_1) with delta = 0 - 7 = -7, a
+    perfect matching of total gain -5 that moves 7 local elements off their
+    rank to keep 2.  The identity (gain 0) is the result."""
+    V = np.array([[7, 2], [0, 0]], np.int64)
+    assert oracle.gain(V, 1, 0) == 2 and oracle.gain(V, 0, 1) == -7
+    assert oracle.total_gain(V, [1, 0]) == -5
+    assert oracle.relabel_greedy(V) == [0, 1]
+    assert oracle.relabel_bruteforce(V) == [0, 1]
+
+
+def test_greedy_is_a_two_approximation_and_never_loses():
+    """A greedy matching on non-negative weights has at least half the
+    weight of a maximum matching (the bound Section 6 relies on): checked
+    against brute force over all P! relabelings wherever every gain is >= 0
+    (volume matrices with an empty diagonal under the locally-free cost).
+    For any volumes and either cost the result is never worse than the
+    identity (Lemma 1: total gain = W(G) - W(G_sigma))."""
+    rng = np.random.default_rng(5)
+    for P in range(2, 7):
+        for _ in range(6):
+            V = _rand_V(rng, P, hi=9)
+            ident = list(range(P))
+            g = oracle.relabel_greedy(V)
+            assert sorted(g) == ident
+            assert oracle.total_gain(V, g) >= 0
+            assert oracle.total_cost(V, g) <= oracle.total_cost(V, ident)
+            Z = V.copy()
+            np.fill_diagonal(Z, 0)
+            assert all(oracle.gain(Z, x, y) >= 0 for x in range(P) for y in range(P))
+            best = max(oracle.total_gain(Z, list(p)) for p in itertools.permutations(range(P)))
+            assert 2 * oracle.total_gain(Z, oracle.relabel_greedy(Z)) >= best
+            L = rng.random((P, P)) * 3
+            Bw = rng.random((P, P))
+            np.fill_diagonal(L, 0.0)
+            np.fill_diagonal(Bw, 0.0)
+            w = oracle.w_topology(L, Bw, 8.0)
+            sg = oracle.relabel_greedy(V, w)
+            assert sorted(sg) == ident
+            assert oracle.total_cost(V, sg, w) <= oracle.total_cost(V, ident, w) + 1e-9
+
+
 def test_blocksize_change_canonical_relabeling():
     # full-size volume pattern (closed form, 4,194,304 per non-zero pair); the
     # optimum keeps 25% local, identity 6.25%

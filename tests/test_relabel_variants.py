@@ -27,6 +27,29 @@ def test_greedy_locally_free_matches_oracle():
             assert after == oracle.total_cost(V, sig)
 
 
+def test_greedy_never_raises_the_cost():
+    """Gains can be negative: on [[7, 2], [0, 0]] the greedy perfect matching
+    has total gain -5 and the identity is kept (both costs)."""
+    V = np.array([[7, 2], [0, 0]], np.int64)
+    assert C.costa_relabel_cost(V, method="greedy") == ([0, 1], 2.0, 2.0)  # only V[0][1] is remote
+    L = np.array([[0.0, 1.0], [1.0, 0.0]])
+    Bw = np.array([[0.0, 1.0], [1.0, 0.0]])
+    sig, before, after = C.costa_relabel_cost(V, 1.0, L, Bw, "greedy")
+    assert sig == [0, 1] and before == after == 3.0
+    rng = np.random.default_rng(23)
+    for P in (2, 3, 5, 8, 17):
+        for _ in range(5):
+            V = _rand(rng, P, hi=9, zero=0.1)
+            _, before, after = C.costa_relabel_cost(V, method="greedy")
+            assert after <= before
+            L = rng.random((P, P))
+            Bw = rng.random((P, P))
+            np.fill_diagonal(L, 0.0)
+            np.fill_diagonal(Bw, 0.0)
+            _, before, after = C.costa_relabel_cost(V, 4.0, L, Bw, "greedy")
+            assert after <= before
+
+
 def test_exact_locally_free_is_the_canonical_relabeling():
     rng = np.random.default_rng(22)
     for P in (3, 7, 12):
