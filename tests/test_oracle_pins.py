@@ -177,6 +177,25 @@ def test_volume_scaled_transpose_matches_separable_small():
     _check_conservation(V, it.A, it.B, it.op)
 
 
+def test_volume_separable_matches_bruteforce_rectangular_blocks():
+    """The per-dimension count against element-by-element counting on
+    block-cyclic layouts with non-square blocks, both rank orders and all
+    ops (a transposed op reads B's column blocks along A's rows)."""
+    rng = np.random.default_rng(6)
+    for case in range(12):
+        op = "NTC"[case % 3]
+        M, N = int(rng.integers(20, 60)), int(rng.integers(20, 60))
+        pa = [(1, 6), (2, 3), (3, 2), (6, 1)][int(rng.integers(0, 4))]
+        pb = [(1, 6), (2, 3), (3, 2), (6, 1)][int(rng.integers(0, 4))]
+        a, b = int(rng.integers(1, 7)), int(rng.integers(1, 7))
+        A = BC(M, N, a, a + int(rng.integers(1, 4)), pa[0], pa[1], ["row", "col"][case % 2], "col")
+        bm, bn = (M, N) if op == "N" else (N, M)
+        B = BC(bm, bn, b + int(rng.integers(1, 4)), b, pb[0], pb[1], ["col", "row"][(case // 2) % 2], "row")
+        V = oracle.volume(oracle.OLayout(A), oracle.OLayout(B), op)
+        assert np.array_equal(V, _separable_volume(A, B, op)), (case, A, B, op)
+        _check_conservation(V, A, B, op)
+
+
 def test_volume_scaled_transpose_full_size_retained():
     # full 20000^2 by per-dimension counting: identity keeps 12,500,384 elements
     # local, the optimal relabeling 13,407,488
@@ -399,7 +418,7 @@ def _dense_from_single_block(buf, spec):
 @pytest.mark.parametrize("dtype", ["f64", "c128", "f32"])
 @pytest.mark.parametrize("op", ["N", "T", "C"])
 @pytest.mark.parametrize("orders", [("col", "col"), ("row", "col"), ("col", "row")])
-@pytest.mark.parametrize("ab", [(1.0, 0.0), (2.0, 0.5), (-0.5, 0.25), ((0.5 - 0.25j), (0.25 + 0.5j))])
+@pytest.mark.parametrize("ab", [(1.0, 0.0), (-2.0, 0.0), (2.0, 0.5), (-0.5, 0.25), ((0.5 - 0.25j), (0.25 + 0.5j))])
 def test_single_rank_reduces_to_dense_numpy(dtype, op, orders, ab):
     """P = 1, one block: the transform is textbook alpha*op(B) + beta*A on the
     dense matrix.  Power-of-two scalars make every product exact, so numpy and
