@@ -4,6 +4,7 @@ rounded on its own)."""
 import numpy as np
 
 import oracle
+import synth
 
 
 def _index(p):
@@ -40,3 +41,19 @@ def _combine(dtype, b, a, alpha, beta, conj):
     out.real = t1r
     out.imag = t1i
     return out
+
+
+def many_rank_cases():
+    """(dtype, op, alpha, beta, A, B, sigma) at many virtual ranks; sigma
+    "auto" means relabeling on."""
+    BC = synth.BlockCyclic
+    return [
+        # P = 1024: the source's 16 block columns leave half of its process
+        # columns empty (zero-size buffers); relabeling on
+        ("f64", "T", 2.0, 0.5,
+         BC(2048, 2048, 64, 64, 32, 32, "row", "col"), BC(2048, 2048, 16, 128, 32, 32, "col", "row"), "auto"),
+        # P = 4096: one 64 x 64 block per target rank, a random relabeling
+        ("c128", "C", 1.0, 0.0,
+         BC(4096, 4096, 64, 64, 64, 64, "col", "col"), BC(4096, 4096, 96, 32, 64, 64, "row", "col"),
+         np.random.default_rng(41).permutation(4096).tolist()),
+    ]

@@ -10,6 +10,7 @@ import torch
 
 import oracle
 import synth
+from replay import many_rank_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -225,6 +226,17 @@ def test_random_larger_layouts_full_compare(dtype):
         case.run()
         case.check_full()
         case.free()
+
+
+@pytest.mark.parametrize("k", [0, 1])
+def test_many_virtual_ranks_full_compare(k):
+    dtype, op, alpha, beta, A, B, sigma = many_rank_cases()[k]
+    w = synth.Workload(f"many{k}", dtype, [synth.Item(A, B, op, alpha, beta)], sigma == "auto", seed=90 + k)
+    _say(f"many ranks: P={A.nranks} {dtype} op={op} sigma={'relabel' if sigma == 'auto' else 'random'}")
+    case = Case(w, sigma="auto" if sigma == "auto" else sigma)
+    case.run()
+    case.check_full()
+    case.free()
 
 
 def test_random_batched_full_compare():

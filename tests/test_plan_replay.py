@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from replay import _combine, _index
+from replay import _combine, _index, many_rank_cases
 
 C = pytest.importorskip("paper_2106_06601_amd")
 
@@ -218,6 +218,17 @@ def test_replay_random_layouts(seed):
         else [(1.0, 0.0), (2.0, 0.5), (-1.5, 0.0)][seed % 3]
     w = synth.Workload("r", dtype, [synth.Item(A, B, op, alpha, beta)], False, seed=seed)
     replay(w, sigma=rng.permutation(P).tolist())
+
+
+@pytest.mark.parametrize("k", [0, 1])
+def test_replay_many_virtual_ranks(k):
+    """1024 and 4096 ranks, empty source process columns, relabeling by the
+    library's exact LAP or a random permutation."""
+    dtype, op, alpha, beta, A, B, sigma = many_rank_cases()[k]
+    w = synth.Workload(f"many{k}", dtype, [synth.Item(A, B, op, alpha, beta)], sigma == "auto", seed=90 + k)
+    if sigma == "auto":
+        sigma = C.costa_relabel(oracle.volume(oracle.OLayout(A), oracle.OLayout(B), op))[0]
+    replay(w, sigma=sigma)
 
 
 @pytest.mark.parametrize("name", synth.WORKLOADS)
