@@ -193,13 +193,13 @@ def test_random_layouts_full_compare(dtype):
         case.check_full()
 
 
-@pytest.mark.parametrize("dtype", ["f64", "c128"])
+@pytest.mark.parametrize("dtype", ["f64", "c128", "f32", "c64"])
 def test_random_larger_layouts_full_compare(dtype):
     """Random layouts large enough that rectangles span many tasks, several
     tile rows and columns, wide tasks and per-XCD ranges (up to 3000 x 3000,
     up to 16 ranks, block sizes 1-300), every element compared."""
-    rng = np.random.default_rng({"f64": 21, "c128": 22}[dtype])
-    for case_no in range(8):
+    rng = np.random.default_rng({"f64": 21, "c128": 22, "f32": 23, "c64": 24}[dtype])
+    for case_no in range(8 if dtype in ("f64", "c128") else 4):
         P = int(rng.integers(1, 17))
         M, N = int(rng.integers(500, 3001)), int(rng.integers(500, 3001))
         op = ["N", "T", "C"][case_no % 3]
@@ -216,7 +216,7 @@ def test_random_larger_layouts_full_compare(dtype):
 
         A = lay(M, N, oa)
         B = lay(M if op == "N" else N, N if op == "N" else M, ob)
-        sc = CSCALARS if dtype == "c128" else SCALARS
+        sc = CSCALARS if dtype in ("c128", "c64") else SCALARS
         alpha, beta = sc[case_no % len(sc)]
         sigma = rng.permutation(P).tolist() if rng.random() < 0.5 else None
         w = synth.Workload(f"larger{case_no}", dtype, [synth.Item(A, B, op, alpha, beta)], False, seed=case_no + 70)
