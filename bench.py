@@ -230,6 +230,8 @@ def main():
     ap.add_argument("--bench2-sweep", action="store_true",
                     help="print the volume-reduction sweep of the paper's relabeling benchmark")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be >= 1 and --warmup >= 0")
     if args.bench2_sweep:
         print(json.dumps(bench2_sweep()), flush=True)
         return
