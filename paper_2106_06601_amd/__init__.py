@@ -261,7 +261,9 @@ class Layout:
 
     def __del__(self):
         h, self.handle = getattr(self, "handle", None), None
-        if h:
+        # at interpreter exit the module's globals may already be cleared;
+        # the process is ending and the handle goes with it
+        if h and _lib is not None:
             _lib.costa_layout_destroy(h)
 
 
