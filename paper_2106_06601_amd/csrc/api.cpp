@@ -50,8 +50,11 @@ struct DevicePlan {
   size_t table_bytes = 0;
   size_t nbufs = 0;
   std::vector<unsigned char> last_table;
-  hipEvent_t table_event = nullptr;
+  hipEvent_t table_event = nullptr;  // the last table upload (h_staging reusable after it)
   bool table_pending = false;
+  hipEvent_t last_use = nullptr;     // end of the last call's launches (they read d_table)
+  hipStream_t last_stream = nullptr;
+  bool used = false;
   ~DevicePlan() {
     if (d_pieces) (void)hipFree(d_pieces);
     if (d_tasks) (void)hipFree(d_tasks);
@@ -59,6 +62,7 @@ struct DevicePlan {
     if (d_table) (void)hipFree(d_table);
     if (h_staging) (void)hipHostFree(h_staging);
     if (table_event) (void)hipEventDestroy(table_event);
+    if (last_use) (void)hipEventDestroy(last_use);
   }
 };
 
@@ -341,6 +345,7 @@ costa_status get_plan(State& S, costa_dtype dt, const std::vector<ItemDesc>& ite
   HIP_OR_FAIL(hipMalloc(&dp->d_table, dp->table_bytes));
   HIP_OR_FAIL(hipHostMalloc(&dp->h_staging, dp->table_bytes, hipHostMallocDefault));
   HIP_OR_FAIL(hipEventCreateWithFlags(&dp->table_event, hipEventDisableTiming));
+  HIP_OR_FAIL(hipEventCreateWithFlags(&dp->last_use, hipEventDisableTiming));
   out = dp.get();
   S.plans.emplace(key, std::move(dp));
   return COSTA_SUCCESS;
@@ -394,6 +399,9 @@ costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_des
     reads_a[k] = !bz;
   }
   if (table != dp->last_table) {
+    // the kernels of the plan's last call read the table until they end: on
+    // another stream, the new table is written only after them
+    if (dp->used && dp->last_stream != stream) HIP_OR_FAIL(hipStreamWaitEvent(stream, dp->last_use, 0));
     if (dp->table_pending) HIP_OR_FAIL(hipEventSynchronize(dp->table_event));
     std::memcpy(dp->h_staging, table.data(), table.size());
     HIP_OR_FAIL(hipMemcpyAsync(dp->d_table, dp->h_staging, table.size(), hipMemcpyHostToDevice, stream));
@@ -432,6 +440,9 @@ costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_des
     ws->last_stream = stream;
     ws->used = true;
   }
+  HIP_OR_FAIL(hipEventRecord(dp->last_use, stream));
+  dp->last_stream = stream;
+  dp->used = true;
   return COSTA_SUCCESS;
 }
 

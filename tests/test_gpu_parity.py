@@ -369,6 +369,36 @@ def test_two_streams_share_the_workspace_safely():
     c2.check_full()
 
 
+@pytest.mark.parametrize("kind", ["messages", "direct_only"])
+def test_one_plan_two_streams_different_buffers(kind):
+    """Two calls of one cached plan with different buffers, on two streams,
+    issued back to back while the first call's kernels still run (full
+    16384^2 sizes): the second call's buffer table must not reach the first
+    call's kernels.  direct_only: a plan without message buffers (the same
+    layout for A and B), where nothing else orders the two calls."""
+    if kind == "messages":
+        w = synth.workload("blocksize_change_16k")
+    else:
+        L = BC(16384, 16384, 256, 256, 4, 4, "row", "col")
+        w = synth.Workload("same_layout", "f64", [synth.Item(L, L, "N", 2.0, 0.5)], False, seed=33)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s1):
+        c1 = Case(w, sigma=None)
+    with torch.cuda.stream(s2):
+        c2 = Case(w, sigma=None)
+    torch.cuda.synchronize()
+    _say(f"one plan, two streams: {kind}")
+    with torch.cuda.stream(s1):
+        c1.run()
+    with torch.cuda.stream(s2):
+        c2.run()
+    torch.cuda.synchronize()
+    c1.check_sampled(n_random=100000, n_corners=100000)
+    c2.check_sampled(n_random=100000, n_corners=100000)
+    c1.free()
+    c2.free()
+
+
 def test_timing_counters():
     w = synth.workload("blocksize_change_16k", "small")
     case = Case(w)
