@@ -3,8 +3,9 @@
 Argument marshalling only: every function calls the C ABI of
 ``include/costa.h`` with the same name; all work runs in the library's HIP
 kernels and host planner.  Device buffers are passed as ``torch`` tensors (or
-raw integer addresses); torch is used for nothing else.  Importing this module
-fails loudly when the library has not been built.
+raw integer addresses); torch is used for nothing else, except that it is
+imported before the library so that the process holds a single HIP runtime.
+Importing this module fails loudly when the library has not been built.
 """
 from __future__ import annotations
 
@@ -20,6 +21,16 @@ LIB_PATH = os.environ.get("COSTA_LIB") or os.path.join(_HERE, "libcosta_mi355x.s
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                       "(or python paper_2106_06601_amd/build.py)")
+
+# One HIP runtime per process.  PyTorch ships its own libamdhip64 and its
+# libraries ask for it by a name that does not match the ROCm copy this
+# library links; loaded first, the ROCm copy would leave two runtimes in the
+# process, of which one sees no device.  With torch loaded first, this library
+# binds to torch's runtime.
+try:
+    import torch  # noqa: F401
+except ImportError:  # no torch: the ROCm runtime alone
+    pass
 
 _lib = ctypes.CDLL(LIB_PATH)
 

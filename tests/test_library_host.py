@@ -204,3 +204,29 @@ def test_plan_waves_respect_workspace_limit():
         C.costa_set_workspace_limit(0)
     st = C.costa_plan_stats(w.dtype, descs)
     assert st["waves"] == 1
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """The binding, the seeded fill library and the C client library, loaded
+    before anything imports torch, leave one HIP runtime in the process
+    (torch's): two copies would each see a different set of devices."""
+    import subprocess
+    import sys
+    code = """
+import ctypes, os, sys
+sys.path.insert(0, %r)
+sys.path.insert(0, os.path.join(%r, "tests"))
+import paper_2106_06601_amd
+import synth
+synth.lib()
+from c_client import build_client
+if os.path.exists(build_client.LIB_OUT):
+    ctypes.CDLL(build_client.LIB_OUT)
+import torch
+maps = open("/proc/self/maps").read().splitlines()
+print(len({l.split()[-1] for l in maps if "libamdhip64" in l}))
+""" % (ROOT, ROOT)
+    r = subprocess.run([sys.executable, "-c", code], stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert r.stdout.strip().splitlines()[-1] == "1"
