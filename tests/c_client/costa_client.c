@@ -10,6 +10,11 @@
  *       reads dir/b.bin and dir/a.bin (the local buffers of ranks 0..P-1,
  *       one after another), writes dir/out.bin (A after the transform)
  *
+ * Built with -DCOSTA_CLIENT_NO_MAIN -shared, the same code is a library whose
+ * costa_client_host() and costa_client_gpu() do what "host" and "gpu" do, for
+ * callers that must stay in one process (a process that has already used the
+ * GPU does not start others).
+ *
  * ro / bo: 'r' (row-major) or 'c' (column-major) rank order and block
  * storage order of a block-cyclic layout.  Exit status 0 on success. */
 #include <stdint.h>
@@ -55,7 +60,9 @@ static costa_status make_layout(char** a, costa_layout* out) {
                                           atoi(a[5]), order_of(a[6]), order_of(a[7]), out);
 }
 
-static int host_mode(char** a, char** b, const char* ops) {
+int costa_client_host(char** a, char** b, const char* ops);
+
+int costa_client_host(char** a, char** b, const char* ops) {
   costa_layout A = NULL, B = NULL;
   CHECK(make_layout(a, &A));
   CHECK(make_layout(b, &B));
@@ -126,7 +133,9 @@ static int read_all(const char* path, double* dst, size_t n) {
   return got == n ? 0 : 1;
 }
 
-static int gpu_mode(const char* dir, char** a, char** b, const char* ops, double alpha, double beta) {
+int costa_client_gpu(const char* dir, char** a, char** b, const char* ops, double alpha, double beta);
+
+int costa_client_gpu(const char* dir, char** a, char** b, const char* ops, double alpha, double beta) {
   costa_layout A = NULL, B = NULL;
   CHECK(make_layout(a, &A));
   CHECK(make_layout(b, &B));
@@ -189,21 +198,26 @@ static int gpu_mode(const char* dir, char** a, char** b, const char* ops, double
   HIP_CHECK(hipStreamDestroy(stream));
   CHECK(costa_layout_destroy(A));
   CHECK(costa_layout_destroy(B));
-  CHECK(costa_finalize());
   free(na);
   free(nb);
   free(dA);
   free(dB);
   free(ha);
   free(hb);
-  printf("ok\n");
   return 0;
 }
 
+#ifndef COSTA_CLIENT_NO_MAIN
 int main(int argc, char** argv) {
-  if (argc == 19 && strcmp(argv[1], "host") == 0) return host_mode(argv + 2, argv + 10, argv[18]);
-  if (argc == 22 && strcmp(argv[1], "gpu") == 0)
-    return gpu_mode(argv[2], argv + 3, argv + 11, argv[19], atof(argv[20]), atof(argv[21]));
+  if (argc == 19 && strcmp(argv[1], "host") == 0) return costa_client_host(argv + 2, argv + 10, argv[18]);
+  if (argc == 22 && strcmp(argv[1], "gpu") == 0) {
+    const int rc = costa_client_gpu(argv[2], argv + 3, argv + 11, argv[19], atof(argv[20]), atof(argv[21]));
+    if (rc != 0) return rc;
+    CHECK(costa_finalize()); /* a program that is done with the library releases its caches */
+    printf("ok\n");
+    return 0;
+  }
   fprintf(stderr, "usage: costa_client host <A x8> <B x8> <op> | gpu <dir> <A x8> <B x8> <op> <alpha> <beta>\n");
   return 2;
 }
+#endif

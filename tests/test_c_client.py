@@ -6,9 +6,11 @@ of the host-only entry points printed by the C program (local sizes, plan
 statistics, every field of every exported rectangle, relabelings, error
 codes) equals what the binding reads through ctypes -- so the header, the
 library and the binding agree on struct layouts and enum values.
-GPU: the C program runs a transform on buffers it allocates with hipMalloc;
-the result equals the oracle's bit for bit.
+GPU: the same C code, loaded as a library (the test process already uses
+the GPU, so it starts no other process), runs a transform on buffers it
+allocates with hipMalloc; the result equals the oracle's bit for bit.
 """
+import ctypes
 import os
 import shutil
 import subprocess
@@ -91,8 +93,12 @@ def test_c_program_agrees_with_the_binding(fresh_client, k):
 @pytest.mark.gpu
 @pytest.mark.parametrize("k", range(len(CASES)))
 def test_c_program_transform_matches_oracle(tmp_path, k):
-    client = build_client.OUT
-    assert os.path.exists(client), "tests/c_client/costa_client is not built: run __graft_entry__.build()"
+    lib = build_client.LIB_OUT
+    assert os.path.exists(lib), "tests/c_client/libcosta_client.so is not built: run __graft_entry__.build()"
+    client = ctypes.CDLL(lib)
+    client.costa_client_gpu.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_char_p),
+                                        ctypes.POINTER(ctypes.c_char_p), ctypes.c_char_p, ctypes.c_double,
+                                        ctypes.c_double]
     A, B, op = CASES[k]
     alpha, beta = (2.0, 0.5) if k != 1 else (1.0, 0.0)
     OA, OB = oracle.OLayout(A), oracle.OLayout(B)
@@ -110,9 +116,9 @@ def test_c_program_transform_matches_oracle(tmp_path, k):
     np.concatenate(hb).tofile(tmp_path / "b.bin")
     np.concatenate(ha).tofile(tmp_path / "a.bin")
     print(f"C client transform case {k}: P={P} op={op}", flush=True)
-    r = subprocess.run([client, "gpu", str(tmp_path), *_args(A), *_args(B), op, repr(alpha), repr(beta)],
-                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
-    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stderr
+    argv = lambda spec: (ctypes.c_char_p * 8)(*[a.encode() for a in _args(spec)])
+    rc = client.costa_client_gpu(str(tmp_path).encode(), argv(A), argv(B), op.encode(), alpha, beta)
+    assert rc == 0
     got = np.fromfile(tmp_path / "out.bin", dtype=np.float64)
     oracle.transform("f64", op, alpha, beta, OA, ha, OB, hb, None)
     exp = np.concatenate(ha)
