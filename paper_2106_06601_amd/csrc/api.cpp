@@ -743,20 +743,24 @@ extern "C" costa_status costa_timing_read(costa_timing* out) {
 
 extern "C" costa_status costa_finalize(void) {
   State& S = state();
-  std::lock_guard<std::mutex> lock(S.mu);
-  if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty()) HIP_OR_FAIL(hipDeviceSynchronize());
-  S.pending.clear();
-  S.plans.clear();
-  S.host_plans.clear();
-  for (auto& kv : S.ws) {
-    if (kv.second.ptr) (void)hipFree(kv.second.ptr);
-    if (kv.second.last_use) (void)hipEventDestroy(kv.second.last_use);
+  {
+    std::lock_guard<std::mutex> lock(S.mu);
+    if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty()) HIP_OR_FAIL(hipDeviceSynchronize());
+    S.pending.clear();
+    S.plans.clear();
+    S.host_plans.clear();
+    for (auto& kv : S.ws) {
+      if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+      if (kv.second.last_use) (void)hipEventDestroy(kv.second.last_use);
+    }
+    S.ws.clear();
+    for (hipEvent_t e : S.event_pool) (void)hipEventDestroy(e);
+    S.event_pool.clear();
+    S.timing = false;
+    S.totals = costa_timing{};
   }
-  S.ws.clear();
-  for (hipEvent_t e : S.event_pool) (void)hipEventDestroy(e);
-  S.event_pool.clear();
-  S.timing = false;
-  S.totals = costa_timing{};
+  // outside the state lock: a ScaLAPACK-style call takes the layout cache's
+  // lock and then the state lock, never the other way round
   release_scalapack_layouts();
   return COSTA_SUCCESS;
 }

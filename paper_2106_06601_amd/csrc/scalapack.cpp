@@ -3,8 +3,10 @@
 // the splits), and the call becomes one transform A <- alpha*op(B) + beta*A
 // (Section 5, eq:costa, which covers pxgemr2d and pxtran).  The layouts are
 // cached by descriptor, grid and window (a block-cyclic layout is a few
-// hundred bytes, whatever the matrix size) until costa_finalize, so that
-// repeated calls keep the same layouts and therefore find their cached plans.
+// hundred bytes, whatever the matrix size), so that repeated calls keep the
+// same layouts and therefore find their cached plans; the cache holds at most
+// kMaxCachedLayouts and starts over when a call would pass that, and
+// costa_finalize empties it.
 #include <map>
 #include <mutex>
 
@@ -17,10 +19,19 @@ namespace {
 // j0, m, n, then the rank map if there is one
 using Key = std::vector<int64_t>;
 
+// A call looks up two layouts; the cache starts over before a call whose two
+// could pass the bound, never between its two lookups.
+constexpr size_t kMaxCachedLayouts = 1024;
+
 struct Cache {
-  std::mutex mu;
+  std::mutex mu;  // held for a whole call: its layouts stay alive until it returns
   std::map<Key, costa_layout> layouts;
 };
+
+void clear_locked(Cache& C) {
+  for (auto& kv : C.layouts) costa_layout_destroy(kv.second);
+  C.layouts.clear();
+}
 
 Cache& cache() {
   static Cache* c = new Cache();
@@ -32,7 +43,8 @@ costa_status check_desc(const char* name, const int32_t* desc, const costa_grid*
   return COSTA_SUCCESS;
 }
 
-// Layout of the rows x cols submatrix at 1-based (i1, j1) of the descriptor's matrix.
+// Layout of the rows x cols submatrix at 1-based (i1, j1) of the descriptor's
+// matrix.  The caller holds the cache's lock.
 costa_status window_layout(const char* name, const int32_t* desc, const costa_grid* grid, int32_t i1, int32_t j1,
                            int64_t rows, int64_t cols, costa_layout* out) {
   costa_status st = check_desc(name, desc, grid);
@@ -45,7 +57,6 @@ costa_status window_layout(const char* name, const int32_t* desc, const costa_gr
           (int64_t)grid->rank_order, grid->nranks, (int64_t)i1 - 1, (int64_t)j1 - 1, rows, cols};
   if (grid->rank_map) key.insert(key.end(), grid->rank_map, grid->rank_map + (size_t)grid->nprow * grid->npcol);
   Cache& C = cache();
-  std::lock_guard<std::mutex> lock(C.mu);
   auto it = C.layouts.find(key);
   if (it != C.layouts.end()) {
     *out = it->second;
@@ -79,6 +90,9 @@ costa_status scalapack_transform(costa_dtype dtype, costa_op op, int32_t m, int3
   if (m == 0 || n == 0) return COSTA_SUCCESS;
   if (!src || !dst) return fail(COSTA_ERROR_INVALID_VALUE, "null buffer array");
   const bool tr = op != COSTA_OP_N;
+  Cache& C = cache();
+  std::lock_guard<std::mutex> lock(C.mu);
+  if (C.layouts.size() + 2 > kMaxCachedLayouts) clear_locked(C);
   costa_layout ls = nullptr, ld = nullptr;
   st = window_layout("the source", descs, grids, is, js, tr ? n : m, tr ? m : n, &ls);
   if (st != COSTA_SUCCESS) return st;
@@ -103,8 +117,7 @@ const void* zero_of(costa_dtype dt) {
 void release_scalapack_layouts() {
   Cache& C = cache();
   std::lock_guard<std::mutex> lock(C.mu);
-  for (auto& kv : C.layouts) costa_layout_destroy(kv.second);
-  C.layouts.clear();
+  clear_locked(C);
 }
 
 }  // namespace costa

@@ -303,3 +303,42 @@ def test_scalapack_between_grids_of_different_sizes(seed):
     k = SLCase(call, seed=seed, null_idle=True)
     k.run()
     k.check_full()
+
+
+def test_many_windows_pass_the_layout_cache_bound():
+    """1156 calls on distinct 8 x 8 windows of two 48 x 48 matrices, about
+    2300 distinct window layouts -- more than the library keeps, so its
+    layout cache starts over during the sequence: the final buffers equal
+    the same window copies applied in order on the host (through the
+    oracle's storage maps), and nothing outside the windows is touched."""
+    import itertools
+    SL = synth.ScaLapack
+    A = SL(48, 48, 5, 7, 0, 1, 27, 2, 2)   # local rows 25 / 23, lld padded to 27
+    Cd = SL(48, 48, 4, 6, 1, 0, 24, 2, 2, rank_order="col")
+    OA, OC = oracle.OLayout(A), oracle.OLayout(Cd)
+    dev = torch.device("cuda:0")
+    s = torch.cuda.current_stream(dev)
+    ha, hc = [], []
+    for q in range(4):
+        a = np.zeros(OA.local_elems(q))
+        oracle.fill("f64", a, 5, synth.stream(synth.ROLE_B, 0, q))
+        ha.append(a)
+        c = np.zeros(OC.local_elems(q))
+        oracle.fill("f64", c, 5, synth.stream(synth.ROLE_A, 0, q))
+        hc.append(c)
+    da = [torch.from_numpy(a).to(dev) for a in ha]
+    dc = [torch.from_numpy(c).to(dev) for c in hc]
+    ii, jj = np.meshgrid(np.arange(8), np.arange(8), indexing="ij")
+    ii, jj = ii.ravel(), jj.ravel()
+    _say("ScaLAPACK-style calls on 1156 distinct windows")
+    for i0, j0 in itertools.product(range(34), range(34)):
+        ic0, jc0 = (i0 * 7) % 41, (j0 * 5) % 41
+        C.costa_pxgemr2d("f64", 8, 8, da, i0 + 1, j0 + 1, A.desc(), _grid(A), dc, ic0 + 1, jc0 + 1, Cd.desc(),
+                         _grid(Cd), stream=s)
+        ra, oa = OA.locate(ii + i0, jj + j0)
+        rc, oc = OC.locate(ii + ic0, jj + jc0)
+        for k in range(ii.size):
+            hc[rc[k]][oc[k]] = ha[ra[k]][oa[k]]
+    torch.cuda.synchronize()
+    for q in range(4):
+        assert np.array_equal(_bits(dc[q].cpu().numpy(), "f64"), _bits(hc[q], "f64")), f"rank {q}"
