@@ -335,9 +335,10 @@ costa_status costa_plan_export(costa_dtype dtype, int32_t n, const costa_transfo
  * submatrix).  Elements land where the destination
  * descriptor puts them (no relabeling); elements outside the destination
  * submatrix are not touched.  m == 0 or n == 0: nothing is enqueued.
- * Asynchronous on `stream`.  The layouts of descriptor + submatrix pairs and
- * the plans are cached (until costa_finalize()), so a repeated call only
- * enqueues kernels.  Errors: those of costa_layout_create_scalapack();
+ * Asynchronous on `stream`.  The layouts of descriptor + submatrix pairs
+ * (up to 1024 of them; past that the cache starts over) and the plans (up to
+ * 32) are cached until costa_finalize(), so a repeated call only enqueues
+ * kernels.  Errors: those of costa_layout_create_scalapack();
  * INVALID_VALUE for negative m/n, indices below 1 or submatrices past the
  * matrix, null pointers; SHAPE_MISMATCH when the grids have different nranks;
  * then those of costa_transform().
