@@ -243,7 +243,11 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePla
     }
     e0 = get_event(S);
     e1 = get_event(S);
-    if (!e0 || !e1) return fail(COSTA_ERROR_DEVICE, "hipEventCreate failed");
+    if (!e0 || !e1) {
+      if (e0) S.event_pool.push_back(e0);
+      if (e1) S.event_pool.push_back(e1);
+      return fail(COSTA_ERROR_DEVICE, "hipEventCreate failed");
+    }
     HIP_OR_FAIL(hipEventRecord(e0, stream));
   }
   LaunchSpec spec{mode, conj, lr.has_transpose};
@@ -746,6 +750,10 @@ extern "C" costa_status costa_finalize(void) {
   {
     std::lock_guard<std::mutex> lock(S.mu);
     if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty()) HIP_OR_FAIL(hipDeviceSynchronize());
+    for (const TimingRec& r : S.pending) {  // recorded but never read: their events go too
+      (void)hipEventDestroy(r.start);
+      (void)hipEventDestroy(r.stop);
+    }
     S.pending.clear();
     S.plans.clear();
     S.host_plans.clear();
