@@ -125,10 +125,7 @@ static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
 // its rows, or a run of small rectangles moved at once.  A launch of row
 // walks also has a wide task table whose tasks are kWideTaskUnits units (a
 // run still one task); launches that copy use it, two units per lane.
-#ifndef COSTA_TASK_LANES
-#define COSTA_TASK_LANES 256  // 128: short row walks +1%, block-size change -1.5%, batch unpack -2%; 64: tiles -21%
-#endif
-constexpr int32_t kThreadsPerTask = COSTA_TASK_LANES;
+constexpr int32_t kThreadsPerTask = 256;
 #ifndef COSTA_COPY_UNITS
 #define COSTA_COPY_UNITS 2  // units per lane in launches of row walks that copy
 #endif
