@@ -57,3 +57,30 @@ def many_rank_cases():
          BC(4096, 4096, 64, 64, 64, 64, "col", "col"), BC(4096, 4096, 96, 32, 64, 64, "row", "col"),
          np.random.default_rng(41).permutation(4096).tolist()),
     ]
+
+
+def short_walk_cases():
+    """Layouts whose transform is all row walks of 4-64 elements that start
+    and end inside 128-byte lines (blocks cut by the other grid's splits):
+    16-byte units and single elements (odd leading dimension), all four
+    element types, every arithmetic mode."""
+    BC = synth.BlockCyclic
+    return [
+        # the scaled transpose's grids at 4000^2
+        synth.Workload("walk0", "f64", [synth.Item(BC(4000, 4000, 100, 100, 4, 8, "row", "row"),
+                                                   BC(4000, 4000, 64, 64, 8, 4, "row", "col"), "T", 2.0, 0.5)],
+                       False, seed=51),
+        # local rows of A 749 elements long (odd): single-element units
+        synth.Workload("walk1", "f64", [synth.Item(BC(3000, 2996, 100, 107, 4, 4, "row", "row"),
+                                                   BC(3000, 2996, 64, 64, 4, 4, "col", "row"), "N", -1.5, 0.0)],
+                       False, seed=52),
+        synth.Workload("walk2", "f32", [synth.Item(BC(3000, 3600, 100, 100, 4, 4, "row", "row"),
+                                                   BC(3600, 3000, 64, 64, 4, 4, "row", "col"), "T", 0.3, 1.0)],
+                       False, seed=53),
+        synth.Workload("walk3", "c128", [synth.Item(BC(2400, 2400, 100, 100, 4, 4, "col", "col"),
+                                                    BC(2400, 2400, 64, 64, 4, 4, "row", "row"), "C",
+                                                    0.5 - 0.25j, 0.25 + 1j)], False, seed=54),
+        synth.Workload("walk4", "c64", [synth.Item(BC(2400, 2400, 100, 100, 4, 4, "row", "row"),
+                                                   BC(2400, 2400, 64, 64, 4, 4, "col", "col"), "T", 1.0, 0.0)],
+                       False, seed=55),
+    ]

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from replay import many_rank_cases
+from replay import many_rank_cases, short_walk_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -291,6 +291,20 @@ def test_transposed_rectangles_around_the_tile_limits(dtype):
 # ---------------------------------------------------------------------------
 # edge cases
 # ---------------------------------------------------------------------------
+@pytest.mark.parametrize("k", range(5))
+def test_short_row_walks_full_compare(k):
+    """Row walks of 4-64 elements starting inside 128-byte lines (16-byte
+    units and single elements, four element types, every arithmetic mode),
+    every element compared."""
+    w = short_walk_cases()[k]
+    sigma = list(range(w.items[0].A.nranks))[::-1] if k == 1 else None
+    it = w.items[0]
+    _say(f"short walks {k}: {w.dtype} {it.A.nrows}x{it.A.ncols} op={it.op} sigma={sigma}")
+    case = Case(w, sigma=sigma)
+    case.run()
+    case.check_full()
+
+
 def test_waves_with_tiny_workspace():
     _say("waves with a 256 KiB workspace")
     try:

@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from replay import _combine, _index, many_rank_cases
+from replay import _combine, _index, many_rank_cases, short_walk_cases
 
 C = pytest.importorskip("paper_2106_06601_amd")
 
@@ -218,6 +218,15 @@ def test_replay_random_layouts(seed):
         else [(1.0, 0.0), (2.0, 0.5), (-1.5, 0.0)][seed % 3]
     w = synth.Workload("r", dtype, [synth.Item(A, B, op, alpha, beta)], False, seed=seed)
     replay(w, sigma=rng.permutation(P).tolist())
+
+
+@pytest.mark.parametrize("k", range(5))
+def test_replay_short_row_walks(k):
+    """Short misaligned row walks in every element type: in bounds, every
+    element of A written once, equal to the oracle."""
+    w = short_walk_cases()[k]
+    pieces, _ = replay(w, sigma=list(range(w.items[0].A.nranks))[::-1] if k == 1 else None)
+    assert not (pieces["flags"] & 1).any(), "the case has transposed rectangles"
 
 
 @pytest.mark.parametrize("k", [0, 1])
