@@ -383,6 +383,45 @@ def test_two_streams_share_the_workspace_safely():
     c2.check_full()
 
 
+def test_host_threads_call_at_once():
+    """Eight host threads call the library at the same moment (the binding
+    releases the interpreter lock during each call), each with its own stream
+    and buffers: four different plans, and one plan that four of the threads
+    share (its first call builds it while the others wait on the library's
+    lock).  Every element of every result compared."""
+    import threading
+    cases = []
+    for name in ("reshuffle_transpose_1k", "blocksize_change_16k", "scaled_transpose_20k", "cosma_complex_16k"):
+        with torch.cuda.stream(torch.cuda.Stream()):
+            cases.append(Case(synth.workload(name, "small")))
+    shared = synth.workload("rpa_batched_tall_skinny", "small")
+    for _ in range(4):
+        with torch.cuda.stream(torch.cuda.Stream()):
+            cases.append(Case(shared))
+    torch.cuda.synchronize()
+    start = threading.Barrier(len(cases))
+    errors = []
+
+    def call(c):
+        try:
+            start.wait(timeout=60)
+            c.run()
+        except Exception as e:  # reported after the join
+            errors.append(e)
+
+    _say(f"{len(cases)} host threads call the library at once")
+    threads = [threading.Thread(target=call, args=(c,)) for c in cases]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a call did not return"
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for c in cases:
+        c.check_full()
+
+
 @pytest.mark.parametrize("kind", ["messages", "direct_only"])
 def test_one_plan_two_streams_different_buffers(kind):
     """Two calls of one cached plan with different buffers, on two streams,
