@@ -432,7 +432,8 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
   hp.pieces_direct = (int32_t)direct.size();
 
   // messages: packages ordered by sender, then receiver (each sender's send
-  // buffer holds one contiguous package per receiver); blocks in source order
+  // buffer holds one contiguous package per receiver; plans of several waves
+  // reorder them by receiver below); blocks in source order
   auto by_package = [](const Cand& a, const Cand& b) {
     if (a.s != b.s) return a.s < b.s;
     if (a.r != b.r) return a.r < b.r;
@@ -458,6 +459,22 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     for (const Cand& c : remote) biggest = std::max(biggest, chunk_bytes(c.p));
   }
   cap = std::max(cap, biggest);
+  if (total_msg > cap) {
+    // Several waves: packages ordered by receiver, then sender, so that each
+    // wave holds every package of a range of receivers and the rectangles
+    // that border one another in A (from different senders) are unpacked by
+    // the same launch.  Cut by sender instead, neighbours land in different
+    // waves and the lines they share are read and written once per wave
+    // (measured on MI355X, the scaled transpose with a 1 GiB workspace, 3
+    // waves: 3.63 ms by sender, 2.85 by receiver; the tall-skinny batch's 7
+    // waves: equal).
+    std::sort(remote.begin(), remote.end(), [](const Cand& a, const Cand& b) {
+      if (a.r != b.r) return a.r < b.r;
+      if (a.s != b.s) return a.s < b.s;
+      if (a.p.src_buf != b.p.src_buf) return a.p.src_buf < b.p.src_buf;
+      return a.p.src_off < b.p.src_off;
+    });
+  }
 
   const int32_t msg_buf = 2 * n * (items.empty() ? 0 : items[0].A->nranks);
   size_t k = 0;

@@ -309,7 +309,7 @@ def test_waves_with_tiny_workspace():
     _say("waves with a 256 KiB workspace")
     try:
         C.costa_set_workspace_limit(256 << 10)
-        for name in ("blocksize_change_16k", "rpa_batched_tall_skinny", "cosma_complex_16k"):
+        for name in ("blocksize_change_16k", "rpa_batched_tall_skinny", "cosma_complex_16k", "scaled_transpose_20k"):
             w = synth.workload(name, "small")
             descs = [dict(op=it.op, alpha=it.alpha, beta=it.beta, A=C.layout_from_spec(it.A),
                           B=C.layout_from_spec(it.B)) for it in w.items]
