@@ -186,12 +186,31 @@ def test_replay_small_workloads(name):
     replay(w, sigma)
 
 
+def _waves_follow_receivers(pieces, P):
+    """Plans of several waves take the packages receiver by receiver: the
+    receivers of a wave's unpack rectangles (message sources) never come
+    before those of the previous wave."""
+    msg = pieces[(pieces["kind"] == UNPACK) & (pieces["src_buf"] == pieces["src_buf"].max())]
+    last = -1
+    for wv in np.unique(msg["wave"]):
+        recv = msg["dst_buf"][msg["wave"] == wv] % P
+        assert recv.min() >= last, "a wave takes packages of an earlier receiver"
+        last = recv.max()
+
+
 def test_replay_with_waves_and_relabeling():
     w = synth.workload("blocksize_change_16k", "small")
     pieces, stats = replay(w, sigma=[3, 1, 0, 2, 5, 4, 7, 6, 9, 8, 11, 10, 15, 12, 14, 13], limit=200 << 10)
     assert stats["waves"] > 10
+    _waves_follow_receivers(pieces, 16)
     w = synth.workload("cosma_complex_16k", "small")
-    replay(w, limit=1 << 20)
+    pieces, stats = replay(w, limit=1 << 20)
+    assert stats["waves"] > 1
+    _waves_follow_receivers(pieces, 64)
+    w = synth.workload("scaled_transpose_20k", "small")
+    pieces, stats = replay(w, limit=4 << 20)
+    assert stats["waves"] > 1
+    _waves_follow_receivers(pieces, 32)
 
 
 @pytest.mark.parametrize("seed", range(12))
