@@ -18,6 +18,7 @@
 #include <chrono>
 #include <new>
 #include <numeric>
+#include <tuple>
 
 #include "plan.hpp"
 
@@ -63,11 +64,50 @@ inline bool same_kind(const Piece& a, const Piece& b) {
 }
 
 // All overlay rectangles of one pair, merged; appended to `local` / `remote`.
+// Owner, leading dimension and local offset of a layout's blocks, with the
+// per-block-row and per-block-column parts of a block-cyclic layout (process
+// row or column and local start; ScaLAPACK INDXG2P / INDXG2L) taken once per
+// row and column instead of once per block.
+struct BlockMap {
+  const Layout& L;
+  std::vector<int32_t> prow, pcol;
+  std::vector<int64_t> li, lj;
+  explicit BlockMap(const Layout& l) : L(l) {
+    if (!L.block_cyclic) return;
+    prow.resize(L.nbr);
+    li.resize(L.nbr);
+    for (int32_t bi = 0; bi < L.nbr; ++bi) {
+      prow[bi] = L.prow_of(bi);
+      li[bi] = ((L.rb0 + bi) / L.prow) * L.mb + (L.r0 + L.rsplit[bi]) % L.mb;
+    }
+    pcol.resize(L.nbc);
+    lj.resize(L.nbc);
+    for (int32_t bj = 0; bj < L.nbc; ++bj) {
+      pcol[bj] = L.pcol_of(bj);
+      lj[bj] = ((L.cb0 + bj) / L.pcol) * L.nb + (L.c0 + L.csplit[bj]) % L.nb;
+    }
+  }
+  int32_t owner(int32_t bi, int32_t bj) const {
+    return L.block_cyclic ? L.rank_at(prow[bi], pcol[bj]) : L.owner[L.block(bi, bj)];
+  }
+  int64_t ld(int32_t bi, int32_t bj) const {
+    if (!L.block_cyclic) return L.bld[L.block(bi, bj)];
+    if (L.lld) return L.lld;
+    const int64_t ext = L.order == COSTA_COL_MAJOR ? L.lrows[prow[bi]] : L.lcols[pcol[bj]];
+    return ext > 1 ? ext : 1;
+  }
+  int64_t offset(int32_t bi, int32_t bj, int64_t ld_) const {
+    if (!L.block_cyclic) return L.boff[L.block(bi, bj)];
+    return L.order == COSTA_COL_MAJOR ? li[bi] + lj[bj] * ld_ : li[bi] * ld_ + lj[bj];
+  }
+};
+
 void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vector<int32_t>& sigma,
                std::vector<Cand>& local, std::vector<Cand>& remote, int64_t& overlay_blocks, int64_t& n_local,
                int64_t& n_remote) {
   const Layout& A = *d.A;
   const Layout& B = *d.B;
+  const BlockMap MA(A), MB(B);
   const bool tr = d.op != COSTA_OP_N;
   const int32_t P = A.nranks;
   // op(B) seen in A's coordinates: its row splits are B's column splits for T/C
@@ -92,20 +132,20 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
       const Interval& ri = a_col ? xi : yi;  // row interval of this overlay block
       const Interval& ci = a_col ? yi : xi;  // column interval
       // destination block and label
-      const int32_t t = A.owner_of(ri.a, ci.a);
+      const int32_t t = MA.owner(ri.a, ci.a);
       const int32_t r = sigma.empty() ? t : sigma[t];
       const int64_t pi = ri.start - A.rsplit[ri.a], pj = ci.start - A.csplit[ci.a];
-      const int64_t lda = A.ld_of(ri.a, ci.a);
-      const int64_t dst_off = A.offset_of(ri.a, ci.a) + (a_col ? pi + pj * lda : pi * lda + pj);
+      const int64_t lda = MA.ld(ri.a, ci.a);
+      const int64_t dst_off = MA.offset(ri.a, ci.a, lda) + (a_col ? pi + pj * lda : pi * lda + pj);
       // source block: op(B) block (ri.b, ci.b) is B block (ci.b, ri.b) for T/C
       const int32_t bi = tr ? ci.b : ri.b, bj = tr ? ri.b : ci.b;
-      const int32_t s = B.owner_of(bi, bj);
-      const int64_t ldb = B.ld_of(bi, bj);
+      const int32_t s = MB.owner(bi, bj);
+      const int64_t ldb = MB.ld(bi, bj);
       // B element of A's (i, j): B(i, j) for N, B(j, i) for T/C
       const int64_t qrow = tr ? ci.start - B.rsplit[bi] : ri.start - B.rsplit[bi];
       const int64_t qcol = tr ? ri.start - B.csplit[bj] : ci.start - B.csplit[bj];
       const int64_t s_brow = b_col ? 1 : ldb, s_bcol = b_col ? ldb : 1;  // strides of B's row / col index
-      const int64_t src_off = B.offset_of(bi, bj) + qrow * s_brow + qcol * s_bcol;
+      const int64_t src_off = MB.offset(bi, bj, ldb) + qrow * s_brow + qcol * s_bcol;
       const int64_t s_i = tr ? s_bcol : s_brow;  // stride along A's row index i
       const int64_t s_j = tr ? s_brow : s_bcol;  // stride along A's column index j
       const int64_t sx = a_col ? s_i : s_j, sy = a_col ? s_j : s_i;
@@ -385,7 +425,9 @@ std::vector<LaunchRange> add_launches(HostPlan& hp, std::vector<Piece>& ps, int 
   std::vector<LaunchRange> out;
   if (ps.empty()) return out;
   std::vector<Piece> tiles, walks;
-  if (COSTA_SPLIT_KINDS) {
+  size_t ntiles = 0;
+  for (const Piece& p : ps) ntiles += (p.flags & PIECE_TRANSPOSE) ? 1 : 0;
+  if (COSTA_SPLIT_KINDS && ntiles > 0 && ntiles < ps.size()) {
     for (const Piece& p : ps) ((p.flags & PIECE_TRANSPOSE) ? tiles : walks).push_back(p);
   }
   if (tiles.empty() || walks.empty()) {
@@ -397,10 +439,25 @@ std::vector<LaunchRange> add_launches(HostPlan& hp, std::vector<Piece>& ps, int 
   return out;
 }
 
-bool by_dst(const Piece& a, const Piece& b) {
-  if (a.dst_buf != b.dst_buf) return a.dst_buf < b.dst_buf;
-  return a.dst_off < b.dst_off;
+// Sorts v by key(element) through an array of (key, index) pairs instead of
+// moving the elements around.  Every key used below is unique (each element
+// of A and of B lies in exactly one rectangle), so the order is the one a
+// sort of the elements themselves gives.
+template <typename T, typename KeyFn>
+void sort_by_key(std::vector<T>& v, KeyFn key) {
+  using K = decltype(key(v[0]));
+  if (v.size() > (size_t)UINT32_MAX) throw std::bad_alloc();
+  std::vector<std::pair<K, uint32_t>> ix(v.size());
+  for (size_t i = 0; i < v.size(); ++i) ix[i] = {key(v[i]), (uint32_t)i};
+  std::sort(ix.begin(), ix.end());
+  std::vector<T> out;
+  out.reserve(v.size());
+  for (const auto& e : ix) out.push_back(std::move(v[e.second]));
+  v.swap(out);
 }
+
+std::pair<int32_t, int64_t> dst_key(const Piece& p) { return {p.dst_buf, p.dst_off}; }
+std::pair<int32_t, int64_t> src_key(const Piece& p) { return {p.src_buf, p.src_off}; }
 
 }  // namespace
 
@@ -428,19 +485,14 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     finish_piece(c.p, es);
     direct.push_back(c.p);
   }
-  std::sort(direct.begin(), direct.end(), by_dst);
+  sort_by_key(direct, dst_key);
   hp.pieces_direct = (int32_t)direct.size();
 
   // messages: packages ordered by sender, then receiver (each sender's send
   // buffer holds one contiguous package per receiver; plans of several waves
   // reorder them by receiver below); blocks in source order
-  auto by_package = [](const Cand& a, const Cand& b) {
-    if (a.s != b.s) return a.s < b.s;
-    if (a.r != b.r) return a.r < b.r;
-    if (a.p.src_buf != b.p.src_buf) return a.p.src_buf < b.p.src_buf;
-    return a.p.src_off < b.p.src_off;
-  };
-  std::sort(remote.begin(), remote.end(), by_package);
+  auto by_package = [](const Cand& c) { return std::make_tuple(c.s, c.r, c.p.src_buf, c.p.src_off); };
+  sort_by_key(remote, by_package);
   auto chunk_bytes = [&](const Piece& p) {
     int64_t b = (int64_t)p.nx * p.ny * es;
     return (b + 255) / 256 * 256;  // every message block starts 256-byte aligned
@@ -454,7 +506,7 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
   if (biggest > cap) {
     // a small workspace: cut the blocks so that each fits one wave
     split_pieces(remote, std::max<int64_t>(1, (cap - 255) / es));
-    std::sort(remote.begin(), remote.end(), by_package);
+    sort_by_key(remote, by_package);
     biggest = 0;
     for (const Cand& c : remote) biggest = std::max(biggest, chunk_bytes(c.p));
   }
@@ -468,12 +520,7 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     // (measured on MI355X, the scaled transpose with a 1 GiB workspace, 3
     // waves: 3.63 ms by sender, 2.85 by receiver; the tall-skinny batch's 7
     // waves: equal).
-    std::sort(remote.begin(), remote.end(), [](const Cand& a, const Cand& b) {
-      if (a.r != b.r) return a.r < b.r;
-      if (a.s != b.s) return a.s < b.s;
-      if (a.p.src_buf != b.p.src_buf) return a.p.src_buf < b.p.src_buf;
-      return a.p.src_off < b.p.src_off;
-    });
+    sort_by_key(remote, [](const Cand& c) { return std::make_tuple(c.r, c.s, c.p.src_buf, c.p.src_off); });
   }
 
   const int32_t msg_buf = 2 * n * (items.empty() ? 0 : items[0].A->nranks);
@@ -517,11 +564,7 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
       const int64_t a = pk.src_off * es % 128, e = (pk.src_off + pk.nx) * es % 128;
       if (a != 0 || e != 0 || (pk.ny > 1 && pk.src_ld * es % 128 != 0)) ++partial;
     }
-    if (COSTA_PACK_BY_SOURCE && 4 * partial > (int64_t)pack.size())
-      std::sort(pack.begin(), pack.end(), [](const Piece& a, const Piece& b) {
-        if (a.src_buf != b.src_buf) return a.src_buf < b.src_buf;
-        return a.src_off < b.src_off;
-      });
+    if (COSTA_PACK_BY_SOURCE && 4 * partial > (int64_t)pack.size()) sort_by_key(pack, src_key);
     hp.pieces_pack += (int32_t)pack.size();
     hp.pieces_unpack += (int32_t)unpack.size();
     const bool last = k == remote.size();
@@ -532,7 +575,7 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
       unpack.insert(unpack.end(), direct.begin(), direct.end());
       direct.clear();
     }
-    std::sort(unpack.begin(), unpack.end(), by_dst);
+    sort_by_key(unpack, dst_key);
     Wave w;
     w.msg_bytes = off;
     w.pack = add_launch(hp, pack, es, n);
