@@ -230,13 +230,21 @@ costa_status collect_timing(State& S) {
   return COSTA_SUCCESS;
 }
 
-// Launches one mover range, bracketed by timing events when enabled.
-costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePlan& dp, const LaunchRange& lr,
+// Device copies of a plan's tables (rectangles, task tables, wide task tables).
+struct DeviceTables {
+  const Piece* pieces;
+  const int32_t* tasks;
+  const int32_t* wide;
+};
+
+// Launches one mover range, bracketed by timing events when enabled (and
+// `timed`).
+costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DeviceTables& dt_, const LaunchRange& lr,
                        int32_t mode, int32_t conj, void* const* d_bufs, const ItemParam* d_items, int32_t allow_wide,
-                       int64_t bytes, hipStream_t stream) {
+                       int64_t bytes, hipStream_t stream, bool timed = true) {
   if (lr.ntasks == 0) return COSTA_SUCCESS;
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (S.timing) {
+  if (S.timing && timed) {
     if (S.pending.size() > 4096) {
       costa_status st = collect_timing(S);
       if (st != COSTA_SUCCESS) return st;
@@ -251,10 +259,10 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DevicePla
     HIP_OR_FAIL(hipEventRecord(e0, stream));
   }
   LaunchSpec spec{mode, conj, lr.has_transpose};
-  HIP_OR_FAIL(launch_mover(kind, dt, spec, dp.d_pieces, dp.d_tasks + lr.task_begin, lr.ntasks,
-                           lr.nwide ? dp.d_wide + lr.wide_begin : nullptr, lr.nwide, d_bufs, d_items, allow_wide,
+  HIP_OR_FAIL(launch_mover(kind, dt, spec, dt_.pieces, dt_.tasks + lr.task_begin, lr.ntasks,
+                           lr.nwide ? dt_.wide + lr.wide_begin : nullptr, lr.nwide, d_bufs, d_items, allow_wide,
                            lr.xcd_ranges, stream));
-  if (S.timing) {
+  if (e1) {
     HIP_OR_FAIL(hipEventRecord(e1, stream));
     costa_kernel_kind kk = kind == KIND_PACK ? COSTA_KERNEL_PACK
                            : kind == KIND_UNPACK ? COSTA_KERNEL_UNPACK
@@ -355,6 +363,72 @@ costa_status get_plan(State& S, costa_dtype dt, const std::vector<ItemDesc>& ite
   return COSTA_SUCCESS;
 }
 
+// The table a call's kernels read: the buffer pointers (A of pair k, rank r
+// at k*P + r; B at n*P + k*P + s; the message workspace at 2*n*P), padded to
+// 64 bytes, then one ItemParam per pair.  Returns the pointers' byte size;
+// reads_a[k]: pair k reads A (beta != 0); aligned: every buffer 16-byte
+// aligned.
+size_t call_table(costa_dtype dt, int32_t n, const costa_transform_desc* desc, int32_t P, void* messages,
+                  std::vector<unsigned char>& table, std::vector<char>& reads_a, bool& aligned) {
+  const size_t nbufs = (size_t)2 * n * P + 1;
+  const size_t ptr_bytes = (nbufs * sizeof(void*) + 63) / 64 * 64;
+  table.assign(ptr_bytes + (size_t)n * sizeof(ItemParam), 0);
+  void** bp = reinterpret_cast<void**>(table.data());
+  aligned = true;
+  auto note = [&](const void* p) { aligned = aligned && ((uintptr_t)p % 16 == 0); };
+  for (int32_t k = 0; k < n; ++k)
+    for (int32_t r = 0; r < P; ++r) {
+      bp[(size_t)k * P + r] = desc[k].A_local[r];
+      bp[(size_t)n * P + (size_t)k * P + r] = const_cast<void*>(desc[k].B_local[r]);
+      note(desc[k].A_local[r]);
+      note(desc[k].B_local[r]);
+    }
+  bp[(size_t)2 * n * P] = messages;
+  ItemParam* ipar = reinterpret_cast<ItemParam*>(table.data() + ptr_bytes);
+  reads_a.assign(n, 0);
+  for (int32_t k = 0; k < n; ++k) {
+    ItemParam& q = ipar[k];
+    to_pair(dt, desc[k].alpha, q.alpha);
+    to_pair(dt, desc[k].beta, q.beta);
+    const bool bz = is_zero(dt, desc[k].beta);
+    q.mode = bz ? (is_one(dt, desc[k].alpha) ? MODE_COPY : MODE_SCALE) : MODE_AXPBY;
+    q.conj = (desc[k].op == COSTA_OP_C && is_complex(dt)) ? 1 : 0;
+    reads_a[k] = !bz;
+  }
+  return ptr_bytes;
+}
+
+// Enqueues every launch of a plan: the direct path (when not merged), then
+// pack and unpack-transform of each wave.
+costa_status launch_plan(State& S, costa_dtype dt, const HostPlan& hp, const DeviceTables& tabs,
+                         const ItemParam* ipar, int32_t n, const std::vector<char>& reads_a, bool aligned,
+                         void* const* d_bufs, const ItemParam* d_items, hipStream_t stream, bool timed) {
+  const int es = elem_size(dt);
+  const int32_t wide = aligned ? 1 : 0;
+  // one arithmetic mode for the whole call when every pair agrees
+  int32_t mode = ipar[0].mode, conj = ipar[0].conj;
+  for (int32_t k = 1; k < n; ++k)
+    if (ipar[k].mode != mode || ipar[k].conj != conj) mode = -1;
+  costa_status st;
+  for (const LaunchRange& lr : hp.direct) {
+    st = run_range(S, KIND_DIRECT, dt, tabs, lr, mode, conj, d_bufs, d_items, wide, range_bytes(lr, es, reads_a),
+                   stream, timed);
+    if (st != COSTA_SUCCESS) return st;
+  }
+  std::vector<char> no_read(n, 0);
+  for (const Wave& w : hp.waves) {
+    st = run_range(S, KIND_PACK, dt, tabs, w.pack, MODE_COPY, 0, d_bufs, d_items, wide,
+                   range_bytes(w.pack, es, no_read), stream, timed);
+    if (st != COSTA_SUCCESS) return st;
+    for (const LaunchRange& lr : w.unpack) {
+      st = run_range(S, KIND_UNPACK, dt, tabs, lr, mode, conj, d_bufs, d_items, wide, range_bytes(lr, es, reads_a),
+                     stream, timed);
+      if (st != COSTA_SUCCESS) return st;
+    }
+  }
+  return COSTA_SUCCESS;
+}
+
 costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_desc* desc, const int32_t* sigma,
                             hipStream_t stream) {
   State& S = state();
@@ -370,38 +444,16 @@ costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_des
   st = get_plan(S, dt, items, sig, dp);
   if (st != COSTA_SUCCESS) return st;
   const HostPlan& hp = dp->host;
-  const int es = elem_size(dt);
   const int32_t P = items[0].A->nranks;
 
   Workspace* ws = nullptr;
   st = ensure_workspace(S, dp->device, (size_t)hp.workspace_bytes, ws);
   if (st != COSTA_SUCCESS) return st;
 
-  // call table: buffer pointers, then pair parameters
-  std::vector<unsigned char> table(dp->table_bytes, 0);
-  void** bp = reinterpret_cast<void**>(table.data());
+  std::vector<unsigned char> table;
+  std::vector<char> reads_a;
   bool aligned = true;
-  auto note = [&](const void* p) { aligned = aligned && ((uintptr_t)p % 16 == 0); };
-  for (int32_t k = 0; k < n; ++k)
-    for (int32_t r = 0; r < P; ++r) {
-      bp[(size_t)k * P + r] = desc[k].A_local[r];
-      bp[(size_t)n * P + (size_t)k * P + r] = const_cast<void*>(desc[k].B_local[r]);
-      note(desc[k].A_local[r]);
-      note(desc[k].B_local[r]);
-    }
-  bp[(size_t)2 * n * P] = ws->ptr;
-  size_t ptr_bytes = (dp->nbufs * sizeof(void*) + 63) / 64 * 64;
-  ItemParam* ipar = reinterpret_cast<ItemParam*>(table.data() + ptr_bytes);
-  std::vector<char> reads_a(n, 0);
-  for (int32_t k = 0; k < n; ++k) {
-    ItemParam& q = ipar[k];
-    to_pair(dt, desc[k].alpha, q.alpha);
-    to_pair(dt, desc[k].beta, q.beta);
-    const bool bz = is_zero(dt, desc[k].beta);
-    q.mode = bz ? (is_one(dt, desc[k].alpha) ? MODE_COPY : MODE_SCALE) : MODE_AXPBY;
-    q.conj = (desc[k].op == COSTA_OP_C && is_complex(dt)) ? 1 : 0;
-    reads_a[k] = !bz;
-  }
+  const size_t ptr_bytes = call_table(dt, n, desc, P, ws->ptr, table, reads_a, aligned);
   if (table != dp->last_table) {
     // the kernels of the plan's last call read the table until they end: on
     // another stream, the new table is written only after them
@@ -418,27 +470,10 @@ costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_des
 
   void* const* d_bufs = reinterpret_cast<void* const*>(dp->d_table);
   const ItemParam* d_items = reinterpret_cast<const ItemParam*>((unsigned char*)dp->d_table + ptr_bytes);
-  const int32_t wide = aligned ? 1 : 0;
-  // one arithmetic mode for the whole call when every pair agrees
-  int32_t mode = ipar[0].mode, conj = ipar[0].conj;
-  for (int32_t k = 1; k < n; ++k)
-    if (ipar[k].mode != mode || ipar[k].conj != conj) mode = -1;
-  for (const LaunchRange& lr : hp.direct) {
-    st = run_range(S, KIND_DIRECT, dt, *dp, lr, mode, conj, d_bufs, d_items, wide, range_bytes(lr, es, reads_a),
-                   stream);
-    if (st != COSTA_SUCCESS) return st;
-  }
-  std::vector<char> no_read(n, 0);
-  for (const Wave& w : hp.waves) {
-    st = run_range(S, KIND_PACK, dt, *dp, w.pack, MODE_COPY, 0, d_bufs, d_items, wide,
-                   range_bytes(w.pack, es, no_read), stream);
-    if (st != COSTA_SUCCESS) return st;
-    for (const LaunchRange& lr : w.unpack) {
-      st = run_range(S, KIND_UNPACK, dt, *dp, lr, mode, conj, d_bufs, d_items, wide, range_bytes(lr, es, reads_a),
-                     stream);
-      if (st != COSTA_SUCCESS) return st;
-    }
-  }
+  const ItemParam* ipar = reinterpret_cast<const ItemParam*>(dp->last_table.data() + ptr_bytes);
+  st = launch_plan(S, dt, hp, DeviceTables{dp->d_pieces, dp->d_tasks, dp->d_wide}, ipar, n, reads_a, aligned,
+                   d_bufs, d_items, stream, true);
+  if (st != COSTA_SUCCESS) return st;
   if (ws->last_use) {
     HIP_OR_FAIL(hipEventRecord(ws->last_use, stream));
     ws->last_stream = stream;
@@ -458,20 +493,26 @@ using namespace costa;
 extern "C" costa_status costa_transform(costa_dtype dtype, costa_op op, const void* alpha, const void* beta,
                                         costa_layout A, void* const* A_local, costa_layout B,
                                         const void* const* B_local, const int32_t* sigma, hipStream_t stream) {
-  costa_transform_desc d{op, alpha, beta, A, A_local, B, B_local};
-  return transform_impl(dtype, 1, &d, sigma, stream);
+  return guarded([&]() -> costa_status {
+    costa_transform_desc d{op, alpha, beta, A, A_local, B, B_local};
+    return transform_impl(dtype, 1, &d, sigma, stream);
+  });
 }
 
 extern "C" costa_status costa_transform_batched(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
                                                 const int32_t* sigma, hipStream_t stream) {
-  return transform_impl(dtype, n, desc, sigma, stream);
+  return guarded([&]() -> costa_status {
+    return transform_impl(dtype, n, desc, sigma, stream);
+  });
 }
 
 extern "C" costa_status costa_set_workspace_limit(size_t bytes) {
-  State& S = state();
-  std::lock_guard<std::mutex> lock(S.mu);
-  S.workspace_limit = bytes;
-  return COSTA_SUCCESS;
+  return guarded([&]() -> costa_status {
+    State& S = state();
+    std::lock_guard<std::mutex> lock(S.mu);
+    S.workspace_limit = bytes;
+    return COSTA_SUCCESS;
+  });
 }
 
 // Host-only plan (no device): the workspace cap is the user limit, else unlimited.
@@ -506,99 +547,103 @@ costa_status host_plan(costa_dtype dtype, int32_t n, const costa_transform_desc*
 extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
                                           const int32_t* sigma, costa_piece_info* out, int64_t capacity,
                                           int64_t* count) {
-  if (!count || capacity < 0 || (capacity > 0 && !out)) return fail(COSTA_ERROR_INVALID_VALUE, "bad output array");
-  State& S = state();
-  std::lock_guard<std::mutex> lock(S.mu);
-  const HostPlan* hp = nullptr;
-  costa_status st = host_plan(dtype, n, desc, sigma, hp);
-  if (st != COSTA_SUCCESS) return st;
-  int64_t k = 0;
-  int32_t launch = 0;
-  auto emit = [&](const LaunchRange& lr, costa_kernel_kind kind, int32_t wave) {
-    for (int64_t i = 0; i < lr.npieces; ++i, ++k) {
-      if (k >= capacity) continue;
-      const Piece& q = hp->pieces[lr.piece_begin + i];
-      // workgroups that move it: from task0 up to the next rectangle's first
-      // one (or the launch's end); 1 for a rectangle that shares a workgroup
-      int64_t end = lr.ntasks;
-      for (int64_t j = i + 1; j < lr.npieces; ++j)
-        if (hp->pieces[lr.piece_begin + j].task0 != q.task0) {
-          end = hp->pieces[lr.piece_begin + j].task0;
-          break;
-        }
-      costa_piece_info& o = out[k];
-      o.kind = kind;
-      o.wave = wave;
-      o.group = q.task0;
-      o.src_off = q.src_off;
-      o.dst_off = q.dst_off;
-      o.src_ld = q.src_ld;
-      o.dst_ld = q.dst_ld;
-      o.src_buf = q.src_buf;
-      o.dst_buf = q.dst_buf;
-      o.nx = q.nx;
-      o.ny = q.ny;
-      o.item = q.item;
-      o.flags = q.flags;
-      o.ntasks = end - q.task0;
-      const bool T = q.flags & PIECE_TRANSPOSE;
-      o.tile_x = T ? tile_x_of(q.aux) : 0;
-      o.tile_y = T ? tile_y_of(q.aux) : 0;
-      // its first task and task count in the wide table (launches without tiles)
-      o.wide_group = lr.nwide ? q.aux : -1;
-      int64_t wend = lr.nwide;
-      for (int64_t j = i + 1; lr.nwide && j < lr.npieces; ++j)
-        if (hp->pieces[lr.piece_begin + j].aux != q.aux) {
-          wend = hp->pieces[lr.piece_begin + j].aux;
-          break;
-        }
-      o.wide_ntasks = lr.nwide ? wend - q.aux : 0;
-      o.launch = launch;
-      o.reserved = 0;
+  return guarded([&]() -> costa_status {
+    if (!count || capacity < 0 || (capacity > 0 && !out)) return fail(COSTA_ERROR_INVALID_VALUE, "bad output array");
+    State& S = state();
+    std::lock_guard<std::mutex> lock(S.mu);
+    const HostPlan* hp = nullptr;
+    costa_status st = host_plan(dtype, n, desc, sigma, hp);
+    if (st != COSTA_SUCCESS) return st;
+    int64_t k = 0;
+    int32_t launch = 0;
+    auto emit = [&](const LaunchRange& lr, costa_kernel_kind kind, int32_t wave) {
+      for (int64_t i = 0; i < lr.npieces; ++i, ++k) {
+        if (k >= capacity) continue;
+        const Piece& q = hp->pieces[lr.piece_begin + i];
+        // workgroups that move it: from task0 up to the next rectangle's first
+        // one (or the launch's end); 1 for a rectangle that shares a workgroup
+        int64_t end = lr.ntasks;
+        for (int64_t j = i + 1; j < lr.npieces; ++j)
+          if (hp->pieces[lr.piece_begin + j].task0 != q.task0) {
+            end = hp->pieces[lr.piece_begin + j].task0;
+            break;
+          }
+        costa_piece_info& o = out[k];
+        o.kind = kind;
+        o.wave = wave;
+        o.group = q.task0;
+        o.src_off = q.src_off;
+        o.dst_off = q.dst_off;
+        o.src_ld = q.src_ld;
+        o.dst_ld = q.dst_ld;
+        o.src_buf = q.src_buf;
+        o.dst_buf = q.dst_buf;
+        o.nx = q.nx;
+        o.ny = q.ny;
+        o.item = q.item;
+        o.flags = q.flags;
+        o.ntasks = end - q.task0;
+        const bool T = q.flags & PIECE_TRANSPOSE;
+        o.tile_x = T ? tile_x_of(q.aux) : 0;
+        o.tile_y = T ? tile_y_of(q.aux) : 0;
+        // its first task and task count in the wide table (launches without tiles)
+        o.wide_group = lr.nwide ? q.aux : -1;
+        int64_t wend = lr.nwide;
+        for (int64_t j = i + 1; lr.nwide && j < lr.npieces; ++j)
+          if (hp->pieces[lr.piece_begin + j].aux != q.aux) {
+            wend = hp->pieces[lr.piece_begin + j].aux;
+            break;
+          }
+        o.wide_ntasks = lr.nwide ? wend - q.aux : 0;
+        o.launch = launch;
+        o.reserved = 0;
 
+      }
+      ++launch;
+    };
+    for (const LaunchRange& lr : hp->direct) emit(lr, COSTA_KERNEL_DIRECT, 0);
+    for (size_t w = 0; w < hp->waves.size(); ++w) {
+      emit(hp->waves[w].pack, COSTA_KERNEL_PACK, (int32_t)w);
+      for (const LaunchRange& lr : hp->waves[w].unpack) emit(lr, COSTA_KERNEL_UNPACK, (int32_t)w);
     }
-    ++launch;
-  };
-  for (const LaunchRange& lr : hp->direct) emit(lr, COSTA_KERNEL_DIRECT, 0);
-  for (size_t w = 0; w < hp->waves.size(); ++w) {
-    emit(hp->waves[w].pack, COSTA_KERNEL_PACK, (int32_t)w);
-    for (const LaunchRange& lr : hp->waves[w].unpack) emit(lr, COSTA_KERNEL_UNPACK, (int32_t)w);
-  }
-  *count = k;
-  return COSTA_SUCCESS;
+    *count = k;
+    return COSTA_SUCCESS;
+  });
 }
 
 extern "C" costa_status costa_plan_stats(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
                                          const int32_t* sigma, costa_stats* out) {
-  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output");
-  State& S = state();
-  std::lock_guard<std::mutex> lock(S.mu);
-  const HostPlan* hpp = nullptr;
-  costa_status st = host_plan(dtype, n, desc, sigma, hpp);
-  if (st != COSTA_SUCCESS) return st;
-  const HostPlan& hp = *hpp;
-  const int es = elem_size(dtype);
-  costa_stats s{};
-  s.overlay_blocks = hp.overlay_blocks;
-  for (int32_t k = 0; k < n; ++k) {
-    bool reads_a = !(desc[k].beta && is_zero(dtype, desc[k].beta));
-    s.total_elems += hp.item_total[k];
-    s.local_elems += hp.item_local[k];
-    s.remote_elems += hp.item_remote[k];
-    s.model_bytes += (int64_t)es * (hp.item_total[k] * (2 + (reads_a ? 1 : 0)) + 2 * hp.item_remote[k]);
-    s.pack_bytes += (int64_t)es * 2 * hp.item_remote[k];
-    s.unpack_bytes += (int64_t)es * hp.item_remote[k] * (2 + (reads_a ? 1 : 0));
-    s.direct_bytes += (int64_t)es * hp.item_local[k] * (2 + (reads_a ? 1 : 0));
-  }
-  s.message_bytes = (int64_t)es * s.remote_elems;
-  s.workspace_bytes = hp.workspace_bytes;
-  s.waves = (int32_t)hp.waves.size();
-  s.pieces_pack = hp.pieces_pack;
-  s.pieces_unpack = hp.pieces_unpack;
-  s.pieces_direct = hp.pieces_direct;
-  s.plan_ms = hp.plan_ms;
-  *out = s;
-  return COSTA_SUCCESS;
+  return guarded([&]() -> costa_status {
+    if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output");
+    State& S = state();
+    std::lock_guard<std::mutex> lock(S.mu);
+    const HostPlan* hpp = nullptr;
+    costa_status st = host_plan(dtype, n, desc, sigma, hpp);
+    if (st != COSTA_SUCCESS) return st;
+    const HostPlan& hp = *hpp;
+    const int es = elem_size(dtype);
+    costa_stats s{};
+    s.overlay_blocks = hp.overlay_blocks;
+    for (int32_t k = 0; k < n; ++k) {
+      bool reads_a = !(desc[k].beta && is_zero(dtype, desc[k].beta));
+      s.total_elems += hp.item_total[k];
+      s.local_elems += hp.item_local[k];
+      s.remote_elems += hp.item_remote[k];
+      s.model_bytes += (int64_t)es * (hp.item_total[k] * (2 + (reads_a ? 1 : 0)) + 2 * hp.item_remote[k]);
+      s.pack_bytes += (int64_t)es * 2 * hp.item_remote[k];
+      s.unpack_bytes += (int64_t)es * hp.item_remote[k] * (2 + (reads_a ? 1 : 0));
+      s.direct_bytes += (int64_t)es * hp.item_local[k] * (2 + (reads_a ? 1 : 0));
+    }
+    s.message_bytes = (int64_t)es * s.remote_elems;
+    s.workspace_bytes = hp.workspace_bytes;
+    s.waves = (int32_t)hp.waves.size();
+    s.pieces_pack = hp.pieces_pack;
+    s.pieces_unpack = hp.pieces_unpack;
+    s.pieces_direct = hp.pieces_direct;
+    s.plan_ms = hp.plan_ms;
+    *out = s;
+    return COSTA_SUCCESS;
+  });
 }
 
 namespace costa {
@@ -633,142 +678,166 @@ hipError_t upload(DevBuf& d, const T* src, size_t n, hipStream_t stream) {
 
 extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, costa_op op, int64_t* V_host,
                                             hipStream_t stream) {
-  const Layout* A = layout_of(A_h);
-  const Layout* B = layout_of(B_h);
-  if (!A || !B || !V_host) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
-  if (op != COSTA_OP_N && op != COSTA_OP_T && op != COSTA_OP_C) return fail(COSTA_ERROR_INVALID_VALUE, "unknown op");
-  const bool tr = op != COSTA_OP_N;
-  if (A->nrows != (tr ? B->ncols : B->nrows) || A->ncols != (tr ? B->nrows : B->ncols))
-    return fail(COSTA_ERROR_SHAPE_MISMATCH, "A is not the shape of op(B)");
-  if (A->nranks != B->nranks) return fail(COSTA_ERROR_SHAPE_MISMATCH, "layouts of A and B have different P");
-  const int32_t P = A->nranks;
-  const size_t PP = (size_t)P * P;
-  std::memset(V_host, 0, sizeof(int64_t) * PP);
-  std::vector<Interval> rows = overlay(A->rsplit, tr ? B->csplit : B->rsplit);
-  std::vector<Interval> cols = overlay(A->csplit, tr ? B->rsplit : B->csplit);
-  if (rows.empty() || cols.empty()) return COSTA_SUCCESS;
-  if (rows.size() > INT32_MAX || cols.size() > INT32_MAX)
-    return fail(COSTA_ERROR_NOT_SUPPORTED, "more than 2^31 overlay intervals in one dimension");
-  State& S = state();
-  std::lock_guard<std::mutex> lock(S.mu);
-  // the separable kernels number the ranks of a grid by its rank order
-  const bool separable = A->block_cyclic && B->block_cyclic && A->rank_map.empty() && B->rank_map.empty();
-  DevBuf d_rows, d_cols, d_oa, d_ob, d_v, d_hr, d_hc;
-  std::vector<unsigned long long> zeros;
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (S.timing) {
-    e0 = get_event(S);
-    e1 = get_event(S);
-  }
-  auto run = [&]() -> costa_status {
-    HIP_OR_FAIL(d_v.alloc(sizeof(int64_t) * PP));
-    if (separable) {
-      // classes of the covering blocks: process row/column of A's block and
-      // of op(B)'s block (B's process column for the rows of op(B) when
-      // transposed, and its process row for the columns)
-      const int32_t nrb = tr ? B->pcol : B->prow, ncb = tr ? B->prow : B->pcol;
-      for (Interval& v : rows) {
-        v.a = A->prow_of(v.a);
-        v.b = tr ? B->pcol_of(v.b) : B->prow_of(v.b);
-      }
-      for (Interval& v : cols) {
-        v.a = A->pcol_of(v.a);
-        v.b = tr ? B->prow_of(v.b) : B->pcol_of(v.b);
-      }
-      const size_t nh_r = (size_t)nrb * A->prow, nh_c = (size_t)ncb * A->pcol;
-      zeros.assign(std::max(nh_r, nh_c), 0ull);
-      HIP_OR_FAIL(upload(d_rows, rows.data(), rows.size(), stream));
-      HIP_OR_FAIL(upload(d_cols, cols.data(), cols.size(), stream));
-      HIP_OR_FAIL(upload(d_hr, zeros.data(), nh_r, stream));
-      HIP_OR_FAIL(upload(d_hc, zeros.data(), nh_c, stream));
-      SeparableArgs a{d_rows.as<Interval>(), (int32_t)rows.size(), d_cols.as<Interval>(), (int32_t)cols.size(),
-                      nrb, A->prow, ncb, A->pcol, d_hr.as<unsigned long long>(), d_hc.as<unsigned long long>(),
-                      A->prow, A->pcol, A->rank_order == COSTA_ROW_MAJOR ? 1 : 0, B->prow, B->pcol,
-                      B->rank_order == COSTA_ROW_MAJOR ? 1 : 0, tr ? 1 : 0, P, d_v.as<unsigned long long>()};
-      if (e0) HIP_OR_FAIL(hipEventRecord(e0, stream));
-      HIP_OR_FAIL(launch_volume_separable(a, stream));
-    } else {
-      // owner tables (block-cyclic layouts keep none: write them out here)
-      std::vector<int32_t> oa_tmp, ob_tmp;
-      auto owners = [](const Layout* L, std::vector<int32_t>& tmp) -> const std::vector<int32_t>& {
-        if (!L->block_cyclic) return L->owner;
-        tmp.resize((size_t)L->nbr * L->nbc);
-        for (int32_t bi = 0; bi < L->nbr; ++bi)
-          for (int32_t bj = 0; bj < L->nbc; ++bj) tmp[L->block(bi, bj)] = L->owner_of(bi, bj);
-        return tmp;
-      };
-      const std::vector<int32_t>& oa = owners(A, oa_tmp);
-      const std::vector<int32_t>& ob = owners(B, ob_tmp);
-      zeros.assign(PP, 0ull);
-      HIP_OR_FAIL(upload(d_rows, rows.data(), rows.size(), stream));
-      HIP_OR_FAIL(upload(d_cols, cols.data(), cols.size(), stream));
-      HIP_OR_FAIL(upload(d_oa, oa.data(), oa.size(), stream));
-      HIP_OR_FAIL(upload(d_ob, ob.data(), ob.size(), stream));
-      HIP_OR_FAIL(hipMemcpyAsync(d_v.p, zeros.data(), sizeof(int64_t) * PP, hipMemcpyHostToDevice, stream));
-      VolumeArgs a{d_rows.as<Interval>(), (int32_t)rows.size(), d_cols.as<Interval>(), (int32_t)cols.size(),
-                   d_oa.as<int32_t>(), A->nbc, d_ob.as<int32_t>(), B->nbc, tr ? 1 : 0, P,
-                   d_v.as<unsigned long long>()};
-      if (e0) HIP_OR_FAIL(hipEventRecord(e0, stream));
-      HIP_OR_FAIL(launch_volume(a, stream));
+  return guarded([&]() -> costa_status {
+    const Layout* A = layout_of(A_h);
+    const Layout* B = layout_of(B_h);
+    if (!A || !B || !V_host) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
+    if (op != COSTA_OP_N && op != COSTA_OP_T && op != COSTA_OP_C) return fail(COSTA_ERROR_INVALID_VALUE, "unknown op");
+    const bool tr = op != COSTA_OP_N;
+    if (A->nrows != (tr ? B->ncols : B->nrows) || A->ncols != (tr ? B->nrows : B->ncols))
+      return fail(COSTA_ERROR_SHAPE_MISMATCH, "A is not the shape of op(B)");
+    if (A->nranks != B->nranks) return fail(COSTA_ERROR_SHAPE_MISMATCH, "layouts of A and B have different P");
+    const int32_t P = A->nranks;
+    const size_t PP = (size_t)P * P;
+    std::memset(V_host, 0, sizeof(int64_t) * PP);
+    std::vector<Interval> rows = overlay(A->rsplit, tr ? B->csplit : B->rsplit);
+    std::vector<Interval> cols = overlay(A->csplit, tr ? B->rsplit : B->csplit);
+    if (rows.empty() || cols.empty()) return COSTA_SUCCESS;
+    if (rows.size() > INT32_MAX || cols.size() > INT32_MAX)
+      return fail(COSTA_ERROR_NOT_SUPPORTED, "more than 2^31 overlay intervals in one dimension");
+    State& S = state();
+    std::lock_guard<std::mutex> lock(S.mu);
+    // two block-cyclic layouts (with or without a rank map): the separable kernels
+    const bool separable = A->block_cyclic && B->block_cyclic;
+    DevBuf d_rows, d_cols, d_oa, d_ob, d_v, d_hr, d_hc, d_ca, d_cb;
+    std::vector<unsigned long long> zeros;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (S.timing) {
+      e0 = get_event(S);
+      e1 = get_event(S);
     }
-    if (e1) {
-      HIP_OR_FAIL(hipEventRecord(e1, stream));
-      S.pending.push_back(TimingRec{COSTA_KERNEL_VOLUME, e0, e1, (int64_t)(rows.size() + cols.size()) * 24});
-      e0 = e1 = nullptr;
-    }
-    HIP_OR_FAIL(hipMemcpyAsync(V_host, d_v.p, sizeof(int64_t) * PP, hipMemcpyDeviceToHost, stream));
-    HIP_OR_FAIL(hipStreamSynchronize(stream));
-    return COSTA_SUCCESS;
-  };
-  costa_status st = run();
-  (void)hipStreamSynchronize(stream);  // device buffers are freed below
-  if (e0) S.event_pool.push_back(e0);
-  if (e1) S.event_pool.push_back(e1);
-  return st;
+    auto run = [&]() -> costa_status {
+      HIP_OR_FAIL(d_v.alloc(sizeof(int64_t) * PP));
+      if (separable) {
+        // classes of the covering blocks: process row/column of A's block and
+        // of op(B)'s block (B's process column for the rows of op(B) when
+        // transposed, and its process row for the columns)
+        const int32_t nrb = tr ? B->pcol : B->prow, ncb = tr ? B->prow : B->pcol;
+        for (Interval& v : rows) {
+          v.a = A->prow_of(v.a);
+          v.b = tr ? B->pcol_of(v.b) : B->prow_of(v.b);
+        }
+        for (Interval& v : cols) {
+          v.a = A->pcol_of(v.a);
+          v.b = tr ? B->prow_of(v.b) : B->pcol_of(v.b);
+        }
+        const size_t nh_r = (size_t)nrb * A->prow, nh_c = (size_t)ncb * A->pcol;
+        zeros.assign(std::max(nh_r, nh_c), 0ull);
+        // each rank's row and column class in A's grid and in op(B)'s (-1
+        // outside the grid: a rank map may leave ranks out)
+        std::vector<int32_t> ca((size_t)2 * P, -1), cb((size_t)2 * P, -1);
+        for (int32_t pr = 0; pr < A->prow; ++pr)
+          for (int32_t pc = 0; pc < A->pcol; ++pc) {
+            const int32_t r = A->rank_at(pr, pc);
+            ca[(size_t)2 * r] = pr;
+            ca[(size_t)2 * r + 1] = pc;
+          }
+        for (int32_t pr = 0; pr < B->prow; ++pr)
+          for (int32_t pc = 0; pc < B->pcol; ++pc) {
+            const int32_t r = B->rank_at(pr, pc);
+            cb[(size_t)2 * r] = tr ? pc : pr;
+            cb[(size_t)2 * r + 1] = tr ? pr : pc;
+          }
+        HIP_OR_FAIL(upload(d_rows, rows.data(), rows.size(), stream));
+        HIP_OR_FAIL(upload(d_cols, cols.data(), cols.size(), stream));
+        HIP_OR_FAIL(upload(d_hr, zeros.data(), nh_r, stream));
+        HIP_OR_FAIL(upload(d_hc, zeros.data(), nh_c, stream));
+        HIP_OR_FAIL(upload(d_ca, ca.data(), ca.size(), stream));
+        HIP_OR_FAIL(upload(d_cb, cb.data(), cb.size(), stream));
+        SeparableArgs a{d_rows.as<Interval>(), (int32_t)rows.size(), d_cols.as<Interval>(), (int32_t)cols.size(),
+                        nrb, A->prow, ncb, A->pcol, d_hr.as<unsigned long long>(), d_hc.as<unsigned long long>(),
+                        d_ca.as<int32_t>(), d_cb.as<int32_t>(), P, d_v.as<unsigned long long>()};
+        if (e0) HIP_OR_FAIL(hipEventRecord(e0, stream));
+        HIP_OR_FAIL(launch_volume_separable(a, stream));
+      } else {
+        // owner tables (block-cyclic layouts keep none: write them out here)
+        std::vector<int32_t> oa_tmp, ob_tmp;
+        auto owners = [](const Layout* L, std::vector<int32_t>& tmp) -> const std::vector<int32_t>& {
+          if (!L->block_cyclic) return L->owner;
+          tmp.resize((size_t)L->nbr * L->nbc);
+          for (int32_t bi = 0; bi < L->nbr; ++bi)
+            for (int32_t bj = 0; bj < L->nbc; ++bj) tmp[L->block(bi, bj)] = L->owner_of(bi, bj);
+          return tmp;
+        };
+        const std::vector<int32_t>& oa = owners(A, oa_tmp);
+        const std::vector<int32_t>& ob = owners(B, ob_tmp);
+        zeros.assign(PP, 0ull);
+        HIP_OR_FAIL(upload(d_rows, rows.data(), rows.size(), stream));
+        HIP_OR_FAIL(upload(d_cols, cols.data(), cols.size(), stream));
+        HIP_OR_FAIL(upload(d_oa, oa.data(), oa.size(), stream));
+        HIP_OR_FAIL(upload(d_ob, ob.data(), ob.size(), stream));
+        HIP_OR_FAIL(hipMemcpyAsync(d_v.p, zeros.data(), sizeof(int64_t) * PP, hipMemcpyHostToDevice, stream));
+        VolumeArgs a{d_rows.as<Interval>(), (int32_t)rows.size(), d_cols.as<Interval>(), (int32_t)cols.size(),
+                     d_oa.as<int32_t>(), A->nbc, d_ob.as<int32_t>(), B->nbc, tr ? 1 : 0, P,
+                     d_v.as<unsigned long long>()};
+        if (e0) HIP_OR_FAIL(hipEventRecord(e0, stream));
+        HIP_OR_FAIL(launch_volume(a, stream));
+      }
+      if (e1) {
+        HIP_OR_FAIL(hipEventRecord(e1, stream));
+        S.pending.push_back(TimingRec{COSTA_KERNEL_VOLUME, e0, e1, (int64_t)(rows.size() + cols.size()) * 24});
+        e0 = e1 = nullptr;
+      }
+      HIP_OR_FAIL(hipMemcpyAsync(V_host, d_v.p, sizeof(int64_t) * PP, hipMemcpyDeviceToHost, stream));
+      HIP_OR_FAIL(hipStreamSynchronize(stream));
+      return COSTA_SUCCESS;
+    };
+    costa_status st = run();
+    (void)hipStreamSynchronize(stream);  // device buffers are freed below
+    if (e0) S.event_pool.push_back(e0);
+    if (e1) S.event_pool.push_back(e1);
+    return st;
+  });
 }
 
 extern "C" costa_status costa_timing_enable(int on) {
-  State& S = state();
-  std::lock_guard<std::mutex> lock(S.mu);
-  costa_status st = collect_timing(S);
-  S.timing = on != 0;
-  S.totals = costa_timing{};
-  return st;
+  return guarded([&]() -> costa_status {
+    State& S = state();
+    std::lock_guard<std::mutex> lock(S.mu);
+    costa_status st = collect_timing(S);
+    S.timing = on != 0;
+    S.totals = costa_timing{};
+    return st;
+  });
 }
 
 extern "C" costa_status costa_timing_read(costa_timing* out) {
-  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output");
-  State& S = state();
-  std::lock_guard<std::mutex> lock(S.mu);
-  costa_status st = collect_timing(S);
-  *out = S.totals;
-  return st;
+  return guarded([&]() -> costa_status {
+    if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output");
+    State& S = state();
+    std::lock_guard<std::mutex> lock(S.mu);
+    costa_status st = collect_timing(S);
+    *out = S.totals;
+    return st;
+  });
 }
 
 extern "C" costa_status costa_finalize(void) {
-  State& S = state();
-  {
-    std::lock_guard<std::mutex> lock(S.mu);
-    if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty()) HIP_OR_FAIL(hipDeviceSynchronize());
-    for (const TimingRec& r : S.pending) {  // recorded but never read: their events go too
-      (void)hipEventDestroy(r.start);
-      (void)hipEventDestroy(r.stop);
+  return guarded([&]() -> costa_status {
+    State& S = state();
+    {
+      std::lock_guard<std::mutex> lock(S.mu);
+      if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty()) HIP_OR_FAIL(hipDeviceSynchronize());
+      for (const TimingRec& r : S.pending) {  // recorded but never read: their events go too
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.stop);
+      }
+      S.pending.clear();
+      S.plans.clear();
+      S.host_plans.clear();
+      for (auto& kv : S.ws) {
+        if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+        if (kv.second.last_use) (void)hipEventDestroy(kv.second.last_use);
+      }
+      S.ws.clear();
+      for (hipEvent_t e : S.event_pool) (void)hipEventDestroy(e);
+      S.event_pool.clear();
+      S.timing = false;
+      S.totals = costa_timing{};
     }
-    S.pending.clear();
-    S.plans.clear();
-    S.host_plans.clear();
-    for (auto& kv : S.ws) {
-      if (kv.second.ptr) (void)hipFree(kv.second.ptr);
-      if (kv.second.last_use) (void)hipEventDestroy(kv.second.last_use);
-    }
-    S.ws.clear();
-    for (hipEvent_t e : S.event_pool) (void)hipEventDestroy(e);
-    S.event_pool.clear();
-    S.timing = false;
-    S.totals = costa_timing{};
-  }
-  // outside the state lock: a ScaLAPACK-style call takes the layout cache's
-  // lock and then the state lock, never the other way round
-  release_scalapack_layouts();
-  return COSTA_SUCCESS;
+    // outside the state lock: a ScaLAPACK-style call takes the layout cache's
+    // lock and then the state lock, never the other way round
+    release_scalapack_layouts();
+    return COSTA_SUCCESS;
+  });
 }

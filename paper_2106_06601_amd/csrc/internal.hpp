@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <new>
+#include <stdexcept>
 #include <string>
 #include <vector>
 
@@ -15,6 +17,33 @@ namespace costa {
 // ---- error reporting -------------------------------------------------------
 void set_error(const std::string& msg);
 costa_status fail(costa_status st, const std::string& msg);
+
+// A valid request past what the kernels index: more than 2^31 rectangles or
+// workgroups in one launch, or more than 2^32 rectangles to sort.
+struct LimitExceeded : std::runtime_error {
+  using std::runtime_error::runtime_error;
+};
+
+// Runs the body of a C entry point so that nothing it throws crosses the C
+// ABI: a host allocation that fails (std::bad_alloc, or a container asked for
+// more than it can hold) is COSTA_ERROR_OUT_OF_MEMORY, a LimitExceeded is
+// COSTA_ERROR_NOT_SUPPORTED.
+template <typename F>
+costa_status guarded(F&& body) noexcept {
+  try {
+    return body();
+  } catch (const LimitExceeded& e) {
+    return fail(COSTA_ERROR_NOT_SUPPORTED, e.what());
+  } catch (const std::bad_alloc&) {
+    return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
+  } catch (const std::length_error&) {
+    return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed (container size limit)");
+  } catch (const std::exception& e) {
+    return fail(COSTA_ERROR_NOT_SUPPORTED, std::string("unexpected host error: ") + e.what());
+  } catch (...) {
+    return fail(COSTA_ERROR_NOT_SUPPORTED, "unexpected host error");
+  }
+}
 
 // ---- layouts (Section 5 "Matrix Layout", Figure 1) -------------------------
 struct Layout {
@@ -252,9 +281,10 @@ struct SeparableArgs {
   int32_t ncb, nca;  // column classes
   unsigned long long* hrow;  // nrb * nra, zeroed by the caller
   unsigned long long* hcol;  // ncb * nca, zeroed by the caller
-  int32_t prowA, pcolA, rowmajA;
-  int32_t prowB, pcolB, rowmajB;
-  int32_t transposed;
+  // per rank r: its row class at [2r] and column class at [2r + 1] in A's
+  // grid (clsA) and in op(B)'s grid (clsB), or -1 for a rank outside the grid
+  const int32_t* clsA;
+  const int32_t* clsB;
   int32_t P;
   unsigned long long* V;
 };

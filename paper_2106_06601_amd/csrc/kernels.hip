@@ -491,19 +491,16 @@ __global__ void __launch_bounds__(kThreads) costa_volume_hist(SeparableArgs a) {
 }
 
 // Separable volume, step 2: V[s][t] = hrow[row class of s][row class of t] *
-// hcol[col class of s][col class of t] (for op T the row overlay of op(B)
-// runs over B's process columns and the column overlay over its rows).
+// hcol[col class of s][col class of t], 0 when s or t has no place in its
+// grid (for op T the row overlay of op(B) runs over B's process columns and
+// the column overlay over its rows; the host folds that into clsB).
 __global__ void __launch_bounds__(kThreads) costa_volume_outer(SeparableArgs a) {
   const int32_t PP = a.P * a.P;
   for (int32_t k = blockIdx.x * kThreads + threadIdx.x; k < PP; k += gridDim.x * kThreads) {
     const int32_t s = k / a.P, t = k % a.P;
-    const int32_t prA = a.rowmajA ? t / a.pcolA : t % a.prowA;
-    const int32_t pcA = a.rowmajA ? t % a.pcolA : t / a.prowA;
-    const int32_t prB = a.rowmajB ? s / a.pcolB : s % a.prowB;
-    const int32_t pcB = a.rowmajB ? s % a.pcolB : s / a.prowB;
-    const int32_t rb = a.transposed ? pcB : prB;  // class of s in the row overlay
-    const int32_t cb = a.transposed ? prB : pcB;  // class of s in the column overlay
-    a.V[k] = a.hrow[(int64_t)rb * a.nra + prA] * a.hcol[(int64_t)cb * a.nca + pcA];
+    const int32_t ra = a.clsA[2 * t], ca = a.clsA[2 * t + 1];
+    const int32_t rb = a.clsB[2 * s], cb = a.clsB[2 * s + 1];
+    a.V[k] = (ra < 0 || rb < 0) ? 0ull : a.hrow[(int64_t)rb * a.nra + ra] * a.hcol[(int64_t)cb * a.nca + ca];
   }
 }
 

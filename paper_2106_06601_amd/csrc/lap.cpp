@@ -186,99 +186,103 @@ void greedy_matching(int n, const std::vector<T>& weight, std::vector<int>& rowc
 extern "C" costa_status costa_relabel_cost(int32_t P, const int64_t* V, double elem_bytes, const double* latency,
                                            const double* inv_bandwidth, costa_relabel_method method, int32_t* sigma,
                                            double* cost_before, double* cost_after) {
-  using namespace costa;
-  if (P < 0) return fail(COSTA_ERROR_INVALID_VALUE, "P must be >= 0");
-  if (P > 0 && (!V || !sigma)) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
-  if ((latency == nullptr) != (inv_bandwidth == nullptr))
-    return fail(COSTA_ERROR_INVALID_VALUE, "latency and inv_bandwidth must both be given or both be NULL");
-  if (method != COSTA_RELABEL_EXACT && method != COSTA_RELABEL_GREEDY)
-    return fail(COSTA_ERROR_INVALID_VALUE, "unknown relabeling method");
-  if (!(elem_bytes > 0) || !std::isfinite(elem_bytes)) return fail(COSTA_ERROR_INVALID_VALUE, "elem_bytes must be > 0");
-  const bool general = latency != nullptr;
-  if (P > (general ? 1024 : 4096)) return fail(COSTA_ERROR_NOT_SUPPORTED, "P too large for the relabeling");
-  const size_t PP = (size_t)P * P;
-  for (size_t k = 0; k < PP; ++k) {
-    if (V[k] < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative volume");
-    if (general && (!std::isfinite(latency[k]) || !std::isfinite(inv_bandwidth[k]) || latency[k] < 0 ||
-                    inv_bandwidth[k] < 0))
-      return fail(COSTA_ERROR_INVALID_VALUE, "latency and inv_bandwidth entries must be finite and >= 0");
-  }
-  // w(p_i, p_j, S_ij) of a non-empty package of `vol` elements
-  auto w = [&](int i, int j, int64_t vol) -> long double {
-    if (vol == 0) return 0.0L;
-    const long double bytes = (long double)vol * elem_bytes;
-    if (!general) return i == j ? 0.0L : bytes;
-    return (long double)latency[(size_t)i * P + j] + (long double)inv_bandwidth[(size_t)i * P + j] * bytes;
-  };
-  auto total = [&](const int32_t* sg) {
-    long double W = 0;
-    for (int i = 0; i < P; ++i)
-      for (int j = 0; j < P; ++j) {
-        const int64_t vol = V[(size_t)i * P + j];
-        if (vol) W += w(i, sg ? sg[j] : j, vol);
-      }
-    return W;
-  };
-  if (P > 0) {
-    if (!general && method == COSTA_RELABEL_EXACT) {
-      solve_relabel(P, V, sigma);  // integer path, canonical tie-break
-    } else if (!general) {
-      // gain remark: delta(p_x, p_y) = V(S_yx) - V(S_xx), exact in integers
-      std::vector<int64_t> gain(PP);
-      for (int x = 0; x < P; ++x)
-        for (int y = 0; y < P; ++y) gain[(size_t)x * P + y] = V[(size_t)y * P + x] - V[(size_t)x * P + x];
-      std::vector<int> rowcol;
-      greedy_matching(P, gain, rowcol);
-      for (int x = 0; x < P; ++x) sigma[x] = rowcol[x];
-    } else {
-      // eq:delta: sum over the left neighbours p_i of p_x (S_ix non-empty)
-      std::vector<long double> gain(PP, 0.0L);
-      for (int x = 0; x < P; ++x)
-        for (int y = 0; y < P; ++y) {
-          long double d = 0;
-          for (int i = 0; i < P; ++i) {
-            const int64_t vol = V[(size_t)i * P + x];
-            if (vol) d += w(i, x, vol) - w(i, y, vol);
-          }
-          gain[(size_t)x * P + y] = d;
+  return costa::guarded([&]() -> costa_status {
+    using namespace costa;
+    if (P < 0) return fail(COSTA_ERROR_INVALID_VALUE, "P must be >= 0");
+    if (P > 0 && (!V || !sigma)) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
+    if ((latency == nullptr) != (inv_bandwidth == nullptr))
+      return fail(COSTA_ERROR_INVALID_VALUE, "latency and inv_bandwidth must both be given or both be NULL");
+    if (method != COSTA_RELABEL_EXACT && method != COSTA_RELABEL_GREEDY)
+      return fail(COSTA_ERROR_INVALID_VALUE, "unknown relabeling method");
+    if (!(elem_bytes > 0) || !std::isfinite(elem_bytes)) return fail(COSTA_ERROR_INVALID_VALUE, "elem_bytes must be > 0");
+    const bool general = latency != nullptr;
+    if (P > (general ? 1024 : 4096)) return fail(COSTA_ERROR_NOT_SUPPORTED, "P too large for the relabeling");
+    const size_t PP = (size_t)P * P;
+    for (size_t k = 0; k < PP; ++k) {
+      if (V[k] < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative volume");
+      if (general && (!std::isfinite(latency[k]) || !std::isfinite(inv_bandwidth[k]) || latency[k] < 0 ||
+                      inv_bandwidth[k] < 0))
+        return fail(COSTA_ERROR_INVALID_VALUE, "latency and inv_bandwidth entries must be finite and >= 0");
+    }
+    // w(p_i, p_j, S_ij) of a non-empty package of `vol` elements
+    auto w = [&](int i, int j, int64_t vol) -> long double {
+      if (vol == 0) return 0.0L;
+      const long double bytes = (long double)vol * elem_bytes;
+      if (!general) return i == j ? 0.0L : bytes;
+      return (long double)latency[(size_t)i * P + j] + (long double)inv_bandwidth[(size_t)i * P + j] * bytes;
+    };
+    auto total = [&](const int32_t* sg) {
+      long double W = 0;
+      for (int i = 0; i < P; ++i)
+        for (int j = 0; j < P; ++j) {
+          const int64_t vol = V[(size_t)i * P + j];
+          if (vol) W += w(i, sg ? sg[j] : j, vol);
         }
-      if (method == COSTA_RELABEL_GREEDY) {
+      return W;
+    };
+    if (P > 0) {
+      if (!general && method == COSTA_RELABEL_EXACT) {
+        solve_relabel(P, V, sigma);  // integer path, canonical tie-break
+      } else if (!general) {
+        // gain remark: delta(p_x, p_y) = V(S_yx) - V(S_xx), exact in integers
+        std::vector<int64_t> gain(PP);
+        for (int x = 0; x < P; ++x)
+          for (int y = 0; y < P; ++y) gain[(size_t)x * P + y] = V[(size_t)y * P + x] - V[(size_t)x * P + x];
         std::vector<int> rowcol;
         greedy_matching(P, gain, rowcol);
         for (int x = 0; x < P; ++x) sigma[x] = rowcol[x];
       } else {
-        std::vector<long double> cost(PP);
-        for (size_t k = 0; k < PP; ++k) cost[k] = -gain[k];
-        std::vector<long double> u, v;
-        std::vector<int> colrow;
-        hungarian<long double>(P, cost, std::numeric_limits<long double>::infinity(), u, v, colrow);  // rows = labels
-        for (int y = 0; y < P; ++y) sigma[colrow[y]] = y;
+        // eq:delta: sum over the left neighbours p_i of p_x (S_ix non-empty)
+        std::vector<long double> gain(PP, 0.0L);
+        for (int x = 0; x < P; ++x)
+          for (int y = 0; y < P; ++y) {
+            long double d = 0;
+            for (int i = 0; i < P; ++i) {
+              const int64_t vol = V[(size_t)i * P + x];
+              if (vol) d += w(i, x, vol) - w(i, y, vol);
+            }
+            gain[(size_t)x * P + y] = d;
+          }
+        if (method == COSTA_RELABEL_GREEDY) {
+          std::vector<int> rowcol;
+          greedy_matching(P, gain, rowcol);
+          for (int x = 0; x < P; ++x) sigma[x] = rowcol[x];
+        } else {
+          std::vector<long double> cost(PP);
+          for (size_t k = 0; k < PP; ++k) cost[k] = -gain[k];
+          std::vector<long double> u, v;
+          std::vector<int> colrow;
+          hungarian<long double>(P, cost, std::numeric_limits<long double>::infinity(), u, v, colrow);  // rows = labels
+          for (int y = 0; y < P; ++y) sigma[colrow[y]] = y;
+        }
       }
     }
-  }
-  if (cost_before) *cost_before = (double)total(nullptr);
-  if (cost_after) *cost_after = (double)total(sigma);
-  return COSTA_SUCCESS;
+    if (cost_before) *cost_before = (double)total(nullptr);
+    if (cost_after) *cost_after = (double)total(sigma);
+    return COSTA_SUCCESS;
+  });
 }
 
 extern "C" costa_status costa_relabel(int32_t P, const int64_t* V_host, int32_t* sigma, int64_t* retained_identity,
                                       int64_t* retained_sigma) {
-  using namespace costa;
-  if (P < 0) return fail(COSTA_ERROR_INVALID_VALUE, "P must be >= 0");
-  if (P > 0 && (!V_host || !sigma)) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
-  if (P > 4096) return fail(COSTA_ERROR_NOT_SUPPORTED, "relabeling is limited to P <= 4096");
-  for (int64_t k = 0; k < (int64_t)P * P; ++k)
-    if (V_host[k] < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative volume");
-  solve_relabel(P, V_host, sigma);
-  if (retained_identity) {
-    int64_t r = 0;
-    for (int t = 0; t < P; ++t) r += V_host[(size_t)t * P + t];
-    *retained_identity = r;
-  }
-  if (retained_sigma) {
-    int64_t r = 0;
-    for (int t = 0; t < P; ++t) r += V_host[(size_t)sigma[t] * P + t];
-    *retained_sigma = r;
-  }
-  return COSTA_SUCCESS;
+  return costa::guarded([&]() -> costa_status {
+    using namespace costa;
+    if (P < 0) return fail(COSTA_ERROR_INVALID_VALUE, "P must be >= 0");
+    if (P > 0 && (!V_host || !sigma)) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
+    if (P > 4096) return fail(COSTA_ERROR_NOT_SUPPORTED, "relabeling is limited to P <= 4096");
+    for (int64_t k = 0; k < (int64_t)P * P; ++k)
+      if (V_host[k] < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative volume");
+    solve_relabel(P, V_host, sigma);
+    if (retained_identity) {
+      int64_t r = 0;
+      for (int t = 0; t < P; ++t) r += V_host[(size_t)t * P + t];
+      *retained_identity = r;
+    }
+    if (retained_sigma) {
+      int64_t r = 0;
+      for (int t = 0; t < P; ++t) r += V_host[(size_t)sigma[t] * P + t];
+      *retained_sigma = r;
+    }
+    return COSTA_SUCCESS;
+  });
 }

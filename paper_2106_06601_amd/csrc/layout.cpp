@@ -71,60 +71,62 @@ extern "C" costa_status costa_layout_create(int64_t nrows, int64_t ncols, int32_
                                             int32_t nbc, const int64_t* col_splits, const int32_t* owners,
                                             int32_t nranks, costa_order block_order, const int64_t* block_offset,
                                             const int64_t* block_ld, costa_layout* out) {
-  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
-  *out = nullptr;
-  if (nranks < 1) return fail(COSTA_ERROR_INVALID_VALUE, "nranks must be >= 1");
-  if (block_order != COSTA_COL_MAJOR && block_order != COSTA_ROW_MAJOR)
-    return fail(COSTA_ERROR_INVALID_VALUE, "unknown block order");
-  costa_status st = check_splits("rows", nrows, nbr, row_splits);
-  if (st != COSTA_SUCCESS) return st;
-  st = check_splits("cols", ncols, nbc, col_splits);
-  if (st != COSTA_SUCCESS) return st;
-  int64_t nblocks = (int64_t)nbr * nbc;
-  if (nblocks > 0 && !owners) return fail(COSTA_ERROR_INVALID_VALUE, "null owners");
-  if ((block_offset == nullptr) != (block_ld == nullptr))
-    return fail(COSTA_ERROR_INVALID_VALUE, "block_offset and block_ld must both be given or both be NULL");
-  for (int64_t b = 0; b < nblocks; ++b)
-    if (owners[b] < 0 || owners[b] >= nranks) return fail(COSTA_ERROR_INVALID_VALUE, "owner out of range");
+  return guarded([&]() -> costa_status {
+    if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
+    *out = nullptr;
+    if (nranks < 1) return fail(COSTA_ERROR_INVALID_VALUE, "nranks must be >= 1");
+    if (block_order != COSTA_COL_MAJOR && block_order != COSTA_ROW_MAJOR)
+      return fail(COSTA_ERROR_INVALID_VALUE, "unknown block order");
+    costa_status st = check_splits("rows", nrows, nbr, row_splits);
+    if (st != COSTA_SUCCESS) return st;
+    st = check_splits("cols", ncols, nbc, col_splits);
+    if (st != COSTA_SUCCESS) return st;
+    int64_t nblocks = (int64_t)nbr * nbc;
+    if (nblocks > 0 && !owners) return fail(COSTA_ERROR_INVALID_VALUE, "null owners");
+    if ((block_offset == nullptr) != (block_ld == nullptr))
+      return fail(COSTA_ERROR_INVALID_VALUE, "block_offset and block_ld must both be given or both be NULL");
+    for (int64_t b = 0; b < nblocks; ++b)
+      if (owners[b] < 0 || owners[b] >= nranks) return fail(COSTA_ERROR_INVALID_VALUE, "owner out of range");
 
-  costa_layout_s* h = new (std::nothrow) costa_layout_s();
-  if (!h) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
-  Layout& L = h->L;
-  L.nrows = nrows;
-  L.ncols = ncols;
-  L.nbr = nbr;
-  L.nbc = nbc;
-  L.nranks = nranks;
-  L.order = block_order;
-  L.rsplit.assign(row_splits ? row_splits : nullptr, row_splits ? row_splits + nbr + 1 : nullptr);
-  if (L.rsplit.empty()) L.rsplit.push_back(0);
-  L.csplit.assign(col_splits ? col_splits : nullptr, col_splits ? col_splits + nbc + 1 : nullptr);
-  if (L.csplit.empty()) L.csplit.push_back(0);
-  L.owner.assign(owners, owners + nblocks);
-  L.boff.assign(nblocks, 0);
-  L.bld.assign(nblocks, 1);
-  if (block_offset) {
-    std::memcpy(L.boff.data(), block_offset, sizeof(int64_t) * nblocks);
-    std::memcpy(L.bld.data(), block_ld, sizeof(int64_t) * nblocks);
-  } else {
-    // default packing: blocks of a rank one after another, row-major over (bi, bj)
-    std::vector<int64_t> next(nranks, 0);
-    for (int32_t bi = 0; bi < nbr; ++bi)
-      for (int32_t bj = 0; bj < nbc; ++bj) {
-        int64_t b = L.block(bi, bj);
-        int64_t hgt = L.rsplit[bi + 1] - L.rsplit[bi], wid = L.csplit[bj + 1] - L.csplit[bj];
-        L.boff[b] = next[L.owner[b]];
-        L.bld[b] = block_order == COSTA_COL_MAJOR ? hgt : wid;
-        next[L.owner[b]] += hgt * wid;
-      }
-  }
-  st = finish_layout(L);
-  if (st != COSTA_SUCCESS) {
-    delete h;
-    return st;
-  }
-  *out = h;
-  return COSTA_SUCCESS;
+    costa_layout_s* h = new (std::nothrow) costa_layout_s();
+    if (!h) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
+    Layout& L = h->L;
+    L.nrows = nrows;
+    L.ncols = ncols;
+    L.nbr = nbr;
+    L.nbc = nbc;
+    L.nranks = nranks;
+    L.order = block_order;
+    L.rsplit.assign(row_splits ? row_splits : nullptr, row_splits ? row_splits + nbr + 1 : nullptr);
+    if (L.rsplit.empty()) L.rsplit.push_back(0);
+    L.csplit.assign(col_splits ? col_splits : nullptr, col_splits ? col_splits + nbc + 1 : nullptr);
+    if (L.csplit.empty()) L.csplit.push_back(0);
+    L.owner.assign(owners, owners + nblocks);
+    L.boff.assign(nblocks, 0);
+    L.bld.assign(nblocks, 1);
+    if (block_offset) {
+      std::memcpy(L.boff.data(), block_offset, sizeof(int64_t) * nblocks);
+      std::memcpy(L.bld.data(), block_ld, sizeof(int64_t) * nblocks);
+    } else {
+      // default packing: blocks of a rank one after another, row-major over (bi, bj)
+      std::vector<int64_t> next(nranks, 0);
+      for (int32_t bi = 0; bi < nbr; ++bi)
+        for (int32_t bj = 0; bj < nbc; ++bj) {
+          int64_t b = L.block(bi, bj);
+          int64_t hgt = L.rsplit[bi + 1] - L.rsplit[bi], wid = L.csplit[bj + 1] - L.csplit[bj];
+          L.boff[b] = next[L.owner[b]];
+          L.bld[b] = block_order == COSTA_COL_MAJOR ? hgt : wid;
+          next[L.owner[b]] += hgt * wid;
+        }
+    }
+    st = finish_layout(L);
+    if (st != COSTA_SUCCESS) {
+      delete h;
+      return st;
+    }
+    *out = h;
+    return COSTA_SUCCESS;
+  });
 }
 
 namespace costa {
@@ -254,125 +256,139 @@ static costa_status make_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, 
 extern "C" costa_status costa_layout_create_block_cyclic(int64_t nrows, int64_t ncols, int64_t mb, int64_t nb,
                                                          int32_t prow, int32_t pcol, costa_order rank_order,
                                                          costa_order block_order, costa_layout* out) {
-  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
-  *out = nullptr;
-  return make_block_cyclic(nrows, ncols, mb, nb, prow, pcol, 0, 0, 0, rank_order, block_order, 0, nullptr, out);
+  return guarded([&]() -> costa_status {
+    if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
+    *out = nullptr;
+    return make_block_cyclic(nrows, ncols, mb, nb, prow, pcol, 0, 0, 0, rank_order, block_order, 0, nullptr, out);
+  });
 }
 
 extern "C" costa_status costa_layout_create_scalapack(const int32_t* desc, const costa_grid* grid,
                                                       costa_layout* out) {
-  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
-  *out = nullptr;
-  if (!desc || !grid) return fail(COSTA_ERROR_INVALID_VALUE, "null descriptor or grid");
-  if (desc[0] != 1) return fail(COSTA_ERROR_NOT_SUPPORTED, "descriptor type (DTYPE_) other than 1 (dense)");
-  if (grid->nprow < 1 || grid->npcol < 1) return fail(COSTA_ERROR_INVALID_VALUE, "process grid must be at least 1x1");
-  if (desc[6] < 0 || desc[6] >= grid->nprow) return fail(COSTA_ERROR_INVALID_VALUE, "RSRC_ outside the process grid");
-  if (desc[7] < 0 || desc[7] >= grid->npcol) return fail(COSTA_ERROR_INVALID_VALUE, "CSRC_ outside the process grid");
-  if (desc[8] < 1) return fail(COSTA_ERROR_INVALID_VALUE, "LLD_ must be >= 1");
-  if (grid->nranks < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative number of ranks");
-  return make_block_cyclic(desc[2], desc[3], desc[4], desc[5], grid->nprow, grid->npcol, desc[6], desc[7], desc[8],
-                           grid->rank_map ? COSTA_ROW_MAJOR : grid->rank_order, COSTA_COL_MAJOR, grid->nranks,
-                           grid->rank_map, out);
+  return guarded([&]() -> costa_status {
+    if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
+    *out = nullptr;
+    if (!desc || !grid) return fail(COSTA_ERROR_INVALID_VALUE, "null descriptor or grid");
+    if (desc[0] != 1) return fail(COSTA_ERROR_NOT_SUPPORTED, "descriptor type (DTYPE_) other than 1 (dense)");
+    if (grid->nprow < 1 || grid->npcol < 1) return fail(COSTA_ERROR_INVALID_VALUE, "process grid must be at least 1x1");
+    if (desc[6] < 0 || desc[6] >= grid->nprow) return fail(COSTA_ERROR_INVALID_VALUE, "RSRC_ outside the process grid");
+    if (desc[7] < 0 || desc[7] >= grid->npcol) return fail(COSTA_ERROR_INVALID_VALUE, "CSRC_ outside the process grid");
+    if (desc[8] < 1) return fail(COSTA_ERROR_INVALID_VALUE, "LLD_ must be >= 1");
+    if (grid->nranks < 0) return fail(COSTA_ERROR_INVALID_VALUE, "negative number of ranks");
+    return make_block_cyclic(desc[2], desc[3], desc[4], desc[5], grid->nprow, grid->npcol, desc[6], desc[7], desc[8],
+                             grid->rank_map ? COSTA_ROW_MAJOR : grid->rank_order, COSTA_COL_MAJOR, grid->nranks,
+                             grid->rank_map, out);
+  });
 }
 
 extern "C" costa_status costa_layout_submatrix(costa_layout parent, int64_t i0, int64_t j0, int64_t m, int64_t n,
                                                costa_layout* out) {
-  if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
-  *out = nullptr;
-  if (!parent) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
-  const Layout& P = parent->L;
-  if (i0 < 0 || j0 < 0 || m < 0 || n < 0 || i0 > P.nrows - m || j0 > P.ncols - n)
-    return fail(COSTA_ERROR_INVALID_VALUE, "submatrix outside the matrix");
-  costa_layout_s* h = new (std::nothrow) costa_layout_s();
-  if (!h) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
-  Layout& L = h->L;
-  costa_status st;
-  if (P.block_cyclic) {
-    L = P;
-    st = set_window(L, P.r0 + i0, P.c0 + j0, m, n);
-  } else {
-    // keep the blocks the window meets, cut to it; each keeps its storage,
-    // the offset moving to the window's first element inside it
-    auto range = [](const std::vector<int64_t>& s, int64_t lo, int64_t len, int32_t& first) -> int32_t {
-      if (len == 0) {
-        first = 0;
-        return 0;
-      }
-      first = (int32_t)(std::upper_bound(s.begin(), s.end(), lo) - s.begin() - 1);
-      const int32_t last = (int32_t)(std::upper_bound(s.begin(), s.end(), lo + len - 1) - s.begin() - 1);
-      return last - first + 1;
-    };
-    int32_t fr, fc;
-    const int32_t nbr = range(P.rsplit, i0, m, fr), nbc = range(P.csplit, j0, n, fc);
-    L.nrows = m;
-    L.ncols = n;
-    L.nbr = nbr;
-    L.nbc = nbc;
-    L.nranks = P.nranks;
-    L.order = P.order;
-    L.rsplit.assign(nbr + 1, 0);
-    for (int32_t k = 1; k < nbr; ++k) L.rsplit[k] = P.rsplit[fr + k] - i0;
-    L.rsplit[nbr] = m;
-    L.csplit.assign(nbc + 1, 0);
-    for (int32_t k = 1; k < nbc; ++k) L.csplit[k] = P.csplit[fc + k] - j0;
-    L.csplit[nbc] = n;
-    const size_t nblocks = (size_t)nbr * nbc;
-    L.owner.resize(nblocks);
-    L.boff.resize(nblocks);
-    L.bld.resize(nblocks);
-    for (int32_t bi = 0; bi < nbr; ++bi)
-      for (int32_t bj = 0; bj < nbc; ++bj) {
-        const int64_t pb = P.block(fr + bi, fc + bj), b = L.block(bi, bj);
-        const int64_t pi = i0 + L.rsplit[bi] - P.rsplit[fr + bi], pj = j0 + L.csplit[bj] - P.csplit[fc + bj];
-        L.owner[b] = P.owner[pb];
-        L.bld[b] = P.bld[pb];
-        L.boff[b] = P.boff[pb] + (P.order == COSTA_COL_MAJOR ? pi + pj * P.bld[pb] : pi * P.bld[pb] + pj);
-      }
-    st = finish_layout(L);
-  }
-  if (st != COSTA_SUCCESS) {
-    delete h;
-    return st;
-  }
-  *out = h;
-  return COSTA_SUCCESS;
+  return guarded([&]() -> costa_status {
+    if (!out) return fail(COSTA_ERROR_INVALID_VALUE, "null output handle");
+    *out = nullptr;
+    if (!parent) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
+    const Layout& P = parent->L;
+    if (i0 < 0 || j0 < 0 || m < 0 || n < 0 || i0 > P.nrows - m || j0 > P.ncols - n)
+      return fail(COSTA_ERROR_INVALID_VALUE, "submatrix outside the matrix");
+    costa_layout_s* h = new (std::nothrow) costa_layout_s();
+    if (!h) return fail(COSTA_ERROR_OUT_OF_MEMORY, "host allocation failed");
+    Layout& L = h->L;
+    costa_status st;
+    if (P.block_cyclic) {
+      L = P;
+      st = set_window(L, P.r0 + i0, P.c0 + j0, m, n);
+    } else {
+      // keep the blocks the window meets, cut to it; each keeps its storage,
+      // the offset moving to the window's first element inside it
+      auto range = [](const std::vector<int64_t>& s, int64_t lo, int64_t len, int32_t& first) -> int32_t {
+        if (len == 0) {
+          first = 0;
+          return 0;
+        }
+        first = (int32_t)(std::upper_bound(s.begin(), s.end(), lo) - s.begin() - 1);
+        const int32_t last = (int32_t)(std::upper_bound(s.begin(), s.end(), lo + len - 1) - s.begin() - 1);
+        return last - first + 1;
+      };
+      int32_t fr, fc;
+      const int32_t nbr = range(P.rsplit, i0, m, fr), nbc = range(P.csplit, j0, n, fc);
+      L.nrows = m;
+      L.ncols = n;
+      L.nbr = nbr;
+      L.nbc = nbc;
+      L.nranks = P.nranks;
+      L.order = P.order;
+      L.rsplit.assign(nbr + 1, 0);
+      for (int32_t k = 1; k < nbr; ++k) L.rsplit[k] = P.rsplit[fr + k] - i0;
+      L.rsplit[nbr] = m;
+      L.csplit.assign(nbc + 1, 0);
+      for (int32_t k = 1; k < nbc; ++k) L.csplit[k] = P.csplit[fc + k] - j0;
+      L.csplit[nbc] = n;
+      const size_t nblocks = (size_t)nbr * nbc;
+      L.owner.resize(nblocks);
+      L.boff.resize(nblocks);
+      L.bld.resize(nblocks);
+      for (int32_t bi = 0; bi < nbr; ++bi)
+        for (int32_t bj = 0; bj < nbc; ++bj) {
+          const int64_t pb = P.block(fr + bi, fc + bj), b = L.block(bi, bj);
+          const int64_t pi = i0 + L.rsplit[bi] - P.rsplit[fr + bi], pj = j0 + L.csplit[bj] - P.csplit[fc + bj];
+          L.owner[b] = P.owner[pb];
+          L.bld[b] = P.bld[pb];
+          L.boff[b] = P.boff[pb] + (P.order == COSTA_COL_MAJOR ? pi + pj * P.bld[pb] : pi * P.bld[pb] + pj);
+        }
+      st = finish_layout(L);
+    }
+    if (st != COSTA_SUCCESS) {
+      delete h;
+      return st;
+    }
+    *out = h;
+    return COSTA_SUCCESS;
+  });
 }
 
 extern "C" costa_status costa_layout_local_elems(costa_layout layout, int32_t rank, int64_t* n) {
-  if (!layout || !n) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
-  if (rank < 0 || rank >= layout->L.nranks) return fail(COSTA_ERROR_INVALID_VALUE, "rank out of range");
-  *n = layout->L.local_elems[rank];
-  return COSTA_SUCCESS;
+  return guarded([&]() -> costa_status {
+    if (!layout || !n) return fail(COSTA_ERROR_INVALID_VALUE, "null argument");
+    if (rank < 0 || rank >= layout->L.nranks) return fail(COSTA_ERROR_INVALID_VALUE, "rank out of range");
+    *n = layout->L.local_elems[rank];
+    return COSTA_SUCCESS;
+  });
 }
 
 extern "C" costa_status costa_layout_block(costa_layout layout, int32_t bi, int32_t bj, int32_t* owner,
                                            int64_t* offset, int64_t* ld) {
-  if (!layout) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
-  const Layout& L = layout->L;
-  if (bi < 0 || bi >= L.nbr || bj < 0 || bj >= L.nbc) return fail(COSTA_ERROR_INVALID_VALUE, "block out of range");
-  if (owner) *owner = L.owner_of(bi, bj);
-  if (offset) *offset = L.offset_of(bi, bj);
-  if (ld) *ld = L.ld_of(bi, bj);
-  return COSTA_SUCCESS;
+  return guarded([&]() -> costa_status {
+    if (!layout) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
+    const Layout& L = layout->L;
+    if (bi < 0 || bi >= L.nbr || bj < 0 || bj >= L.nbc) return fail(COSTA_ERROR_INVALID_VALUE, "block out of range");
+    if (owner) *owner = L.owner_of(bi, bj);
+    if (offset) *offset = L.offset_of(bi, bj);
+    if (ld) *ld = L.ld_of(bi, bj);
+    return COSTA_SUCCESS;
+  });
 }
 
 extern "C" costa_status costa_layout_info(costa_layout layout, int64_t* nrows, int64_t* ncols, int32_t* nbr,
                                           int32_t* nbc, int32_t* nranks, costa_order* block_order) {
-  if (!layout) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
-  const Layout& L = layout->L;
-  if (nrows) *nrows = L.nrows;
-  if (ncols) *ncols = L.ncols;
-  if (nbr) *nbr = L.nbr;
-  if (nbc) *nbc = L.nbc;
-  if (nranks) *nranks = L.nranks;
-  if (block_order) *block_order = L.order;
-  return COSTA_SUCCESS;
+  return guarded([&]() -> costa_status {
+    if (!layout) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
+    const Layout& L = layout->L;
+    if (nrows) *nrows = L.nrows;
+    if (ncols) *ncols = L.ncols;
+    if (nbr) *nbr = L.nbr;
+    if (nbc) *nbc = L.nbc;
+    if (nranks) *nranks = L.nranks;
+    if (block_order) *block_order = L.order;
+    return COSTA_SUCCESS;
+  });
 }
 
 extern "C" costa_status costa_layout_destroy(costa_layout layout) {
-  if (!layout) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
-  delete layout;
-  return COSTA_SUCCESS;
+  return guarded([&]() -> costa_status {
+    if (!layout) return fail(COSTA_ERROR_INVALID_VALUE, "null layout");
+    delete layout;
+    return COSTA_SUCCESS;
+  });
 }
 
 extern "C" const char* costa_last_error(void) { return g_last_error.c_str(); }

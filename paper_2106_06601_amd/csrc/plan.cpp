@@ -323,7 +323,8 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   lr.piece_begin = (int64_t)hp.pieces.size();
   lr.npieces = (int64_t)ps.size();
   lr.task_begin = (int64_t)hp.tasks.size();
-  if (hp.pieces.size() + ps.size() > (size_t)INT32_MAX) throw std::bad_alloc();
+  if (hp.pieces.size() + ps.size() > (size_t)INT32_MAX)
+    throw LimitExceeded("more than 2^31-1 rectangles in one plan");
   const int32_t base = (int32_t)hp.pieces.size();
   int64_t b = 0;
   // the open run of small row walks
@@ -375,7 +376,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
       g_task = -1;
     }
   }
-  if (b > INT32_MAX) throw std::bad_alloc();
+  if (b > INT32_MAX) throw LimitExceeded("more than 2^31-1 workgroups in one launch");
   lr.ntasks = b;
   // the wide task table of a launch of row walks: kWideTaskUnits units per
   // task, a run of small rectangles still one task
@@ -446,7 +447,7 @@ std::vector<LaunchRange> add_launches(HostPlan& hp, std::vector<Piece>& ps, int 
 template <typename T, typename KeyFn>
 void sort_by_key(std::vector<T>& v, KeyFn key) {
   using K = decltype(key(v[0]));
-  if (v.size() > (size_t)UINT32_MAX) throw std::bad_alloc();
+  if (v.size() > (size_t)UINT32_MAX) throw LimitExceeded("more than 2^32-1 rectangles to order");
   std::vector<std::pair<K, uint32_t>> ix(v.size());
   for (size_t i = 0; i < v.size(); ++i) ix[i] = {key(v[i]), (uint32_t)i};
   std::sort(ix.begin(), ix.end());

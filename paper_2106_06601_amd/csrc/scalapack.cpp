@@ -128,48 +128,60 @@ extern "C" costa_status costa_pxgemr2d(costa_dtype dtype, int32_t m, int32_t n, 
                                        int32_t ja, const int32_t* desca, const costa_grid* grida, void* const* b,
                                        int32_t ib, int32_t jb, const int32_t* descb, const costa_grid* gridb,
                                        hipStream_t stream) {
-  if (dtype != COSTA_R64 && dtype != COSTA_C128 && dtype != COSTA_R32 && dtype != COSTA_C64)
-    return fail(COSTA_ERROR_INVALID_VALUE, "unknown dtype");
-  return scalapack_transform(dtype, COSTA_OP_N, m, n, one_of(dtype), a, ia, ja, desca, grida, zero_of(dtype), b, ib,
-                             jb, descb, gridb, stream);
+  return guarded([&]() -> costa_status {
+    if (dtype != COSTA_R64 && dtype != COSTA_C128 && dtype != COSTA_R32 && dtype != COSTA_C64)
+      return fail(COSTA_ERROR_INVALID_VALUE, "unknown dtype");
+    return scalapack_transform(dtype, COSTA_OP_N, m, n, one_of(dtype), a, ia, ja, desca, grida, zero_of(dtype), b, ib,
+                               jb, descb, gridb, stream);
+  });
 }
 
 extern "C" costa_status costa_pxtran(costa_dtype dtype, costa_op op, int32_t m, int32_t n, const void* alpha,
                                      const void* const* a, int32_t ia, int32_t ja, const int32_t* desca,
                                      const costa_grid* grida, const void* beta, void* const* c, int32_t ic,
                                      int32_t jc, const int32_t* descc, const costa_grid* gridc, hipStream_t stream) {
-  if (op != COSTA_OP_T && op != COSTA_OP_C)
-    return fail(COSTA_ERROR_INVALID_VALUE, "op must be T or C (pxgemr2d copies without transposing)");
-  if (!alpha || !beta) return fail(COSTA_ERROR_INVALID_VALUE, "null alpha or beta");
-  return scalapack_transform(dtype, op, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc, stream);
+  return guarded([&]() -> costa_status {
+    if (op != COSTA_OP_T && op != COSTA_OP_C)
+      return fail(COSTA_ERROR_INVALID_VALUE, "op must be T or C (pxgemr2d copies without transposing)");
+    if (!alpha || !beta) return fail(COSTA_ERROR_INVALID_VALUE, "null alpha or beta");
+    return scalapack_transform(dtype, op, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc, stream);
+  });
 }
 
 extern "C" costa_status costa_pdgemr2d(int32_t m, int32_t n, const void* const* a, int32_t ia, int32_t ja,
                                        const int32_t* desca, const costa_grid* grida, void* const* b, int32_t ib,
                                        int32_t jb, const int32_t* descb, const costa_grid* gridb, hipStream_t stream) {
-  return costa_pxgemr2d(COSTA_R64, m, n, a, ia, ja, desca, grida, b, ib, jb, descb, gridb, stream);
+  return guarded([&]() -> costa_status {
+    return costa_pxgemr2d(COSTA_R64, m, n, a, ia, ja, desca, grida, b, ib, jb, descb, gridb, stream);
+  });
 }
 
 extern "C" costa_status costa_pdtran(int32_t m, int32_t n, const double* alpha, const void* const* a, int32_t ia,
                                      int32_t ja, const int32_t* desca, const costa_grid* grida, const double* beta,
                                      void* const* c, int32_t ic, int32_t jc, const int32_t* descc,
                                      const costa_grid* gridc, hipStream_t stream) {
-  return costa_pxtran(COSTA_R64, COSTA_OP_T, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
-                      stream);
+  return guarded([&]() -> costa_status {
+    return costa_pxtran(COSTA_R64, COSTA_OP_T, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
+                        stream);
+  });
 }
 
 extern "C" costa_status costa_pztranu(int32_t m, int32_t n, const double* alpha, const void* const* a, int32_t ia,
                                       int32_t ja, const int32_t* desca, const costa_grid* grida, const double* beta,
                                       void* const* c, int32_t ic, int32_t jc, const int32_t* descc,
                                       const costa_grid* gridc, hipStream_t stream) {
-  return costa_pxtran(COSTA_C128, COSTA_OP_T, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
-                      stream);
+  return guarded([&]() -> costa_status {
+    return costa_pxtran(COSTA_C128, COSTA_OP_T, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
+                        stream);
+  });
 }
 
 extern "C" costa_status costa_pztranc(int32_t m, int32_t n, const double* alpha, const void* const* a, int32_t ia,
                                       int32_t ja, const int32_t* desca, const costa_grid* grida, const double* beta,
                                       void* const* c, int32_t ic, int32_t jc, const int32_t* descc,
                                       const costa_grid* gridc, hipStream_t stream) {
-  return costa_pxtran(COSTA_C128, COSTA_OP_C, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
-                      stream);
+  return guarded([&]() -> costa_status {
+    return costa_pxtran(COSTA_C128, COSTA_OP_C, m, n, alpha, a, ia, ja, desca, grida, beta, c, ic, jc, descc, gridc,
+                        stream);
+  });
 }

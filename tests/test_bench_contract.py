@@ -16,11 +16,13 @@ def _run(*args, timeout=300):
                           text=True, timeout=timeout)
 
 
+@pytest.mark.spawns
 def test_more_than_one_gpu_is_refused_with_a_message():
     r = _run("--gpus", "2")
     assert r.returncode == 2 and "one GPU" in r.stderr and r.stdout == ""
 
 
+@pytest.mark.spawns
 def test_bad_step_counts_are_refused():
     assert _run("--steps", "0").returncode == 2
     assert _run("--warmup", "-1").returncode == 2

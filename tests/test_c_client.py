@@ -61,6 +61,7 @@ def fresh_client(tmp_path_factory):
 
 
 @pytest.mark.parametrize("k", range(len(CASES)))
+@pytest.mark.spawns
 def test_c_program_agrees_with_the_binding(fresh_client, k):
     A, B, op = CASES[k]
     r = subprocess.run([fresh_client, "host", *_args(A), *_args(B), op], stdout=subprocess.PIPE,

@@ -303,6 +303,14 @@ def test_scalapack_between_grids_of_different_sizes(seed):
     k = SLCase(call, seed=seed, null_idle=True)
     k.run()
     k.check_full()
+    # the volume matrix of the two rank-mapped windows (separable kernels,
+    # ranks outside a grid send or receive nothing) against brute-force counting
+    op = ROUTINE_OP[routine]
+    LA = C.layout_from_spec(dA).submatrix(ia - 1, ja - 1, ra, ca)
+    LC = C.layout_from_spec(dC).submatrix(ic - 1, jc - 1, m, n)
+    V = C.costa_volume_matrix(LC, LA, op)
+    want = oracle.volume_window(oracle.OLayout(dC), ic - 1, jc - 1, oracle.OLayout(dA), ia - 1, ja - 1, m, n, op)
+    assert np.array_equal(V, want)
 
 
 def test_many_windows_pass_the_layout_cache_bound():

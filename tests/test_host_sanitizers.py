@@ -20,6 +20,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 BUILD = os.path.join(ROOT, "_build", "sanitize")
 CLANG = "/opt/rocm/llvm/bin/clang"
 
+pytestmark = pytest.mark.spawns
+
 # host-side modules only (the GPU modules are deselected by the marker)
 MODULES = ["tests/test_library_host.py", "tests/test_scalapack_host.py", "tests/test_relabel_variants.py",
            "tests/test_oracle_pins.py", "tests/test_oracle_scalapack.py", "tests/test_plan_replay.py"]

@@ -206,6 +206,7 @@ def test_plan_waves_respect_workspace_limit():
     assert st["waves"] == 1
 
 
+@pytest.mark.spawns
 def test_one_hip_runtime_whatever_the_import_order():
     """The binding, the seeded fill library and the C client library, loaded
     before anything imports torch, leave one HIP runtime in the process
@@ -230,3 +231,4 @@ print(len({l.split()[-1] for l in maps if "libamdhip64" in l}))
                        timeout=300)
     assert r.returncode == 0, r.stderr[-2000:]
     assert r.stdout.strip().splitlines()[-1] == "1"
+

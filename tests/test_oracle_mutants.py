@@ -20,12 +20,23 @@ PIN_MODULES = ["test_oracle_pins.py", "test_oracle_scalapack.py"]
 C_SRC = "oracle/costa_oracle.c"
 PY_SRC = "oracle/__init__.py"
 
+pytestmark = pytest.mark.spawns
+
 # (name, file, text of the correct code, the mistake planted in its place)
 MUTANTS = [
     ("complex product, real part sign", C_SRC, "r.re = p1 - p2;", "r.re = p1 + p2;"),
     ("complex product, imaginary part sign", C_SRC, "r.im = p3 + p4;", "r.im = p3 - p4;"),
     ("real beta term scales B instead of A", C_SRC, "t2.re = beta.re * a_old.re;", "t2.re = beta.re * b.re;"),
     ("complex beta term uses alpha", C_SRC, "t2 = cmul(beta, a_old);", "t2 = cmul(alpha, a_old);"),
+    ("complex64 product, real part sign", C_SRC, "float t1r = p1 - p2, t1i = p3 + p4;",
+     "float t1r = p1 + p2, t1i = p3 + p4;"),
+    ("complex64 beta term, real part sign", C_SRC, "float t2r = q1 - q2, t2i = q3 + q4;",
+     "float t2r = q1 + q2, t2i = q3 + q4;"),
+    ("complex64 beta term, imaginary part sign", C_SRC, "float t2r = q1 - q2, t2i = q3 + q4;",
+     "float t2r = q1 - q2, t2i = q3 - q4;"),
+    ("complex64 beta imaginary part dropped", C_SRC,
+     "float q1 = beta[0] * a_old[0], q2 = beta[1] * a_old[1], q3 = beta[0] * a_old[1], q4 = beta[1] * a_old[0];",
+     "float q1 = beta[0] * a_old[0], q2 = 0.0f, q3 = beta[0] * a_old[1], q4 = 0.0f;"),
     ("real beta term dropped", C_SRC, "\n  return cadd(t1, t2);\n}", "\n  return t1;\n}"),
     ("alpha = 1 shortcut for any real alpha", C_SRC, "int alpha_one = alpha.re == 1.0 && alpha.im == 0.0;",
      "int alpha_one = alpha.im == 0.0;"),

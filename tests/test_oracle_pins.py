@@ -415,16 +415,19 @@ def _dense_from_single_block(buf, spec):
     return buf.reshape(spec.nrows, spec.ncols)
 
 
-@pytest.mark.parametrize("dtype", ["f64", "c128", "f32"])
+@pytest.mark.parametrize("dtype", ["f64", "c128", "f32", "c64"])
 @pytest.mark.parametrize("op", ["N", "T", "C"])
 @pytest.mark.parametrize("orders", [("col", "col"), ("row", "col"), ("col", "row")])
-@pytest.mark.parametrize("ab", [(1.0, 0.0), (-2.0, 0.0), (2.0, 0.5), (-0.5, 0.25), ((0.5 - 0.25j), (0.25 + 0.5j))])
+@pytest.mark.parametrize("ab", [(1.0, 0.0), (-2.0, 0.0), (2.0, 0.5), (-0.5, 0.25), ((0.5 - 0.25j), (0.25 + 0.5j)),
+                                ((-2 + 0.5j), 0.0), (1.0, (-0.25 + 0.5j))])
 def test_single_rank_reduces_to_dense_numpy(dtype, op, orders, ab):
     """P = 1, one block: the transform is textbook alpha*op(B) + beta*A on the
     dense matrix.  Power-of-two scalars make every product exact, so numpy and
-    the oracle must agree bit for bit whatever the evaluation details."""
+    the oracle must agree bit for bit whatever the evaluation details.  Complex
+    scalars with both parts nonzero (for c128 and c64) reach every term of the
+    complex products, alpha's and beta's."""
     alpha, beta = ab
-    if dtype != "c128" and isinstance(alpha, complex):
+    if dtype not in ("c128", "c64") and (isinstance(alpha, complex) or isinstance(beta, complex)):
         pytest.skip("complex scalars need a complex type")
     M, N = 13, 9
     A = GEN(M, N, [0, M], [0, N], [0], 1, orders[0])
