@@ -258,6 +258,32 @@ typedef struct {
 costa_status costa_transform_batched(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
                                      const int32_t* sigma, hipStream_t stream);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the batched
+ * transform (same arguments, same results bit for bit as
+ * costa_transform_batched) without any device or pinned-host allocation.
+ * Its plan tables, the call's pointer table and the message buffers live in
+ * one static device array of COSTA_NOALLOC_SCRATCH_BYTES per device, held
+ * from the library's loading until the process ends: the first
+ * COSTA_NOALLOC_TABLE_BYTES for the tables, the rest for the messages of one
+ * wave (plans whose messages are larger run in more waves).  Nothing in the
+ * array needs to start at zero.
+ * Limits and errors: as costa_transform_batched(), plus NOT_SUPPORTED, returned
+ * before any device work is enqueued, when the plan's rectangle and task
+ * tables exceed COSTA_NOALLOC_TABLE_BYTES (very many rectangles or
+ * workgroups; costa_transform_batched has no such limit).  No timing events
+ * are recorded (costa_timing_enable does not cover this call).  Host memory
+ * for planning and the plan cache comes from the C++ heap on the first call
+ * of a (layouts, op, sigma, type) combination.
+ * Every call on one device shares that device's array and keeps what the last
+ * call left there: calls that overlap on one device (on different streams, or
+ * from different threads without stream ordering) race and give undefined
+ * results.  Calls on one stream are ordered by the stream. */
+#define COSTA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+#define COSTA_NOALLOC_TABLE_BYTES ((size_t)16 << 20)
+costa_status costa_transform_batched_noalloc(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
+                                             const int32_t* sigma, hipStream_t stream);
+
 /* Caps the message-buffer workspace.  A plan whose messages exceed the cap
  * is executed in waves (pack + unpack per wave).  0 = automatic (a share of
  * the free device memory at planning time).  Affects plans built afterwards. */

@@ -100,6 +100,7 @@ _SIGS = {
                            _P(ctypes.c_double)],
     "costa_transform": [ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp],
     "costa_transform_batched": [ctypes.c_int, _i32, _vp, _vp, _vp],
+    "costa_transform_batched_noalloc": [ctypes.c_int, _i32, _vp, _vp, _vp],
     "costa_set_workspace_limit": [ctypes.c_size_t],
     "costa_plan_stats": [ctypes.c_int, _i32, _vp, _vp, _P(CostaStats)],
     "costa_plan_export": [ctypes.c_int, _i32, _vp, _vp, _vp, _i64, _P(_i64)],
@@ -366,6 +367,23 @@ def costa_transform_batched(dtype: str, descs: Sequence[dict], sigma=None, strea
     s, sp = _sigma(sigma)
     _check(_lib.costa_transform_batched(DTYPES[dtype], len(descs), ctypes.cast(arr, _vp), sp, _stream(stream)),
            "costa_transform_batched")
+
+
+# Size of the static device array of costa_transform_batched_noalloc (per
+# device) and the part of it that holds the plan's tables.
+NOALLOC_SCRATCH_BYTES = 64 << 20
+NOALLOC_TABLE_BYTES = 16 << 20
+
+
+def costa_transform_batched_noalloc(dtype: str, descs: Sequence[dict], sigma=None, stream=None) -> None:
+    """costa_transform_batched without device allocation (tables and messages
+    in the library's static scratch array); same descriptors."""
+    keep: List = []
+    arr = (CostaDesc * len(descs))(*[_desc(dtype, d["op"], d["alpha"], d["beta"], d["A"], d["A_local"], d["B"],
+                                           d["B_local"], keep) for d in descs])
+    s, sp = _sigma(sigma)
+    _check(_lib.costa_transform_batched_noalloc(DTYPES[dtype], len(descs), ctypes.cast(arr, _vp), sp,
+                                                _stream(stream)), "costa_transform_batched_noalloc")
 
 
 def costa_plan_stats(dtype: str, descs: Sequence[dict], sigma=None) -> dict:

@@ -790,6 +790,164 @@ extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, 
   });
 }
 
+// ---------------------------------------------------------------------------
+// The transform that allocates nothing
+// ---------------------------------------------------------------------------
+namespace costa {
+namespace {
+
+constexpr size_t kNoallocBytes = COSTA_NOALLOC_SCRATCH_BYTES;
+constexpr size_t kNoallocTableBytes = COSTA_NOALLOC_TABLE_BYTES;
+constexpr size_t kNoallocMessageBytes = kNoallocBytes - kNoallocTableBytes;
+static_assert(kNoallocTableBytes % 256 == 0 && kNoallocTableBytes < kNoallocBytes, "scratch partition");
+
+// The device memory of costa_transform_batched_noalloc: the plan's tables and
+// the call's pointer table in the first kNoallocTableBytes, the message
+// buffers of one wave in the rest.  Each device holds its own copy until the
+// process ends.  In host code this name is only a stand-in: host code uses
+// the address hipGetSymbolAddress returns on each device.
+static __device__ __align__(256) unsigned char scratch[kNoallocBytes];
+
+// A plan of the no-allocation path: planned for messages of at most
+// kNoallocMessageBytes per wave, with the offsets of its tables in the
+// scratch array.
+struct NoallocPlan {
+  HostPlan host;
+  uint64_t serial = 0;  // tells plans apart when one is rebuilt at a freed address
+  size_t off_tasks = 0, off_wide = 0, off_table = 0, end = 0;
+};
+
+// What one device's scratch array holds.
+struct NoallocDevice {
+  unsigned char* base = nullptr;     // address of `scratch` on the device
+  uint64_t resident = 0;             // serial of the plan whose tables it holds (0: none)
+  std::vector<unsigned char> table;  // the call table it holds
+};
+
+struct NoallocState {
+  std::map<std::string, std::unique_ptr<NoallocPlan>> plans;
+  std::map<int, NoallocDevice> devices;
+  uint64_t next_serial = 1;
+};
+
+NoallocState& noalloc_state() {
+  static NoallocState* s = new NoallocState();
+  return *s;
+}
+
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+// Host plan of a no-allocation call (host memory only; no device call).
+costa_status noalloc_plan(costa_dtype dt, const std::vector<ItemDesc>& items, const std::vector<int32_t>& sig,
+                          NoallocPlan*& out) {
+  NoallocState& N = noalloc_state();
+  const int es = elem_size(dt);
+  std::string key = plan_key(-1, es, items, sig, kNoallocMessageBytes);
+  auto it = N.plans.find(key);
+  if (it == N.plans.end()) {
+    if (N.plans.size() >= 32) N.plans.clear();
+    std::unique_ptr<NoallocPlan> np(new NoallocPlan());
+    build_plan(items, sig, make_config(es),
+               [](int64_t need) { return std::min<int64_t>(need, (int64_t)kNoallocMessageBytes); }, np->host);
+    const HostPlan& hp = np->host;
+    const int32_t P = items.empty() ? 0 : items[0].A->nranks;
+    const size_t nbufs = (size_t)2 * items.size() * P + 1;
+    np->off_tasks = align256(hp.pieces.size() * sizeof(Piece));
+    np->off_wide = np->off_tasks + align256(hp.tasks.size() * sizeof(int32_t));
+    np->off_table = np->off_wide + align256(hp.wide_tasks.size() * sizeof(int32_t));
+    np->end = np->off_table + (nbufs * sizeof(void*) + 63) / 64 * 64 + items.size() * sizeof(ItemParam);
+    np->serial = N.next_serial++;
+    it = N.plans.emplace(key, std::move(np)).first;
+  }
+  NoallocPlan& np = *it->second;
+  if (np.end > kNoallocTableBytes)
+    return fail(COSTA_ERROR_NOT_SUPPORTED, "the plan's tables need " + std::to_string(np.end) +
+                                               " bytes; the no-allocation scratch holds " +
+                                               std::to_string(kNoallocTableBytes) +
+                                               " bytes of tables (costa_transform_batched has no such limit)");
+  if ((size_t)np.host.workspace_bytes > kNoallocMessageBytes)
+    return fail(COSTA_ERROR_NOT_SUPPORTED, "a wave's messages exceed the no-allocation scratch");
+  out = &np;
+  return COSTA_SUCCESS;
+}
+
+// The scratch array of the current device: its address, looked up once per
+// device with that device current.
+costa_status noalloc_device(NoallocDevice*& out) {
+  int device = 0;
+  HIP_OR_FAIL(hipGetDevice(&device));
+  NoallocDevice& d = noalloc_state().devices[device];
+  if (!d.base) {
+    void* ptr = nullptr;
+    HIP_OR_FAIL(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr || (uintptr_t)ptr % 256 != 0) return fail(COSTA_ERROR_DEVICE, "scratch array address is not usable");
+    d.base = static_cast<unsigned char*>(ptr);
+  }
+  out = &d;
+  return COSTA_SUCCESS;
+}
+
+}  // namespace
+}  // namespace costa
+
+extern "C" costa_status costa_transform_batched_noalloc(costa_dtype dtype, int32_t n, const costa_transform_desc* desc,
+                                                        const int32_t* sigma, hipStream_t stream) {
+  return guarded([&]() -> costa_status {
+    std::vector<ItemDesc> items;
+    std::vector<int32_t> sig;
+    costa_status st = validate(dtype, n, desc, sigma, true, items, sig);
+    if (st != COSTA_SUCCESS) return st;
+    State& S = state();
+    std::lock_guard<std::mutex> lock(S.mu);
+    int64_t total = 0;
+    for (const ItemDesc& d : items) total += d.A->nrows * d.A->ncols;
+    if (total == 0) return COSTA_SUCCESS;
+    // planning and the size checks come first: a request that does not fit
+    // is refused before any device call
+    NoallocPlan* np = nullptr;
+    st = noalloc_plan(dtype, items, sig, np);
+    if (st != COSTA_SUCCESS) return st;
+    NoallocDevice* dev = nullptr;
+    st = noalloc_device(dev);
+    if (st != COSTA_SUCCESS) return st;
+    const HostPlan& hp = np->host;
+    unsigned char* base = dev->base;
+    // the plan's tables, unless the scratch holds them already (copies from
+    // pageable host memory: the host data has been taken when the call returns)
+    if (dev->resident != np->serial) {
+      dev->resident = 0;
+      dev->table.clear();
+      if (!hp.pieces.empty())
+        HIP_OR_FAIL(hipMemcpyAsync(base, hp.pieces.data(), hp.pieces.size() * sizeof(Piece), hipMemcpyHostToDevice,
+                                   stream));
+      if (!hp.tasks.empty())
+        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_tasks, hp.tasks.data(), hp.tasks.size() * sizeof(int32_t),
+                                   hipMemcpyHostToDevice, stream));
+      if (!hp.wide_tasks.empty())
+        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_wide, hp.wide_tasks.data(), hp.wide_tasks.size() * sizeof(int32_t),
+                                   hipMemcpyHostToDevice, stream));
+      dev->resident = np->serial;
+    }
+    const int32_t P = items[0].A->nranks;
+    std::vector<unsigned char> table;
+    std::vector<char> reads_a;
+    bool aligned = true;
+    const size_t ptr_bytes = call_table(dtype, n, desc, P, base + kNoallocTableBytes, table, reads_a, aligned);
+    if (table != dev->table) {
+      HIP_OR_FAIL(hipMemcpyAsync(base + np->off_table, table.data(), table.size(), hipMemcpyHostToDevice, stream));
+      dev->table.swap(table);
+    }
+    const ItemParam* ipar = reinterpret_cast<const ItemParam*>(dev->table.data() + ptr_bytes);
+    void* const* d_bufs = reinterpret_cast<void* const*>(base + np->off_table);
+    const ItemParam* d_items = reinterpret_cast<const ItemParam*>(base + np->off_table + ptr_bytes);
+    const DeviceTables tabs{reinterpret_cast<const Piece*>(base),
+                            reinterpret_cast<const int32_t*>(base + np->off_tasks),
+                            reinterpret_cast<const int32_t*>(base + np->off_wide)};
+    // no timing events on this path (creating one may allocate)
+    return launch_plan(S, dtype, hp, tabs, ipar, n, reads_a, aligned, d_bufs, d_items, stream, false);
+  });
+}
+
 extern "C" costa_status costa_timing_enable(int on) {
   return guarded([&]() -> costa_status {
     State& S = state();
@@ -817,7 +975,9 @@ extern "C" costa_status costa_finalize(void) {
     State& S = state();
     {
       std::lock_guard<std::mutex> lock(S.mu);
-      if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty()) HIP_OR_FAIL(hipDeviceSynchronize());
+      NoallocState& N = noalloc_state();
+      if (!S.plans.empty() || !S.ws.empty() || !S.pending.empty() || !N.devices.empty())
+        HIP_OR_FAIL(hipDeviceSynchronize());
       for (const TimingRec& r : S.pending) {  // recorded but never read: their events go too
         (void)hipEventDestroy(r.start);
         (void)hipEventDestroy(r.stop);
@@ -825,6 +985,11 @@ extern "C" costa_status costa_finalize(void) {
       S.pending.clear();
       S.plans.clear();
       S.host_plans.clear();
+      N.plans.clear();
+      for (auto& kv : N.devices) {  // the scratch arrays stay (static); what they hold is forgotten
+        kv.second.resident = 0;
+        kv.second.table.clear();
+      }
       for (auto& kv : S.ws) {
         if (kv.second.ptr) (void)hipFree(kv.second.ptr);
         if (kv.second.last_use) (void)hipEventDestroy(kv.second.last_use);

@@ -20,7 +20,7 @@ BC, GEN = synth.BlockCyclic, synth.General
 def test_every_declared_symbol_is_exported():
     header = open(os.path.join(ROOT, "include", "costa.h")).read()
     names = set(re.findall(r"^\s*(?:costa_status|const char\*)\s+(costa_\w+)\s*\(", header, re.M))
-    assert len(names) == 27  # every entry point of the header
+    assert len(names) == 28  # every entry point of the header
     lib = ctypes.CDLL(C.LIB_PATH)
     missing = [n for n in sorted(names) if not hasattr(lib, n)]
     assert not missing, missing
@@ -232,3 +232,22 @@ print(len({l.split()[-1] for l in maps if "libamdhip64" in l}))
     assert r.returncode == 0, r.stderr[-2000:]
     assert r.stdout.strip().splitlines()[-1] == "1"
 
+
+def test_noalloc_refuses_a_plan_whose_tables_exceed_its_scratch():
+    """costa_transform_batched_noalloc plans before any device call: a plan
+    whose tables pass its table area is refused with NOT_SUPPORTED, one that
+    fits goes on to the device (here: none, so a device error).  The buffer
+    addresses are never dereferenced: without a GPU nothing is launched."""
+    import torch
+    if torch.cuda.device_count() > 0:
+        pytest.skip("with a GPU present the fitting plan would launch its kernels")
+    fake = lambda P: [4096 * (r + 1) for r in range(P)]  # noqa: E731
+    for name, want in (("scaled_transpose_20k", C.NOT_SUPPORTED), ("blocksize_change_16k", C.DEVICE)):
+        w = synth.workload(name)
+        it = w.items[0]
+        P = it.A.nranks
+        d = dict(op=it.op, alpha=it.alpha, beta=it.beta, A=C.layout_from_spec(it.A), A_local=fake(P),
+                 B=C.layout_from_spec(it.B), B_local=fake(P))
+        assert _status(C.costa_transform_batched_noalloc, w.dtype, [d]) == want, name
+        if want == C.NOT_SUPPORTED:
+            assert "bytes of tables" in C.costa_last_error()
