@@ -83,64 +83,85 @@ def _cpu_model() -> str:
     return "unknown"
 
 
+def host_cpus() -> dict:
+    """What the host offers: logical CPUs of the machine, CPUs this process may
+    run on, and the CPU model."""
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = os.cpu_count() or 1
+    return {"nproc": os.cpu_count() or 1, "affinity": affinity, "cpu": _cpu_model()}
+
+
 def cpu_baseline(w, sigma, model_bytes_per_elem: float, target_s: float, threads: int):
-    """The CPU oracle on bands of target rows of pair 0, run by `threads`
-    threads at once (the oracle's C loop runs outside the GIL)."""
+    """The CPU oracle on bands of target rows, run by `threads` threads at once
+    (the oracle's C loop runs outside the GIL).  Pairs of a batch are taken one
+    after another, each for an equal share of `target_s`, with only that pair's
+    buffers in host memory; the figure is the elements of all pairs over the
+    summed time."""
     import threading
     import numpy as np
     import oracle
     import synth
-    it = w.items[0]
-    OA, OB = oracle.OLayout(it.A), oracle.OLayout(it.B)
-    P = it.A.nranks
+    P = w.items[0].A.nranks
     sg = sigma if sigma is not None else list(range(P))
     inv = [0] * P
     for t, r in enumerate(sg):
         inv[r] = t
     npt = oracle.NUMPY[w.dtype]
-    hb = []
-    for s in range(P):
-        b = np.empty(OB.local_elems(s), dtype=npt)
-        oracle.fill(w.dtype, b, w.seed, synth.stream(synth.ROLE_B, 0, s))
-        hb.append(b)
-    ha = []
-    for r in range(P):
-        a = np.empty(OA.local_elems(inv[r]), dtype=npt)
-        oracle.fill(w.dtype, a, w.seed, synth.stream(synth.ROLE_A, 0, r))
-        ha.append(a)
-    M, N = it.A.nrows, it.A.ncols
-    # bands of target rows handed out in order (wrapping around) until
-    # target_s has passed
-    band = max(1, min((M + threads - 1) // threads, (1 << 22) // max(1, N)))
-    nbands = (M + band - 1) // band
-    lock = threading.Lock()
-    state = {"next": 0, "elems": 0}
-    t0 = time.perf_counter()
+    per_item_s = target_s / len(w.items)
+    total_elems, total_s, passes = 0, 0.0, []
+    for k, it in enumerate(w.items):
+        OA, OB = oracle.OLayout(it.A), oracle.OLayout(it.B)
+        hb = []
+        for s in range(P):
+            b = np.empty(OB.local_elems(s), dtype=npt)
+            synth.fill_host_parallel(w.dtype, b, w.seed, synth.stream(synth.ROLE_B, k, s), threads)
+            hb.append(b)
+        ha = []
+        for r in range(P):
+            a = np.empty(OA.local_elems(inv[r]), dtype=npt)
+            synth.fill_host_parallel(w.dtype, a, w.seed, synth.stream(synth.ROLE_A, k, r), threads)
+            ha.append(a)
+        M, N = it.A.nrows, it.A.ncols
+        # bands of target rows handed out in order (wrapping around) until
+        # this pair's share of the time has passed
+        band = max(1, min((M + threads - 1) // threads, (1 << 22) // max(1, N)))
+        nbands = (M + band - 1) // band
+        lock = threading.Lock()
+        state = {"next": 0, "elems": 0}
+        t0 = time.perf_counter()
 
-    def worker():
-        while time.perf_counter() - t0 < target_s:
-            with lock:
-                k = state["next"] % nbands
-                state["next"] += 1
-            r0 = k * band
-            r1 = min(M, r0 + band)
-            oracle.transform(w.dtype, it.op, it.alpha, it.beta, OA, ha, OB, hb, sigma, r0, r1)
-            with lock:
-                state["elems"] += (r1 - r0) * N
+        def worker():
+            while time.perf_counter() - t0 < per_item_s:
+                with lock:
+                    b = state["next"] % nbands
+                    state["next"] += 1
+                r0 = b * band
+                r1 = min(M, r0 + band)
+                oracle.transform(w.dtype, it.op, it.alpha, it.beta, OA, ha, OB, hb, sigma, r0, r1)
+                with lock:
+                    state["elems"] += (r1 - r0) * N
 
-    pool = [threading.Thread(target=worker) for _ in range(threads)]
-    for t in pool:
-        t.start()
-    for t in pool:
-        t.join()
-    dt = time.perf_counter() - t0
-    elems = state["elems"]
-    return {"value": round(elems * model_bytes_per_elem / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{elems} elements of A in pair 0 (bands of {band} target rows of {M}, handed out in order, "
-                      f"{elems / (M * N):.2f} passes over the {M}x{N} matrix) in {dt:.1f} s by {threads} threads; "
-                      f"same bytes-per-element model as the GPU figure",
-            "cpu": _cpu_model(), "seconds": round(dt, 2)}
+        pool = [threading.Thread(target=worker) for _ in range(threads)]
+        for t in pool:
+            t.start()
+        for t in pool:
+            t.join()
+        total_s += time.perf_counter() - t0
+        total_elems += state["elems"]
+        passes.append(state["elems"] / (M * N))
+        del ha, hb
+    it0 = w.items[0]
+    what = (f"bands of target rows of the {it0.A.nrows}x{it0.A.ncols} matrix" if len(w.items) == 1 else
+            f"each of the {len(w.items)} pairs in turn for {per_item_s:.1f} s, only its buffers in host memory; "
+            f"bands of target rows of its {it0.A.nrows}x{it0.A.ncols} matrix")
+    return {"value": round(total_elems * model_bytes_per_elem / total_s / 1e9, 4), "unit": "GB/s",
+            "cores": threads, "kind": "oracle",
+            "sample": f"{total_elems} elements of A ({what}, handed out in order; "
+                      f"{', '.join(f'{p:.2f}' for p in passes)} passes over the matrix) in {total_s:.1f} s by "
+                      f"{threads} threads; same bytes-per-element model as the GPU figure",
+            "seconds": round(total_s, 2), **host_cpus()}
 
 
 def relabel_report() -> dict:
@@ -210,49 +231,321 @@ def bench2_sweep() -> dict:
             "data": "synthetic (volume only)", "matrix": [n, n], "grid": [p, p], "target_block": tb, "sweep": rows}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="blocksize_change_16k")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1),
-                    help="threads of the CPU baseline (default: up to 16, the host share of one GPU)")
-    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
-                    help="before warm-up, run a plain device copy of this many MiB (counter calibration)")
-    ap.add_argument("--relabel-report", action="store_true",
-                    help="print the relabeling comparison of every workload instead of the throughput line")
-    ap.add_argument("--scalapack", metavar="NAME",
-                    choices=["pdgemr2d_16k", "pdtran_16k", "pztranc_8k", "pdgemr2d_scatter_16k"],
-                    help="time a ScaLAPACK-style call through its C entry point instead of the default workload")
-    ap.add_argument("--bench2-sweep", action="store_true",
-                    help="print the volume-reduction sweep of the paper's relabeling benchmark")
-    args = ap.parse_args()
-    if args.steps < 1 or args.warmup < 0:
-        ap.error("--steps must be >= 1 and --warmup >= 0")
-    if args.bench2_sweep:
-        print(json.dumps(bench2_sweep()), flush=True)
-        return
-    if args.relabel_report:
-        print(json.dumps(relabel_report()), flush=True)
-        return
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the transform's virtual ranks all live in "
-              "one GPU's HBM and this build has no multi-GPU exchange", file=sys.stderr)
-        sys.exit(2)
+# --------------------------------------------------------------------------
+# profiles/: summaries of the rocprofv3 runs (the commands are in each file)
+# --------------------------------------------------------------------------
+PROFILE_WORKLOADS = ["reshuffle_transpose_1k", "blocksize_change_16k", "scaled_transpose_20k", "cosma_complex_16k",
+                     "rpa_batched_tall_skinny"]
+PROFILE_CALLS = ["pdgemr2d_16k", "pdgemr2d_scatter_16k", "pdtran_16k", "pztranc_8k"]
+TRAFFIC_WORKLOADS = ["blocksize_change_16k", "scaled_transpose_20k", "cosma_complex_16k", "rpa_batched_tall_skinny",
+                     "pztranc_8k"]
+LDS_WORKLOADS = ["reshuffle_transpose_1k", "cosma_complex_16k", "rpa_batched_tall_skinny", "pdtran_16k",
+                 "pztranc_8k"]
+PMC_READ = "TCC_BUBBLE_sum TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_32B_sum"
+PMC_WRITE = "WRITE_SIZE TCC_EA0_RDREQ_DRAM_32B_sum TCC_EA0_WRREQ_WRITE_DRAM_32B_sum"
+PMC_LDS = "SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS SQ_WAVES SQ_WAVE_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE"
+_MODES = {0: "copy", 1: "scale", 2: "axpby", 3: "per pair"}
+_TEMPLATE_NOTE = ("Kernel template arguments: <scalar, complex, kind (0 pack, 1 unpack-transform, 2 direct), "
+                  "mode (0 copy, 1 scale, 2 axpby, 3 per pair), conjugate, LDS tiles>.")
 
+
+def _bench_args(name: str) -> str:
+    if name in PROFILE_CALLS:
+        return f"--scalapack {name}"
+    return f"--workload {name} --no-cpu-baseline"
+
+
+def profile_commands(name: str, what: str) -> list:
+    """The rocprofv3 commands behind a summary (run from /tmp with TMPDIR=/tmp;
+    <out> is the directory given to --summarize-profiles, <repo> this tree)."""
+    b = f"python3 <repo>/bench.py {_bench_args(name)}"
+    if what == "trace":
+        return [f"rocprofv3 --kernel-trace --stats -f csv -d <out>/trace_{name} -o run -- {b} --steps 20"]
+    if what == "traffic":
+        return [f"rocprofv3 --pmc {PMC_READ} -f csv -d <out>/pmcA_{name} -o run -- {b} --steps 2 --warmup 1 "
+                f"--copy-probe 1024",
+                f"rocprofv3 --pmc {PMC_WRITE} -f csv -d <out>/pmcB_{name} -o run -- {b} --steps 2 --warmup 1 "
+                f"--copy-probe 1024"]
+    return [f"rocprofv3 --pmc {PMC_LDS} -f csv -d <out>/lds_{name} -o run -- {b} --steps 2 --warmup 1"]
+
+
+def _last_json(path: str) -> dict:
+    with open(path) as fh:
+        lines = [x for x in fh.read().splitlines() if x.startswith("{")]
+    return json.loads(lines[-1])
+
+
+def _short_name(name: str) -> str:
+    n = name.strip()
+    if n.startswith("void "):
+        n = n[5:]
+    depth, cut = 0, None
+    for i in range(len(n) - 1, -1, -1):
+        if n[i] == ")":
+            depth += 1
+        elif n[i] == "(":
+            depth -= 1
+            if depth == 0:
+                cut = i
+                break
+    if cut is not None and n.endswith(")"):
+        n = n[:cut]
+    n = n.replace("costa::(anonymous namespace)::", "").replace("costa::", "").replace("(anonymous namespace)::", "")
+    return n if len(n) <= 64 else n[:60]
+
+
+def _mover_args(n: str):
+    import re
+    m = re.match(r"costa_mover(?:_lds)?<(\w+), (\w+), (\d), (\d), (\w+), (\w+)>", n)
+    if not m:
+        return None
+    return {"kind": int(m.group(3)), "mode": int(m.group(4)), "conj": m.group(5) == "true",
+            "tiles": m.group(6) == "true"}
+
+
+def _role(n: str) -> str:
+    a = _mover_args(n)
+    if a:
+        if a["kind"] == 0:
+            return "pack"
+        tags = [_MODES[a["mode"]]] + (["conjugate"] if a["conj"] else []) + (["LDS tiles"] if a["tiles"] else [])
+        base = "unpack-transform (+direct rectangles)" if a["kind"] == 1 else "direct"
+        return f"{base} [{', '.join(tags)}]"
+    if "costa_volume" in n:
+        return "volume matrix (planning, not timed)"
+    if "copyBuffer" in n:
+        return "plan/table upload or copy probe (setup)"
+    if "fill_kernel" in n:
+        return "seeded input fill (setup, not timed)"
+    if n.startswith("at::"):
+        return "torch (setup)"
+    return "other"
+
+
+def _pmc_values(path: str) -> dict:
+    """{counter: {dispatch id: (kernel, value)}} of one --pmc run."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    if len(files) != 1:
+        raise RuntimeError(f"expected one counter_collection.csv under {path}, found {files}")
+    out = {}
+    with open(files[0]) as fh:
+        for r in csv.DictReader(fh):
+            key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+            d = out.setdefault(r["Counter_Name"], {})
+            name, v = d.get(key, (r["Kernel_Name"], 0.0))
+            d[key] = (name, v + float(r["Counter_Value"]))
+    return out
+
+
+def _per_kernel_mean(vals: dict) -> dict:
+    """{short kernel name: (dispatches, mean value)} over the mover kernels."""
+    acc = {}
+    for name, v in vals.values():
+        s = _short_name(name)
+        if _mover_args(s) is None:
+            continue
+        a = acc.setdefault(s, [0, 0.0])
+        a[0] += 1
+        a[1] += v
+    return {k: (n, tot / n) for k, (n, tot) in acc.items()}
+
+
+def _probe_value(vals: dict) -> float:
+    probes = [v for n, v in vals.values() if "copyBuffer" in n]
+    if not probes:
+        raise RuntimeError("no copy probe dispatch in the counter run")
+    return max(probes)
+
+
+def _title(name: str) -> str:
+    if name in PROFILE_CALLS:
+        return f"{name} (ScaLAPACK-style call through its C entry point)"
+    import synth
+    return f"{name} ({synth.workload(name).description})"
+
+
+def summarize_profiles(src: str, out_dir: str = None) -> None:
+    """Writes profiles/*.md (and the counters_*.json that bench.py reads for
+    roofline.traffic) from the rocprofv3 output under `src`: whatever of
+    trace_*, pmcA_*/pmcB_* and lds_* is there."""
+    out_dir = out_dir or os.path.join(ROOT, "profiles")
+    h = kernel_source_hash()
+    stamp = f"Kernel source hash: `{h}` (bench.py's hash of the kernel, planner and launch sources)."
+    wrote = []
+    # kernel traces
+    import csv
+    import glob
+    for name in PROFILE_WORKLOADS + PROFILE_CALLS:
+        stats = glob.glob(os.path.join(src, f"trace_{name}", "**", "*kernel_stats.csv"), recursive=True)
+        if not stats:
+            continue
+        d = _last_json(os.path.join(src, f"trace_{name}.json"))
+        with open(stats[0]) as fh:
+            rows = list(csv.DictReader(fh))
+        lines = [f"# Kernel trace: {_title(name)}", "", "Command (from /tmp with TMPDIR=/tmp, on one MI355X):", "",
+                 "```", *profile_commands(name, "trace"), "```", "",
+                 "Each transform kernel: 1 plan-building call + 20 warm-up + 20 timed steps (times the launches per "
+                 "step).", _TEMPLATE_NOTE, "",
+                 "| kernel | role | calls | average (us) | min (us) | max (us) | share |",
+                 "|---|---|---|---|---|---|---|"]
+        for r in rows:
+            n = _short_name(r["Name"])
+            lines.append(f"| `{n}` | {_role(n)} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                         f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                         f"{float(r['Percentage']):.1f}% |")
+        lines += ["", "Same kernels measured live by bench.py in the same run (HIP events around each launch on the "
+                      "launch stream):", ""]
+        for kind, k in d.get("kernels", {}).items():
+            lines.append(f"- {kind}: {k['ms_per_launch'] * 1000:.1f} us per launch, {k['bytes_per_launch']} "
+                         f"algorithmic bytes -> {k['GB_s']} GB/s ({k['launches_per_step']:g} launches per step)")
+        lines.append(f"- whole step: {d['ms_per_step']} ms for {d['model_bytes_per_step']} model bytes -> "
+                     f"{d['value']} GB/s ({d['pct_of_hbm_peak']}% of 8 TB/s)")
+        r = d["roofline"]
+        lines += [f"- roofline (dominant kernel {r['kernel']}): {r['achieved']} of {r['peak']:g} GB/s, "
+                  f"frac {r['frac']}", "", stamp, ""]
+        path = os.path.join(out_dir, f"kernel_trace_{name}.md")
+        with open(path, "w") as fh:
+            fh.write("\n".join(lines))
+        wrote.append(path)
+    # HBM traffic: FETCH_SIZE from its three inputs, WRITE_SIZE, and the
+    # DRAM-side request counts, each calibrated on the 1 GiB device copy
+    for name in TRAFFIC_WORKLOADS:
+        pa, pb = os.path.join(src, f"pmcA_{name}"), os.path.join(src, f"pmcB_{name}")
+        if not (os.path.isdir(pa) and os.path.isdir(pb)):
+            continue
+        A, B = _pmc_values(pa), _pmc_values(pb)
+        dA = _last_json(os.path.join(src, f"pmcA_{name}.json"))
+
+        def fetch_kib(bub, req, r32):
+            return (bub * 128 + (req - bub - r32) * 64 + r32 * 32) / 1024
+
+        # FETCH_SIZE per dispatch from its inputs
+        fetch = {}
+        for key, (kn, bub) in A["TCC_BUBBLE_sum"].items():
+            req = A["TCC_EA0_RDREQ_sum"][key][1]
+            r32 = A["TCC_EA0_RDREQ_32B_sum"][key][1]
+            fetch[key] = (kn, fetch_kib(bub, req, r32))
+        write = B["WRITE_SIZE"]
+        dram_r = {k: (n, v * 32 / 1024) for k, (n, v) in B["TCC_EA0_RDREQ_DRAM_32B_sum"].items()}
+        dram_w = {k: (n, v * 32 / 1024) for k, (n, v) in B["TCC_EA0_WRREQ_WRITE_DRAM_32B_sum"].items()}
+        copy_kib = 1048576.0
+        pf, pw = _probe_value(fetch), _probe_value(write)
+        pdr, pdw = _probe_value(dram_r), _probe_value(dram_w)
+        ff, wf, drf, dwf = copy_kib / pf, copy_kib / pw, copy_kib / pdr, copy_kib / pdw
+        bub_share = {n: v for n, v in _per_kernel_mean(A["TCC_BUBBLE_sum"]).items()}
+        req_share = _per_kernel_mean(A["TCC_EA0_RDREQ_sum"])
+        r32_share = _per_kernel_mean(A["TCC_EA0_RDREQ_32B_sum"])
+        F, W = _per_kernel_mean(fetch), _per_kernel_mean(write)
+        DR, DW = _per_kernel_mean(dram_r), _per_kernel_mean(dram_w)
+        pb_bub = _probe_value(A["TCC_BUBBLE_sum"])
+        pb_req = _probe_value(A["TCC_EA0_RDREQ_sum"])
+        pb_32 = _probe_value(A["TCC_EA0_RDREQ_32B_sum"])
+        lines = [f"# HBM traffic counters: {_title(name)}", "",
+                 "Commands (from /tmp with TMPDIR=/tmp; one rocprofv3 run per counter group):", "", "```",
+                 *profile_commands(name, "traffic"), "```", "",
+                 "FETCH_SIZE (KiB) = (TCC_BUBBLE x 128 + (TCC_EA0_RDREQ - TCC_BUBBLE - TCC_EA0_RDREQ_32B) x 64 + "
+                 "TCC_EA0_RDREQ_32B x 32) / 1024, rocprofv3's gfx950 definition, computed here from its three "
+                 "inputs; the DRAM counters count 32-byte units of the requests that go to memory (a 64-byte "
+                 "request counts 2, a 128-byte one 4).", "",
+                 f"Calibration on the plain device copy of 1024 MiB (`__amd_rocclr_copyBuffer`, `--copy-probe`): "
+                 f"FETCH_SIZE {pf:.0f} KiB (TCC_BUBBLE {pb_bub:.0f}, TCC_EA0_RDREQ {pb_req:.0f}, 32-byte "
+                 f"{pb_32:.0f}), WRITE_SIZE {pw:.0f} KiB, DRAM reads {pdr:.0f} KiB, DRAM writes {pdw:.0f} KiB, "
+                 f"for 1048576 KiB moved each way: factors {ff:.5f} (fetch), {wf:.5f} (write), {drf:.5f} (DRAM "
+                 f"read), {dwf:.5f} (DRAM write).", "",
+                 "| kernel | role | dispatches | TCC_BUBBLE | TCC_EA0_RDREQ | RDREQ_32B | FETCH_SIZE (KiB) | "
+                 "WRITE_SIZE (KiB) | DRAM read (KiB) | DRAM write (KiB) |",
+                 "|---|---|---|---|---|---|---|---|---|---|"]
+        kinds = {}
+        for s in sorted(F):
+            n, fv = F[s]
+            wv, drv, dwv = W[s][1], DR[s][1], DW[s][1]
+            lines.append(f"| `{s}` | {_role(s)} | {n} | {bub_share[s][1]:.0f} | {req_share[s][1]:.0f} | "
+                         f"{r32_share[s][1]:.0f} | {fv:.0f} | {wv:.0f} | {drv:.0f} | {dwv:.0f} |")
+            k = {0: "pack", 1: "unpack", 2: "direct"}[_mover_args(s)["kind"]]
+            a = kinds.setdefault(k, [0, 0.0, 0.0, 0.0, 0.0])
+            a[0] += n
+            a[1] += fv * n
+            a[2] += wv * n
+            a[3] += drv * n
+            a[4] += dwv * n
+        lines += ["", "Per kernel kind (all launches of the kind; algorithmic bytes from bench.py's per-launch "
+                      "figure of the same run; calibrated bytes = counter x 1024 x the copy's factor):", "",
+                  "| kind | launches | FETCH+WRITE bytes per launch | ratio | DRAM read+write bytes per launch | "
+                  "ratio | algorithmic bytes per launch |", "|---|---|---|---|---|---|---|"]
+        for k, (n, sf, sw, sdr, sdw) in kinds.items():
+            hbm = round((sf / n * ff + sw / n * wf) * 1024)
+            dram = round((sdr / n * drf + sdw / n * dwf) * 1024)
+            alg = dA["kernels"][k]["bytes_per_launch"]
+            lines.append(f"| {k} | {n} | {hbm} | {hbm / alg:.4f} | {dram} | {dram / alg:.4f} | {alg} |")
+            with open(os.path.join(out_dir, f"counters_{k}_{name}.json"), "w") as fh:
+                json.dump({"workload": name, "kernel": k, "kernel_source_hash": h, "fetch_kib": sf / n,
+                           "write_kib": sw / n, "fetch_factor": ff, "write_factor": wf,
+                           "dram_read_kib": sdr / n, "dram_write_kib": sdw / n, "dram_read_factor": drf,
+                           "dram_write_factor": dwf, "hbm_bytes_per_launch": hbm, "dram_bytes_per_launch": dram,
+                           "algorithmic_bytes_per_launch": alg}, fh, indent=1)
+                fh.write("\n")
+        lines += ["", "FETCH_SIZE and WRITE_SIZE count the L2's requests to the memory fabric; part of the fetches "
+                      "can be served by the 256 MB Infinity Cache (MALL) behind it.  `roofline.traffic` in "
+                      "bench.py's line is the FETCH+WRITE figure.", "", stamp, ""]
+        path = os.path.join(out_dir, f"counters_traffic_{name}.md")
+        with open(path, "w") as fh:
+            fh.write("\n".join(lines))
+        wrote.append(path)
+    # LDS bank conflicts and occupancy
+    sections = []
+    for name in LDS_WORKLOADS:
+        pl = os.path.join(src, f"lds_{name}")
+        if not os.path.isdir(pl):
+            continue
+        V = _pmc_values(pl)
+        M = {c: _per_kernel_mean(V[c]) for c in PMC_LDS.split()}
+        sec = [f"## {_title(name)}", "", "```", *profile_commands(name, "lds"), "```", "",
+               "| kernel | dispatches | SQ_INSTS_LDS | SQ_LDS_BANK_CONFLICT | conflicts per LDS instruction | "
+               "SQ_WAVES | SQ_WAVE_CYCLES | GRBM_GUI_ACTIVE | resident waves per CU |",
+               "|---|---|---|---|---|---|---|---|---|"]
+        for s in sorted(M["SQ_WAVES"]):
+            n = M["SQ_WAVES"][s][0]
+            ins, conf = M["SQ_INSTS_LDS"][s][1], M["SQ_LDS_BANK_CONFLICT"][s][1]
+            wc, gui = M["SQ_WAVE_CYCLES"][s][1], M["GRBM_GUI_ACTIVE"][s][1]
+            per = f"{conf / ins:.3f}" if ins else "-"
+            occ = 4 * wc / (gui / 8) / 256 if gui else 0.0
+            sec.append(f"| `{s}` | {n} | {ins:.0f} | {conf:.0f} | {per} | {M['SQ_WAVES'][s][1]:.0f} | {wc:.4g} | "
+                       f"{gui:.4g} | {occ:.1f} |")
+        sections += sec + [""]
+    if sections:
+        lines = ["# LDS bank conflicts and occupancy", "",
+                 "One rocprofv3 --pmc run per workload (from /tmp with TMPDIR=/tmp); counts are per dispatch (mean). "
+                 "SQ_WAVE_CYCLES counts quad-cycles (4 clocks) and GRBM_GUI_ACTIVE is summed over the 8 XCDs "
+                 "(about 8x the kernel's cycles); resident waves per CU = 4 x SQ_WAVE_CYCLES / (GRBM_GUI_ACTIVE / 8) "
+                 "/ 256 CUs.", _TEMPLATE_NOTE, "", *sections, stamp, ""]
+        path = os.path.join(out_dir, "counters_lds_occupancy.md")
+        with open(path, "w") as fh:
+            fh.write("\n".join(lines))
+        wrote.append(path)
+    for p in wrote:
+        print("wrote", os.path.relpath(p, ROOT))
+
+
+# The configurations the default run times, in this order: the block-size
+# change first (the headline figure), the tall-skinny batch last (its 256 GiB
+# of A and B need the device to themselves).
+ALL_WORKLOADS = ["blocksize_change_16k", "reshuffle_transpose_1k", "scaled_transpose_20k", "cosma_complex_16k",
+                 "rpa_batched_tall_skinny"]
+HEADLINE = "blocksize_change_16k"
+NO_BANDWIDTH_CLAIM = {"reshuffle_transpose_1k": "29 MB per step, launch-bound and cache-resident: "
+                                                "correctness case, no bandwidth claim"}
+
+
+def run_workload(name: str, args, cpu_seconds: float, want_copy: bool) -> dict:
+    """Plan, fill, time and (optionally) run the CPU baseline of one workload;
+    frees its device memory and the library's plans before returning."""
     import torch
     import synth
     import paper_2106_06601_amd as C
-
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    if args.scalapack:
-        print(json.dumps(scalapack_bench(args.scalapack, args)), flush=True)
-        return
     torch.cuda.set_device(0)
-    w = synth.workload(args.workload)
+    w = synth.workload(name)
     P = w.items[0].A.nranks
     stream = torch.cuda.current_stream()
     dev = torch.device("cuda:0")
@@ -294,32 +587,111 @@ def main():
             C.costa_transform_batched(w.dtype, descs, sigma, stream)
 
     t_setup = time.perf_counter() - t_plan0
-    m = measure(step, stats, w.name, args)
+    m = measure(step, stats, w.name, args, want_copy)
+    # the device is no longer needed: free it before the CPU leg
+    del A, B, descs, step
+    torch.cuda.synchronize()
+    C.costa_finalize()
+    torch.cuda.empty_cache()
     cpu = None
-    if not args.no_cpu_baseline and len(w.items) == 1:
-        cpu = cpu_baseline(w, sigma, stats["model_bytes"] / stats["total_elems"], args.cpu_seconds,
+    if cpu_seconds > 0:
+        cpu = cpu_baseline(w, sigma, stats["model_bytes"] / stats["total_elems"], cpu_seconds,
                            max(1, args.cpu_threads))
+    rec = {"value": m["value"], "unit": "GB/s", "ms_per_step": m["ms_per_step"],
+           "pct_of_hbm_peak": round(100 * m["value"] / HBM_PEAK_GBS, 2), "dtype": w.dtype,
+           "config": describe(w),
+           "ms_per_step_median": m["ms_per_step_median"], "ms_per_step_min": m["ms_per_step_min"],
+           "model_bytes_per_step": stats["model_bytes"],
+           "bytes_without_staging_per_step": stats["model_bytes"] - 2 * stats["message_bytes"],
+           "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
+           "waves": m["kernels"].get("pack", {}).get("launches_per_step", 0),
+           "plan_s": round(t_setup + m["first_step_s"], 3),
+           "kernels": m["kernels"], "roofline": m["roofline"], "cpu_baseline": cpu}
+    if want_copy:
+        rec["copy_ceiling"] = m["copy_ceiling"]
+    if name in NO_BANDWIDTH_CLAIM:
+        rec["note"] = NO_BANDWIDTH_CLAIM[name]
+    return rec
 
-    out = {
-        "metric": METRIC, "value": m["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": m["ms_per_step"], "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-        "pct_of_hbm_peak": round(100 * m["value"] / HBM_PEAK_GBS, 2),
-        "config": describe(w),
-        "ms_per_step_median": m["ms_per_step_median"], "ms_per_step_min": m["ms_per_step_min"],
-        "model_bytes_per_step": stats["model_bytes"],
-        "bytes_without_staging_per_step": stats["model_bytes"] - 2 * stats["message_bytes"],
-        "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
-        "waves": m["kernels"].get("pack", {}).get("launches_per_step", 0), "plan_s": round(t_setup + m["first_step_s"], 3),
-        "kernels": m["kernels"],
-        "roofline": m["roofline"],
-        "copy_ceiling": m["copy_ceiling"],
-        "cpu_baseline": cpu,
-    }
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="all", choices=["all"] + ALL_WORKLOADS,
+                    help="one workload, or all of them (the headline figure is the block-size change; every "
+                         "workload's figures are under 'configs')")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU-baseline time of a single workload (half of it per workload with 'all', 2 s for "
+                         "the 1024^2 case)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1),
+                    help="threads of the CPU baseline (default: up to 16, the host share of one GPU)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="before warm-up, run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--relabel-report", action="store_true",
+                    help="print the relabeling comparison of every workload instead of the throughput line")
+    ap.add_argument("--scalapack", metavar="NAME",
+                    choices=["pdgemr2d_16k", "pdtran_16k", "pztranc_8k", "pdgemr2d_scatter_16k"],
+                    help="time a ScaLAPACK-style call through its C entry point instead of the default workload")
+    ap.add_argument("--bench2-sweep", action="store_true",
+                    help="print the volume-reduction sweep of the paper's relabeling benchmark")
+    ap.add_argument("--summarize-profiles", metavar="DIR",
+                    help="write the profiles/ summaries from the rocprofv3 output under DIR (no GPU needed)")
+    args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be >= 1 and --warmup >= 0")
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles)
+        return
+    if args.bench2_sweep:
+        print(json.dumps(bench2_sweep()), flush=True)
+        return
+    if args.relabel_report:
+        print(json.dumps(relabel_report()), flush=True)
+        return
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the transform's virtual ranks all live in "
+              "one GPU's HBM and this build has no multi-GPU exchange", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2106_06601_amd  # noqa: F401  (fails loudly when the library is not built)
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.scalapack:
+        print(json.dumps(scalapack_bench(args.scalapack, args)), flush=True)
+        return
+    names = ALL_WORKLOADS if args.workload == "all" else [args.workload]
+    recs = {}
+    for name in names:
+        if len(names) == 1:
+            cs = args.cpu_seconds
+        else:
+            cs = 2.0 if name in NO_BANDWIDTH_CLAIM else args.cpu_seconds / 2
+        if args.no_cpu_baseline:
+            cs = 0.0
+        print(f"bench: {name}", file=sys.stderr, flush=True)
+        recs[name] = run_workload(name, args, cs, want_copy=name == names[0])
+    head = recs[HEADLINE if HEADLINE in recs else names[0]]
+    out = {"metric": METRIC, "value": head["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": head["ms_per_step"], "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": head["dtype"], "data": "synthetic",
+           "pct_of_hbm_peak": head["pct_of_hbm_peak"], "config": head["config"]}
+    for k in ("ms_per_step_median", "ms_per_step_min", "model_bytes_per_step", "bytes_without_staging_per_step",
+              "local_fraction", "waves", "plan_s", "kernels", "roofline", "copy_ceiling", "cpu_baseline"):
+        if k in head:
+            out[k] = head[k]
+    if len(names) > 1:
+        claims = [r for n, r in recs.items() if n not in NO_BANDWIDTH_CLAIM]
+        out["min_pct_of_hbm_peak"] = min(r["pct_of_hbm_peak"] for r in claims)
+        out["min_roofline_frac"] = min(r["roofline"]["frac"] for r in claims)
+        out["configs"] = recs
     print(json.dumps(out), flush=True)
 
 
-def measure(step, stats: dict, workload: str, args) -> dict:
+def measure(step, stats: dict, workload: str, args, want_copy: bool = True) -> dict:
     """Warm-up, then `args.steps` timed steps: per-launch HIP events on the
     launch stream plus one event pair around all steps."""
     import torch
@@ -374,7 +746,8 @@ def measure(step, stats: dict, workload: str, args) -> dict:
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
             "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
     return {"value": round(value, 1), "ms_per_step": round(ms_per_step, 4), "kernels": per_kernel,
-            "roofline": roof, "first_step_s": first_step_s, "copy_ceiling": copy_ceiling(dev, stream),
+            "roofline": roof, "first_step_s": first_step_s,
+            "copy_ceiling": copy_ceiling(dev, stream) if want_copy else None,
             "ms_per_step_median": round(per_step[len(per_step) // 2], 4), "ms_per_step_min": round(per_step[0], 4)}
 
 

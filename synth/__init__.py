@@ -161,6 +161,9 @@ def lib():
         L.synth_fill_host.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
                                       ctypes.c_uint64]
         L.synth_fill_host.restype = ctypes.c_int
+        L.synth_fill_host_range.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
+                                            ctypes.c_uint64, ctypes.c_uint64]
+        L.synth_fill_host_range.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -178,6 +181,28 @@ def fill_host(dtype: str, arr: np.ndarray, seed: int, strm: int) -> None:
     rc = lib().synth_fill_host(DTYPES[dtype], ctypes.c_void_p(arr.ctypes.data), arr.size, seed, strm)
     if rc != 0:
         raise RuntimeError(f"synth_fill_host failed ({rc})")
+
+
+def fill_host_parallel(dtype: str, arr: np.ndarray, seed: int, strm: int, threads: int = 16,
+                       chunk: int = 1 << 22) -> None:
+    """fill_host in chunks on `threads` threads (the C loop runs outside the GIL)."""
+    from concurrent.futures import ThreadPoolExecutor
+    assert arr.flags["C_CONTIGUOUS"] and arr.dtype == NUMPY[dtype]
+    n = arr.size
+    if n == 0:
+        return
+    L = lib()
+    es = arr.itemsize
+    base = arr.ctypes.data
+
+    def part(first: int) -> int:
+        m = min(chunk, n - first)
+        return L.synth_fill_host_range(DTYPES[dtype], ctypes.c_void_p(base + first * es), first, m, seed, strm)
+
+    with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
+        rcs = list(ex.map(part, range(0, n, chunk)))
+    if any(rcs):
+        raise RuntimeError("synth_fill_host_range failed")
 
 
 # --------------------------------------------------------------------------

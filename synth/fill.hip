@@ -93,3 +93,39 @@ extern "C" int synth_fill_host(int dtype, void* dst, uint64_t n, uint64_t seed, 
     default: return 1;
   }
 }
+
+// Host fill of elements [first, first + n) of a buffer: dst[i] gets the value of
+// element first + i (so that several threads can fill one buffer in parts).
+extern "C" int synth_fill_host_range(int dtype, void* dst, uint64_t first, uint64_t n, uint64_t seed,
+                                     uint64_t stream) {
+  if (n > 0 && dst == nullptr) return 1;
+  switch (dtype) {
+    case 0: {
+      double* p = (double*)dst;
+      for (uint64_t i = 0; i < n; ++i) p[i] = synth_f64(seed, stream, first + i);
+      return 0;
+    }
+    case 1: {
+      double* p = (double*)dst;
+      for (uint64_t i = 0; i < n; ++i) {
+        p[2 * i] = synth_c128_re(seed, stream, first + i);
+        p[2 * i + 1] = synth_c128_im(seed, stream, first + i);
+      }
+      return 0;
+    }
+    case 2: {
+      float* p = (float*)dst;
+      for (uint64_t i = 0; i < n; ++i) p[i] = synth_f32(seed, stream, first + i);
+      return 0;
+    }
+    case 3: {
+      float* p = (float*)dst;
+      for (uint64_t i = 0; i < n; ++i) {
+        p[2 * i] = synth_c64_re(seed, stream, first + i);
+        p[2 * i + 1] = synth_c64_im(seed, stream, first + i);
+      }
+      return 0;
+    }
+    default: return 1;
+  }
+}

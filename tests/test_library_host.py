@@ -251,3 +251,15 @@ def test_noalloc_refuses_a_plan_whose_tables_exceed_its_scratch():
         assert _status(C.costa_transform_batched_noalloc, w.dtype, [d]) == want, name
         if want == C.NOT_SUPPORTED:
             assert "bytes of tables" in C.costa_last_error()
+
+
+@pytest.mark.parametrize("dtype", ["f64", "c128", "f32", "c64"])
+def test_parallel_host_fill_equals_the_oracle_fill(dtype):
+    """The chunked multi-threaded host fill (used for the CPU baseline's
+    inputs) gives the generator's values, element for element."""
+    n = 10007
+    a = np.zeros(n, dtype=oracle.NUMPY[dtype])
+    synth.fill_host_parallel(dtype, a, 99, synth.stream(synth.ROLE_A, 5, 3), threads=4, chunk=1000)
+    b = np.zeros(n, dtype=oracle.NUMPY[dtype])
+    oracle.fill(dtype, b, 99, synth.stream(synth.ROLE_A, 5, 3))
+    assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
