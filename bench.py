@@ -194,8 +194,48 @@ def relabel_report() -> dict:
                      "remote_reduction_greedy_pct": round(100 * (kept_g - kept_id) / max(1, total - kept_id), 3),
                      "greedy_gap_pct_of_exact_gain": round(100 * (kept_e - kept_g) / max(1, kept_e - kept_id), 3),
                      "volume_ms": round(t_v * 1e3, 3), "exact_ms": round(t_e * 1e3, 3), "greedy_ms": round(t_g * 1e3, 3)}
+    # random layouts: two independent random general grids (random cuts, random
+    # owners) of an 8192^2 matrix; greedy against exact under the locally-free
+    # cost and under a two-level topology cost (nodes of 8 ranks)
+    import numpy as np
+    rand = []
+    for P in (8, 16, 32, 64, 128, 256):
+        rows = []
+        for seed in range(5):
+            A, B = synth.random_layout_pair(P, 1000 * P + seed, n=8192)
+            V = C.costa_volume_matrix(C.layout_from_spec(A), C.layout_from_spec(B), "N")
+            _, kept_id, kept_e = C.costa_relabel(V)
+            _, _, after_g = C.costa_relabel_cost(V, method="greedy")
+            kept_g = int(V.sum()) - int(after_g)
+            node = np.arange(P) // 8
+            same = node[:, None] == node[None, :]
+            L = np.where(same, 0.0, 5.0)
+            Bw = np.where(same, 1.0, 8.0)
+            np.fill_diagonal(Bw, 0.0)
+            _, w0, we = C.costa_relabel_cost(V, 8.0, L, Bw, "exact")
+            _, _, wg = C.costa_relabel_cost(V, 8.0, L, Bw, "greedy")
+            rows.append((kept_id, kept_e, kept_g, w0, we, wg))
+        share = [100 * (g - i) / max(1, e - i) for i, e, g, *_ in rows]
+        tshare = [100 * (w0 - wg) / (w0 - we) if w0 > we else 100.0 for *_, w0, we, wg in rows]
+        rand.append({"P": P, "layouts": len(rows),
+                     "local_identity_mean": round(float(np.mean([r[0] for r in rows])), 1),
+                     "local_exact_mean": round(float(np.mean([r[1] for r in rows])), 1),
+                     "local_greedy_mean": round(float(np.mean([r[2] for r in rows])), 1),
+                     "greedy_share_of_exact_gain_pct": {"mean": round(float(np.mean(share)), 2),
+                                                        "min": round(float(np.min(share)), 2)},
+                     "topology_cost_reduction_exact_pct": round(float(np.mean([100 * (r[3] - r[4]) / r[3]
+                                                                                for r in rows])), 2),
+                     "topology_cost_reduction_greedy_pct": round(float(np.mean([100 * (r[3] - r[5]) / r[3]
+                                                                                 for r in rows])), 2),
+                     "topology_greedy_share_of_exact_gain_pct": {"mean": round(float(np.mean(tshare)), 2),
+                                                                 "min": round(float(np.min(tshare)), 2)}})
     return {"metric": "relabeling: local volume kept (identity / exact / greedy)", "unit": "elements",
-            "data": "synthetic", "workloads": out}
+            "data": "synthetic", "workloads": out,
+            "random_layouts": {"matrix": [8192, 8192], "source and target": "independent random general grids "
+                               "(about 2 sqrt(P) random cuts per dimension, owners uniform over P)",
+                               "topology": "nodes of 8 ranks: latency 0 and 1 unit/byte within a node, latency "
+                                           "5 and 8 units/byte between nodes, 8-byte elements",
+                               "rows": rand}}
 
 
 def bench2_sweep() -> dict:

@@ -342,6 +342,22 @@ def _cosma_like(n: int, g: int) -> General:
     return General(n, n, splits, splits, owners, g * g, "col")
 
 
+def random_layout_pair(P: int, seed: int, n: int = 4096, cuts: int = None) -> tuple:
+    """Two independent random general grids of an n x n matrix over P ranks
+    (the relabeling comparison's "random layouts"): `cuts` distinct random
+    interior cut points per dimension (default about 2 sqrt(P)), every block's
+    owner drawn uniformly from the P ranks.  Returns (target A, source B)."""
+    if cuts is None:
+        cuts = max(1, int(round(2 * P ** 0.5)))
+    out = []
+    for role in (0, 1):
+        rs = [0] + random_cuts(seed, stream(4, role, 0), n, cuts) + [n]
+        cs = [0] + random_cuts(seed, stream(4, role, 1), n, cuts) + [n]
+        owners = random_owners(seed, stream(4, role, 2), (len(rs) - 1) * (len(cs) - 1), P)
+        out.append(General(n, n, rs, cs, owners, P, "col"))
+    return out[0], out[1]
+
+
 def workload(name: str, scale: str = "full", seed: int = DEFAULT_SEED) -> Workload:
     """The five workloads at full size ('full') or at a reduced size with the same
     grids, block sizes and ragged structure ('small', for element-wise parity)."""

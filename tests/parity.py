@@ -128,6 +128,50 @@ class Case:
                                          f"{bad[:5]}: got {got.ravel()[bad[:3] % max(1, got.size)]} "
                                          f"expected {exp.ravel()[bad[:3] % max(1, exp.size)]}")
 
+    def check_rows(self, k: int, row_begin: int = 0, row_end=None, ranks=None, threads: int = 16):
+        """Every element of the given physical ranks of pair k (default: all of
+        them) equal, bit for bit, to the oracle's result, which is computed on
+        bands of the target rows [row_begin, row_end) by `threads` host
+        threads at once (disjoint rows write disjoint elements).  The ranks
+        compared must hold no element outside those rows.  Host inputs come
+        from the generator, filled on the same threads."""
+        from concurrent.futures import ThreadPoolExecutor
+        torch.cuda.synchronize()
+        it = self.w.items[k]
+        npt = oracle.NUMPY[self.dtype]
+        row_end = it.A.nrows if row_end is None else row_end
+        ranks = list(range(self.P)) if ranks is None else list(ranks)
+        hb = []
+        for s in range(self.P):
+            b = np.empty(self.OB[k].local_elems(s), dtype=npt)
+            synth.fill_host_parallel(self.dtype, b, self.w.seed, synth.stream(synth.ROLE_B, k, s), threads)
+            hb.append(b)
+        ha = []
+        for r in range(self.P):
+            a = np.empty(self.OA[k].local_elems(self.inv[r]), dtype=npt)
+            if self.a_init == "gen":
+                synth.fill_host_parallel(self.dtype, a, self.w.seed, synth.stream(synth.ROLE_A, k, r), threads)
+            else:
+                a[:] = np.nan
+            ha.append(a)
+        N = it.A.ncols
+        band = max(1, min(1024, (1 << 21) // max(1, N)))
+        bands = [(r0, min(row_end, r0 + band)) for r0 in range(row_begin, row_end, band)]
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(lambda b: oracle.transform(self.dtype, it.op, it.alpha, it.beta, self.OA[k], ha,
+                                                   self.OB[k], hb, self.sigma, b[0], b[1]), bands))
+        del hb
+        checked = 0
+        for r in ranks:
+            got = bits(self.A[k][r].cpu().numpy(), self.dtype)
+            exp = bits(ha[r], self.dtype)
+            if not np.array_equal(got, exp):
+                bad = np.nonzero(got != exp)[0]
+                raise AssertionError(f"pair {k} rank {r}: {bad.size} of {exp.size} elements differ; first at "
+                                     f"{bad[:5]}")
+            checked += ha[r].size
+        return checked
+
     def sample_points(self, k: int, n_random: int, n_corners: int, seed: int = 0):
         """Random points plus first/last rows and columns of overlay intervals."""
         it = self.w.items[k]

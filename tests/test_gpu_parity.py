@@ -99,8 +99,9 @@ def test_workload_full_size_sampled(name):
     assert n > 100000
     if beta0:
         case.check_all_written()
-    if name == "reshuffle_transpose_1k":
-        case.check_full()
+    # every element of every rank, the oracle run on bands of rows on 16 host threads
+    _say(f"transform {name} full size: every element")
+    assert case.check_rows(0) == w.items[0].A.nrows * w.items[0].A.ncols
     case.free()
 
 
@@ -115,6 +116,15 @@ def test_workload_rpa_full_size_sampled():
     case.run()
     n = case.check_sampled(n_random=50000, n_corners=100000)
     assert n > 100000
+    # every element of the eight ranks of process row 0 (target rows 0..511,
+    # one block row of 512 x 524288, written by every wave) of an identity
+    # pair and a transposed pair
+    it = w.items[0]
+    assert it.A.prow == 8 and it.A.mb == 512 and it.A.nrows == 4096 and it.A.rank_order == "row"
+    for k in (0, 4):
+        _say(f"transform rpa_batched_tall_skinny full size: every element of ranks 0-7 of pair {k}")
+        assert w.items[k].op == ("N" if k == 0 else "T")
+        assert case.check_rows(k, 0, 512, ranks=range(8)) == 512 * 524288
     case.free()
 
 
