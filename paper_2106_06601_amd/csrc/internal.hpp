@@ -124,12 +124,14 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 //   src_off + x*src_ld + y   (flag TRANSPOSE set: contiguous along y).
 // PIECE_WIDE: a non-transposed rectangle whose offsets, strides and width
 //   allow 16-byte vectors.
-// PIECE_GROUP_NEXT: the next rectangle of the launch is moved by the same
-//   workgroup (a run of small rectangles shares one workgroup).
+// PIECE_GROUP_NEXT: the next rectangle of the launch continues this one's
+//   segment (its units follow this one's in the tasks that cover them).
 // A transposed rectangle is moved in LDS tiles of tile_x x tile_y elements
 // (tile_x along the destination's contiguous direction; choose_tile below),
 // packed into `aux` with tile_pack.
-enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_GROUP_NEXT = 16 };
+// PIECE_TILE_COLS: the tiles of a transposed rectangle are numbered down its
+//   tile columns (y first) instead of along its tile rows (x first).
+enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_TILE_COLS = 4, PIECE_GROUP_NEXT = 16 };
 
 struct alignas(16) Piece {
   int64_t src_off;
@@ -145,58 +147,87 @@ struct alignas(16) Piece {
   int32_t task0;    // first workgroup of its launch that moves it
   int32_t aux;      // transposed rectangles: tile_pack(tile_x, tile_y); row walks in a
                     // launch without tiles: its first task in the launch's wide task table
+                    // (task0 and the wide task are for inspection; the kernels read the
+                    // task tables)
 };
 static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
 
 // Work of one workgroup (kThreadsPerTask lanes): one LDS tile of a
-// transposed rectangle, kThreadsPerTask units (16-byte vectors, or single
-// elements when the rectangle is not PIECE_WIDE) of a rectangle walked along
-// its rows, or a run of small rectangles moved at once.  A launch of row
-// walks also has a wide task table whose tasks are kWideTaskUnits units (a
-// run still one task); launches that copy use it, two units per lane.
+// transposed rectangle, or kThreadsPerTask units (16-byte vectors, or single
+// elements when the rectangle is not PIECE_WIDE) of a segment of row walks
+// (rectangles whose units are numbered one after another, see plan.cpp).  A
+// launch of row walks also has a wide task table whose tasks are
+// kWideTaskUnits units; launches that copy use it, two units per lane.
 constexpr int32_t kThreadsPerTask = 256;
 #ifndef COSTA_COPY_UNITS
 #define COSTA_COPY_UNITS 2  // units per lane in launches of row walks that copy
 #endif
 constexpr int32_t kWideTaskUnits = (COSTA_COPY_UNITS > 1 ? COSTA_COPY_UNITS : 2) * kThreadsPerTask;
-constexpr int32_t kGroupUnitsMax = 128;  // rectangles of at most this many units may share a workgroup
-constexpr int32_t kGroupPiecesMax = 8;
+constexpr int32_t kGroupUnitsMax = 128;  // without flat tasks: rectangles of at most this many units
+constexpr int32_t kGroupPiecesMax = 8;   // (at most this many) may share a workgroup
 
 // Elements per 16-byte unit of a PIECE_WIDE rectangle.
 constexpr int32_t wide_elems(int32_t es) { return es >= 16 ? 1 : 16 / es; }
 
-// LDS tiles of transposed rectangles.  A tile holds at most
-// tile_budget(es) elements and is at most tile_max_x(es) wide; its rows (one
-// per x) take tile_y | 1 elements in LDS, an odd stride, so that lanes
-// reading one LDS row element each (consecutive x) hit distinct banks.
-// Small rectangles are one tile; larger ones are cut into tiles of equal
-// width (at most tile_max_x) and equal height (as many rows as the budget
-// allows), so that every lane of a workgroup has an element.
+// LDS tiles of transposed rectangles.  A tile is at most tile_max_x(es)
+// wide; its rows (one per x) take tile_y | 1 elements in LDS -- an odd
+// stride, so that lanes reading one LDS row element each (consecutive x) hit
+// distinct banks -- and all of them fit the tile's LDS array of
+// tile_lds_elems(es) elements.  Small rectangles are one tile; larger ones
+// are cut into tiles of equal width (at most tile_max_x) and equal height.
+// When the rectangle's source columns start on 128-byte lines the height is
+// what tile_budget(es) elements allow (for the usual shapes a whole number of
+// lines per column, so no tile shares a line with the one below it, and the
+// lanes storing a column to LDS do not straddle two columns).  Otherwise the
+// height is odd and as large as the LDS array allows: the rows then need no
+// padding, so the lanes storing a tile's columns one after another write
+// consecutive LDS addresses (padded rows would make each group of lanes that
+// crosses a column end hit one bank twice).
 #ifndef COSTA_TILE_BUDGET16
 #define COSTA_TILE_BUDGET16 3072  // three workgroups per CU (4096: two, -1 to -9%; 2048: four, shorter tiles)
 #endif
 #ifndef COSTA_TILE_MAXX16
 #define COSTA_TILE_MAXX16 256
 #endif
+#ifndef COSTA_ODD_TILES
+#define COSTA_ODD_TILES 0  // 1: cut tiles of misaligned columns with an odd height that fills the LDS array
+#endif
 constexpr int32_t tile_budget(int32_t es) { return es >= 16 ? COSTA_TILE_BUDGET16 : es == 8 ? 2048 : 4096; }
 constexpr int32_t tile_max_x(int32_t es) { return es >= 16 ? COSTA_TILE_MAXX16 : 128; }
 constexpr int32_t tile_lds_elems(int32_t es) { return tile_budget(es) + tile_max_x(es); }
+// Elements of the largest tile (what a workgroup's lanes must cover).
+constexpr int32_t tile_max_elems(int32_t es) { return COSTA_ODD_TILES ? tile_lds_elems(es) : tile_budget(es); }
 constexpr int32_t tile_pack(int32_t tx, int32_t ty) { return tx | ty << 16; }
 constexpr int32_t tile_x_of(int32_t t) { return t & 0xffff; }
 constexpr int32_t tile_y_of(int32_t t) { return t >> 16; }
-inline void choose_tile(int32_t es, int32_t nx, int32_t ny, int32_t& tx, int32_t& ty) {
-  const int32_t budget = tile_budget(es), maxx = tile_max_x(es);
-  if (nx <= maxx && (int64_t)nx * ny <= budget) {
+// aligned_cols: the source columns (runs along y) start on 128-byte lines.
+inline void choose_tile(int32_t es, int32_t nx, int32_t ny, bool aligned_cols, int32_t& tx, int32_t& ty) {
+  const int32_t maxx = tile_max_x(es);
+  const bool odd = COSTA_ODD_TILES && !aligned_cols;
+  const int32_t cap = tile_lds_elems(es), budget = tile_budget(es);
+  if (nx <= maxx && (odd ? (int64_t)nx * (ny | 1) <= cap : (int64_t)nx * ny <= budget)) {
     tx = nx;
     ty = ny;
     return;
   }
   const int32_t ntx = (nx + maxx - 1) / maxx;
   tx = (nx + ntx - 1) / ntx;
-  ty = budget / tx;
-  if (ty > ny) ty = ny;
-  const int32_t nty = (ny + ty - 1) / ty;
+  if (!odd) {
+    ty = budget / tx;
+    if (ty > ny) ty = ny;
+    const int32_t nty = (ny + ty - 1) / ty;
+    ty = (ny + nty - 1) / nty;
+    return;
+  }
+  int32_t tymax = cap / tx;  // >= 1: tx <= maxx < cap
+  if (tymax > 1 && tymax % 2 == 0) --tymax;  // odd: rows without padding
+  if (ny <= tymax) {
+    ty = ny;  // one tile row: (ny | 1) <= tymax since tymax is odd (or 1)
+    return;
+  }
+  const int32_t nty = (ny + tymax - 1) / tymax;
   ty = (ny + nty - 1) / nty;
+  if (ty % 2 == 0 && ty < tymax) ++ty;  // keeps at most nty tiles, the last one shorter
 }
 
 // Per-pair parameters of a call, read by the kernels.
@@ -221,7 +252,7 @@ struct LaunchRange {
   int64_t wide_begin = 0, nwide = 0;  // wide task table (launches without tiles; 0 tasks otherwise)
   int64_t elems = 0;
   bool has_transpose = false;
-  int32_t xcd_ranges = 0;  // 1: each XCD takes one contiguous range of the launch's tasks
+  int32_t xcd_ranges = 0;  // 1: each XCD takes one contiguous range of the launch's tasks; K >= 2: runs of K
   std::vector<int64_t> item_elems;  // elements of each pair in this launch
 };
 
@@ -243,15 +274,18 @@ struct LaunchSpec {
   int32_t conj;
   bool has_transpose;
 };
-// pieces: the plan's rectangles (global indices); tasks: the launch's
-// ntasks entries, wide: its wide task table (nwide entries, 0 in launches
-// with tiles).
+// pieces: the plan's rectangles (global indices); tasks / offs: the launch's
+// ntasks entries (the rectangle a task starts in, and its tile or first unit
+// there), wide / wide_offs: its wide task table (nwide entries, 0 in
+// launches with tiles).
 // xcd_ranges: 0 runs task b in workgroup b (workgroups are dispatched
 // round-robin over the 8 XCDs); 1 hands each XCD one contiguous range of the
-// tasks of each launch slice.
+// tasks of each launch slice; K >= 2 hands each XCD runs of K consecutive
+// tasks.
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
-                        const int32_t* tasks, int64_t ntasks, const int32_t* wide, int64_t nwide, void* const* bufs,
-                        const ItemParam* items, int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream);
+                        const int32_t* tasks, const int32_t* offs, int64_t ntasks, const int32_t* wide,
+                        const int32_t* wide_offs, int64_t nwide, void* const* bufs, const ItemParam* items,
+                        int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream);
 
 struct VolumeArgs {
   const Interval* rows;

@@ -43,14 +43,24 @@ constexpr int kThreads = kThreadsPerTask;
 // The task of workgroup b of n.  Workgroups are dispatched round-robin over
 // the 8 XCDs (b % 8 is b's XCD).  ranges 0: task b.  ranges 1: XCD x takes
 // the x-th of 8 contiguous ranges of tasks, workgroup b the (b/8)-th task of
-// its XCD's range.
+// its XCD's range.  ranges K >= 2: runs of K consecutive tasks per XCD --
+// each block of 8K workgroups takes a block of 8K tasks, XCD x the K tasks
+// from x*K (the tail that fills no block keeps dispatch order) -- so that
+// neighbouring tasks, which share cache lines at their edges, meet in one
+// XCD's L2.
 __device__ __forceinline__ int32_t xcd_order(int32_t b, int32_t n, int32_t ranges) {
   constexpr int32_t X = 8;
   if (!ranges) return b;
-  const int32_t q = n / X, r = n % X;
-  const int32_t xcd = b % X, idx = b / X;
-  const int32_t start = xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q;
-  return start + idx;
+  if (ranges == 1) {
+    const int32_t q = n / X, r = n % X;
+    const int32_t xcd = b % X, idx = b / X;
+    const int32_t start = xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q;
+    return start + idx;
+  }
+  const int32_t blk = X * ranges;
+  if (b >= n - n % blk) return b;
+  const int32_t j = b % blk;
+  return b - j + (j % X) * ranges + j / X;
 }
 
 template <typename S, int N>
@@ -151,7 +161,7 @@ struct TypeTraits {
   static constexpr int WIDE_NEL = wide_elems(ES); // elements per 16-byte unit
   static constexpr bool NT_WALK = COSTA_NT_LOADS && ES <= COSTA_NT_LOADS_MAX_ES;
   static constexpr int LDS_ELEMS = tile_lds_elems(ES);
-  static constexpr int TILE_PASSES = tile_budget(ES) / kThreads;  // elements per lane of a full tile
+  static constexpr int TILE_PASSES = (tile_max_elems(ES) + kThreads - 1) / kThreads;  // elements per lane
 };
 
 // y = u / n and x = u - y*n from a float estimate of the quotient, corrected
@@ -169,15 +179,16 @@ __device__ __forceinline__ void divmod(int32_t u, int32_t n, int32_t& y, int32_t
   }
 }
 
-// Row walk: dst[y*dst_ld + x] = f(src[y*src_ld + x]).  Task c of the
-// rectangle covers units [c*UL*kThreads, (c+1)*UL*kThreads) of its
-// flattened (y, x) index (a unit is a 16-byte vector for PIECE_WIDE
-// rectangles, else one element); lane l takes units l + k*kThreads, k < UL.
-// A run of small rectangles (PIECE_GROUP_NEXT) is flattened the same way:
-// lane l takes unit l of the run.  A lane issues all its loads (and those of
-// A when it is read) before its stores.
+// Row walk: dst[y*dst_ld + x] = f(src[y*src_ld + x]).  The task starts at
+// unit u0 of rectangle pi (a unit is a 16-byte vector for PIECE_WIDE
+// rectangles, else one element; the flattened (y, x) index of a rectangle
+// numbers its units) and covers the next UL*kThreads units of its segment,
+// continuing into the following rectangles while they carry on the segment
+// (PIECE_GROUP_NEXT); lane l takes units u0 + l + k*kThreads, k < UL.  A
+// lane issues all its loads (and those of A when it is read) before its
+// stores.
 template <typename S, bool CPLX, int MODE, bool CONJ, int UL>
-__device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int32_t pi, int32_t c,
+__device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int32_t pi, int32_t u0,
                                           void* const* __restrict__ bufs, int32_t allow_wide, S ar, S ai, S br,
                                           S bi) {
   using TT = TypeTraits<S, CPLX>;
@@ -190,25 +201,27 @@ __device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int3
   int64_t soffs[UL], doffs[UL];
 #pragma unroll
   for (int k = 0; k < UL; ++k) {
-    int32_t u = c * (UL * kThreads) + k * kThreads + (int32_t)threadIdx.x;
+    int32_t u = u0 + k * kThreads + (int32_t)threadIdx.x;
     int64_t soff = -1, doff = 0;
     int32_t sbuf = 0, dbuf = 0;
     int32_t q = pi;
-    while (true) {
-      const Piece& p = pieces[q];
-      const int32_t nxu = wide ? p.nx / W : p.nx;
-      const int32_t units = nxu * p.ny;
-      if (u >= 0 && u < units) {
-        int32_t y, x;
-        divmod(u, nxu, y, x);
-        soff = p.src_off + (int64_t)y * p.src_ld + (int64_t)x * epu;
-        doff = p.dst_off + (int64_t)y * p.dst_ld + (int64_t)x * epu;
-        sbuf = p.src_buf;
-        dbuf = p.dst_buf;
-      }
+    int32_t nxu = wide ? pieces[q].nx / W : pieces[q].nx;
+    int32_t units = nxu * pieces[q].ny;
+    // the rectangle of the segment that holds unit u (a task spans few)
+    while (u >= units && (pieces[q].flags & PIECE_GROUP_NEXT)) {
       u -= units;
-      if (!(p.flags & PIECE_GROUP_NEXT)) break;
       ++q;
+      nxu = wide ? pieces[q].nx / W : pieces[q].nx;
+      units = nxu * pieces[q].ny;
+    }
+    if (u < units) {
+      const Piece& p = pieces[q];
+      int32_t y, x;
+      divmod(u, nxu, y, x);
+      soff = p.src_off + (int64_t)y * p.src_ld + (int64_t)x * epu;
+      doff = p.dst_off + (int64_t)y * p.dst_ld + (int64_t)x * epu;
+      sbuf = p.src_buf;
+      dbuf = p.dst_buf;
     }
     soffs[k] = soff;
     doffs[k] = doff;
@@ -257,7 +270,8 @@ __device__ __forceinline__ void move_walk(const Piece* __restrict__ pieces, int3
 }
 
 // One LDS tile of a rectangle whose source runs along y while the
-// destination runs along x: tile c (tiles numbered along x first) of
+// destination runs along x: tile c (tiles numbered along x first, or down
+// the tile columns with PIECE_TILE_COLS) of
 // tile_x x tile_y elements, cut at the rectangle's edges to w x h.  Loads
 // take the tile's elements in source order (y fastest: runs of h elements),
 // stores in destination order (x fastest: runs of w elements); lanes walk
@@ -278,8 +292,16 @@ __device__ __forceinline__ void move_tile(const Piece* __restrict__ pieces, int3
   const int32_t tid = threadIdx.x;
   const int32_t tx = tile_x_of(p.aux), ty = tile_y_of(p.aux);
   const int32_t stride = ty | 1;
-  const int32_t ntx = (p.nx + tx - 1) / tx;
-  const int32_t x0 = (c % ntx) * tx, y0 = (c / ntx) * ty;
+  int32_t x0, y0;
+  if (p.flags & PIECE_TILE_COLS) {
+    const int32_t nty = (p.ny + ty - 1) / ty;
+    x0 = (c / nty) * tx;
+    y0 = (c % nty) * ty;
+  } else {
+    const int32_t ntx = (p.nx + tx - 1) / tx;
+    x0 = (c % ntx) * tx;
+    y0 = (c / ntx) * ty;
+  }
   const int32_t w = min(tx, p.nx - x0), h = min(ty, p.ny - y0);
   const int32_t n = w * h;
   const E* __restrict__ se = reinterpret_cast<const E*>(bufs[p.src_buf]) + p.src_off + (int64_t)x0 * p.src_ld + y0;
@@ -353,26 +375,27 @@ __device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int3
 constexpr int MODE_ANY = 3;
 
 // One launch slice: workgroup b moves task task_off + xcd_order(b) of the
-// launch's task table.
+// launch's task table (tasks: the rectangle a task starts in; offs: its tile
+// or its first unit there).
 //   KIND: pack (bitwise copy into message buffers, never transposed),
 //         unpack-transform, or direct.
 //   MODE: the arithmetic of every pair of the call, or MODE_ANY to read it
 //         per workgroup (batches that mix modes; a workgroup's rectangles
 //         belong to one pair); CONJ likewise.
 //   HAS_T: whether the launch contains transposed rectangles (LDS tiles).
-//   UL: units per lane of its row walks; with UL = 2 the table is the
-//       launch's wide task table, whose first task of a rectangle is in aux.
+//   UL: units per lane of its row walks; with UL = 2 the tables are the
+//       launch's wide task tables (tasks of kWideTaskUnits units).
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T, int UL>
 __device__ __forceinline__ void mover_body(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks,
-                                           int32_t task_off, void* const* __restrict__ bufs,
-                                           const ItemParam* __restrict__ items, int32_t allow_wide,
-                                           int32_t ranges) {
+                                           const int32_t* __restrict__ offs, int32_t task_off,
+                                           void* const* __restrict__ bufs, const ItemParam* __restrict__ items,
+                                           int32_t allow_wide, int32_t ranges) {
   using TT = TypeTraits<S, CPLX>;
   using E = Vec<S, TT::NS>;
   __shared__ E lds[HAS_T ? TT::LDS_ELEMS : 1];
   const int32_t b = task_off + xcd_order((int32_t)blockIdx.x, (int32_t)gridDim.x, ranges);
   const int32_t pi = tasks[b];
-  const int32_t c = b - (UL == 1 ? pieces[pi].task0 : pieces[pi].aux);
+  const int32_t c = offs[b];  // the tile of a transposed rectangle, or the first unit of a row walk
   if constexpr (KIND == KIND_PACK) {
     move_walk<S, CPLX, MODE_COPY, false, UL>(pieces, pi, c, bufs, allow_wide, S(0), S(0), S(0), S(0));
   } else {
@@ -418,19 +441,19 @@ constexpr int units_per_lane() {
 
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
-costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
-            void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
-            int32_t ranges) {
-  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, units_per_lane<KIND, MODE, HAS_T>()>(pieces, tasks, task_off, bufs,
-                                                                                   items, allow_wide, ranges);
+costa_mover(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, const int32_t* __restrict__ offs,
+            int32_t task_off, void* const* __restrict__ bufs, const ItemParam* __restrict__ items,
+            int32_t allow_wide, int32_t ranges) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, units_per_lane<KIND, MODE, HAS_T>()>(pieces, tasks, offs, task_off,
+                                                                                   bufs, items, allow_wide, ranges);
 }
 
 template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
-costa_mover_lds(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks, int32_t task_off,
-                void* const* __restrict__ bufs, const ItemParam* __restrict__ items, int32_t allow_wide,
-                int32_t ranges) {
-  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, 1>(pieces, tasks, task_off, bufs, items, allow_wide, ranges);
+costa_mover_lds(const Piece* __restrict__ pieces, const int32_t* __restrict__ tasks,
+                const int32_t* __restrict__ offs, int32_t task_off, void* const* __restrict__ bufs,
+                const ItemParam* __restrict__ items, int32_t allow_wide, int32_t ranges) {
+  mover_body<S, CPLX, KIND, MODE, CONJ, HAS_T, 1>(pieces, tasks, offs, task_off, bufs, items, allow_wide, ranges);
 }
 
 // Volume of the grid overlay: every overlay block (k, l) adds its element
@@ -466,8 +489,10 @@ struct Launch {
   hipStream_t stream;
   const Piece* pieces;
   const int32_t* tasks;  // the launch's task table
+  const int32_t* offs;
   int64_t ntasks;
   const int32_t* wide;   // its wide task table (launches of row walks)
+  const int32_t* wide_offs;
   int64_t nwide;
   void* const* bufs;
   const ItemParam* items;
@@ -510,6 +535,7 @@ template <typename S, bool CPLX, int KIND, int MODE, bool CONJ, bool HAS_T>
 hipError_t go(const Launch& l) {
   constexpr bool WIDE = units_per_lane<KIND, MODE, HAS_T>() > 1;
   const int32_t* tasks = WIDE ? l.wide : l.tasks;
+  const int32_t* offs = WIDE ? l.wide_offs : l.offs;
   const int64_t ntasks = WIDE ? l.nwide : l.ntasks;
   if (ntasks > INT32_MAX) return hipErrorInvalidValue;
   constexpr int64_t kSlice = (int64_t)1 << 23;
@@ -517,10 +543,10 @@ hipError_t go(const Launch& l) {
     const unsigned n = (unsigned)(ntasks - off < kSlice ? ntasks - off : kSlice);
     if constexpr (big_lds<S, CPLX, HAS_T>())
       hipLaunchKernelGGL((costa_mover_lds<S, CPLX, KIND, MODE, CONJ, HAS_T>), dim3(n), dim3(kThreads), 0, l.stream,
-                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.ranges);
+                         l.pieces, tasks, offs, (int32_t)off, l.bufs, l.items, l.allow_wide, l.ranges);
     else
       hipLaunchKernelGGL((costa_mover<S, CPLX, KIND, MODE, CONJ, HAS_T>), dim3(n), dim3(kThreads), 0, l.stream,
-                         l.pieces, tasks, (int32_t)off, l.bufs, l.items, l.allow_wide, l.ranges);
+                         l.pieces, tasks, offs, (int32_t)off, l.bufs, l.items, l.allow_wide, l.ranges);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -557,11 +583,12 @@ hipError_t launch_typed(MoverKind kind, const LaunchSpec& spec, const Launch& l)
 }  // namespace
 
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
-                        const int32_t* tasks, int64_t ntasks, const int32_t* wide, int64_t nwide, void* const* bufs,
-                        const ItemParam* items, int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream) {
+                        const int32_t* tasks, const int32_t* offs, int64_t ntasks, const int32_t* wide,
+                        const int32_t* wide_offs, int64_t nwide, void* const* bufs, const ItemParam* items,
+                        int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream) {
   if (ntasks <= 0) return hipSuccess;
   if (!spec.has_transpose && nwide <= 0) return hipErrorInvalidValue;  // a launch of row walks has both tables
-  Launch l{stream, pieces, tasks, ntasks, wide, nwide, bufs, items, allow_wide, xcd_ranges};
+  Launch l{stream, pieces, tasks, offs, ntasks, wide, wide_offs, nwide, bufs, items, allow_wide, xcd_ranges};
   switch (dtype) {
     case COSTA_R64: return launch_typed<double, false>(kind, spec, l);
     case COSTA_C128: return launch_typed<double, true>(kind, spec, l);

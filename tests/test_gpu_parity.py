@@ -277,7 +277,7 @@ def test_transposed_rectangles_around_the_tile_limits(dtype):
     tiles): W x H rectangles on the direct path (one rank) and through
     messages (two ranks that swap their blocks), with and without beta."""
     widths = [1, 2, 15, 16, 17, 63, 64, 65, 127, 128, 129, 200, 255, 256, 257, 300, 513]
-    heights = [1, 3, 16, 17, 33, 129]
+    heights = [1, 3, 12, 13, 14, 16, 17, 18, 26, 27, 33, 34, 129]
     sc = CSCALARS if dtype in ("c128", "c64") else SCALARS
     k = 0
     for W in widths:
