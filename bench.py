@@ -533,15 +533,21 @@ def summarize_profiles(src: str, out_dir: str = None) -> None:
         with open(path, "w") as fh:
             fh.write("\n".join(lines))
         wrote.append(path)
-    # LDS bank conflicts and occupancy
+    # LDS bank conflicts and occupancy (also of the odd-height tile variant)
     sections = []
-    for name in LDS_WORKLOADS:
-        pl = os.path.join(src, f"lds_{name}")
+    for prefix, name in [("lds", n) for n in LDS_WORKLOADS] + [("ldsodd", n) for n in LDS_WORKLOADS]:
+        pl = os.path.join(src, f"{prefix}_{name}")
         if not os.path.isdir(pl):
             continue
         V = _pmc_values(pl)
         M = {c: _per_kernel_mean(V[c]) for c in PMC_LDS.split()}
-        sec = [f"## {_title(name)}", "", "```", *profile_commands(name, "lds"), "```", "",
+        cmds = profile_commands(name, "lds")
+        head = f"## {_title(name)}"
+        if prefix == "ldsodd":
+            head = f"## Variant with odd tile heights (COSTA_ODD_TILES=1): {_title(name)}"
+            cmds = ["python3 <repo>/paper_2106_06601_amd/build.py --define COSTA_ODD_TILES=1 --out <lib>"] + \
+                   [f"COSTA_LIB=<lib> {c.replace(f'lds_{name}', f'ldsodd_{name}')}" for c in cmds]
+        sec = [head, "", "```", *cmds, "```", "",
                "| kernel | dispatches | SQ_INSTS_LDS | SQ_LDS_BANK_CONFLICT | conflicts per LDS instruction | "
                "SQ_WAVES | SQ_WAVE_CYCLES | GRBM_GUI_ACTIVE | resident waves per CU |",
                "|---|---|---|---|---|---|---|---|---|"]

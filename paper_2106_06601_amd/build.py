@@ -87,4 +87,15 @@ def build(verbose: bool = False, defines=(), out=None, build_dir=None, synth=Tru
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    # python paper_2106_06601_amd/build.py [-v] [--define NAME=VALUE ...] [--out LIB]
+    # (tuning switches of the kernels and planner; a library built with
+    # --out elsewhere is loaded by setting COSTA_LIB to its path)
+    import argparse
+    ap = argparse.ArgumentParser()
+    ap.add_argument("-v", action="store_true")
+    ap.add_argument("--define", action="append", default=[])
+    ap.add_argument("--out")
+    a = ap.parse_args()
+    out = os.path.abspath(a.out) if a.out else None
+    bdir = os.path.join(BUILD_DIR, "variant_" + os.path.basename(out)) if out else None
+    print(build(verbose=a.v, defines=a.define, out=out, build_dir=bdir, synth=out is None))
