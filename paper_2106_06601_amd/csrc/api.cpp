@@ -42,8 +42,8 @@ struct DevicePlan {
   HostPlan host;
   int device = -1;
   Piece* d_pieces = nullptr;
-  int32_t* d_tasks = nullptr;  // task table, then its offsets
-  int32_t* d_wide = nullptr;   // wide task table, then its offsets
+  int32_t* d_tasks = nullptr;
+  int32_t* d_wide = nullptr;
   // per-call table: buffer pointers then pair parameters
   void* d_table = nullptr;
   void* h_staging = nullptr;  // pinned
@@ -230,14 +230,11 @@ costa_status collect_timing(State& S) {
   return COSTA_SUCCESS;
 }
 
-// Device copies of a plan's tables (rectangles, task tables and their
-// offsets, wide task tables and their offsets).
+// Device copies of a plan's tables (rectangles, task tables, wide task tables).
 struct DeviceTables {
   const Piece* pieces;
   const int32_t* tasks;
-  const int32_t* offs;
   const int32_t* wide;
-  const int32_t* wide_offs;
 };
 
 // Launches one mover range, bracketed by timing events when enabled (and
@@ -262,10 +259,9 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DeviceTab
     HIP_OR_FAIL(hipEventRecord(e0, stream));
   }
   LaunchSpec spec{mode, conj, lr.has_transpose};
-  HIP_OR_FAIL(launch_mover(kind, dt, spec, dt_.pieces, dt_.tasks + lr.task_begin, dt_.offs + lr.task_begin,
-                           lr.ntasks, lr.nwide ? dt_.wide + lr.wide_begin : nullptr,
-                           lr.nwide ? dt_.wide_offs + lr.wide_begin : nullptr, lr.nwide, d_bufs, d_items,
-                           allow_wide, lr.xcd_ranges, stream));
+  HIP_OR_FAIL(launch_mover(kind, dt, spec, dt_.pieces, dt_.tasks + lr.task_begin, lr.ntasks,
+                           lr.nwide ? dt_.wide + lr.wide_begin : nullptr, lr.nwide, d_bufs, d_items, allow_wide,
+                           lr.xcd_ranges, stream));
   if (e1) {
     HIP_OR_FAIL(hipEventRecord(e1, stream));
     costa_kernel_kind kk = kind == KIND_PACK ? COSTA_KERNEL_PACK
@@ -346,14 +342,12 @@ costa_status get_plan(State& S, costa_dtype dt, const std::vector<ItemDesc>& ite
   if (!hp.pieces.empty()) {
     HIP_OR_FAIL(hipMalloc(&dp->d_pieces, hp.pieces.size() * sizeof(Piece)));
     HIP_OR_FAIL(hipMemcpy(dp->d_pieces, hp.pieces.data(), hp.pieces.size() * sizeof(Piece), hipMemcpyHostToDevice));
-    const size_t nt = hp.tasks.size(), nw = hp.wide_tasks.size();
-    HIP_OR_FAIL(hipMalloc(&dp->d_tasks, 2 * nt * sizeof(int32_t)));
-    HIP_OR_FAIL(hipMemcpy(dp->d_tasks, hp.tasks.data(), nt * sizeof(int32_t), hipMemcpyHostToDevice));
-    HIP_OR_FAIL(hipMemcpy(dp->d_tasks + nt, hp.task_offs.data(), nt * sizeof(int32_t), hipMemcpyHostToDevice));
-    if (nw) {
-      HIP_OR_FAIL(hipMalloc(&dp->d_wide, 2 * nw * sizeof(int32_t)));
-      HIP_OR_FAIL(hipMemcpy(dp->d_wide, hp.wide_tasks.data(), nw * sizeof(int32_t), hipMemcpyHostToDevice));
-      HIP_OR_FAIL(hipMemcpy(dp->d_wide + nw, hp.wide_offs.data(), nw * sizeof(int32_t), hipMemcpyHostToDevice));
+    HIP_OR_FAIL(hipMalloc(&dp->d_tasks, hp.tasks.size() * sizeof(int32_t)));
+    HIP_OR_FAIL(hipMemcpy(dp->d_tasks, hp.tasks.data(), hp.tasks.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    if (!hp.wide_tasks.empty()) {
+      HIP_OR_FAIL(hipMalloc(&dp->d_wide, hp.wide_tasks.size() * sizeof(int32_t)));
+      HIP_OR_FAIL(hipMemcpy(dp->d_wide, hp.wide_tasks.data(), hp.wide_tasks.size() * sizeof(int32_t),
+                            hipMemcpyHostToDevice));
     }
   }
   const int32_t P = items.empty() ? 0 : items[0].A->nranks;
@@ -477,10 +471,8 @@ costa_status transform_impl(costa_dtype dt, int32_t n, const costa_transform_des
   void* const* d_bufs = reinterpret_cast<void* const*>(dp->d_table);
   const ItemParam* d_items = reinterpret_cast<const ItemParam*>((unsigned char*)dp->d_table + ptr_bytes);
   const ItemParam* ipar = reinterpret_cast<const ItemParam*>(dp->last_table.data() + ptr_bytes);
-  const size_t nt = hp.tasks.size(), nw = hp.wide_tasks.size();
-  const DeviceTables tabs{dp->d_pieces, dp->d_tasks, dp->d_tasks ? dp->d_tasks + nt : nullptr, dp->d_wide,
-                          dp->d_wide ? dp->d_wide + nw : nullptr};
-  st = launch_plan(S, dt, hp, tabs, ipar, n, reads_a, aligned, d_bufs, d_items, stream, true);
+  st = launch_plan(S, dt, hp, DeviceTables{dp->d_pieces, dp->d_tasks, dp->d_wide}, ipar, n, reads_a, aligned,
+                   d_bufs, d_items, stream, true);
   if (st != COSTA_SUCCESS) return st;
   if (ws->last_use) {
     HIP_OR_FAIL(hipEventRecord(ws->last_use, stream));
@@ -568,6 +560,14 @@ extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const co
       for (int64_t i = 0; i < lr.npieces; ++i, ++k) {
         if (k >= capacity) continue;
         const Piece& q = hp->pieces[lr.piece_begin + i];
+        // workgroups that move it: from task0 up to the next rectangle's first
+        // one (or the launch's end); 1 for a rectangle that shares a workgroup
+        int64_t end = lr.ntasks;
+        for (int64_t j = i + 1; j < lr.npieces; ++j)
+          if (hp->pieces[lr.piece_begin + j].task0 != q.task0) {
+            end = hp->pieces[lr.piece_begin + j].task0;
+            break;
+          }
         costa_piece_info& o = out[k];
         o.kind = kind;
         o.wave = wave;
@@ -582,13 +582,19 @@ extern "C" costa_status costa_plan_export(costa_dtype dtype, int32_t n, const co
         o.ny = q.ny;
         o.item = q.item;
         o.flags = q.flags;
-        o.ntasks = hp->piece_ntasks[lr.piece_begin + i];
+        o.ntasks = end - q.task0;
         const bool T = q.flags & PIECE_TRANSPOSE;
         o.tile_x = T ? tile_x_of(q.aux) : 0;
         o.tile_y = T ? tile_y_of(q.aux) : 0;
         // its first task and task count in the wide table (launches without tiles)
         o.wide_group = lr.nwide ? q.aux : -1;
-        o.wide_ntasks = lr.nwide ? hp->piece_wide_ntasks[lr.piece_begin + i] : 0;
+        int64_t wend = lr.nwide;
+        for (int64_t j = i + 1; lr.nwide && j < lr.npieces; ++j)
+          if (hp->pieces[lr.piece_begin + j].aux != q.aux) {
+            wend = hp->pieces[lr.piece_begin + j].aux;
+            break;
+          }
+        o.wide_ntasks = lr.nwide ? wend - q.aux : 0;
         o.launch = launch;
         o.reserved = 0;
 
@@ -808,7 +814,7 @@ static __device__ __align__(256) unsigned char scratch[kNoallocBytes];
 struct NoallocPlan {
   HostPlan host;
   uint64_t serial = 0;  // tells plans apart when one is rebuilt at a freed address
-  size_t off_tasks = 0, off_wide = 0, off_table = 0, end = 0;  // task and wide tables with their offsets
+  size_t off_tasks = 0, off_wide = 0, off_table = 0, end = 0;
 };
 
 // What one device's scratch array holds.
@@ -847,8 +853,8 @@ costa_status noalloc_plan(costa_dtype dt, const std::vector<ItemDesc>& items, co
     const int32_t P = items.empty() ? 0 : items[0].A->nranks;
     const size_t nbufs = (size_t)2 * items.size() * P + 1;
     np->off_tasks = align256(hp.pieces.size() * sizeof(Piece));
-    np->off_wide = np->off_tasks + align256(2 * hp.tasks.size() * sizeof(int32_t));
-    np->off_table = np->off_wide + align256(2 * hp.wide_tasks.size() * sizeof(int32_t));
+    np->off_wide = np->off_tasks + align256(hp.tasks.size() * sizeof(int32_t));
+    np->off_table = np->off_wide + align256(hp.wide_tasks.size() * sizeof(int32_t));
     np->end = np->off_table + (nbufs * sizeof(void*) + 63) / 64 * 64 + items.size() * sizeof(ItemParam);
     np->serial = N.next_serial++;
     it = N.plans.emplace(key, std::move(np)).first;
@@ -914,17 +920,12 @@ extern "C" costa_status costa_transform_batched_noalloc(costa_dtype dtype, int32
       if (!hp.pieces.empty())
         HIP_OR_FAIL(hipMemcpyAsync(base, hp.pieces.data(), hp.pieces.size() * sizeof(Piece), hipMemcpyHostToDevice,
                                    stream));
-      const size_t nt = hp.tasks.size() * sizeof(int32_t), nw = hp.wide_tasks.size() * sizeof(int32_t);
-      if (nt) {
-        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_tasks, hp.tasks.data(), nt, hipMemcpyHostToDevice, stream));
-        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_tasks + nt, hp.task_offs.data(), nt, hipMemcpyHostToDevice,
-                                   stream));
-      }
-      if (nw) {
-        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_wide, hp.wide_tasks.data(), nw, hipMemcpyHostToDevice, stream));
-        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_wide + nw, hp.wide_offs.data(), nw, hipMemcpyHostToDevice,
-                                   stream));
-      }
+      if (!hp.tasks.empty())
+        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_tasks, hp.tasks.data(), hp.tasks.size() * sizeof(int32_t),
+                                   hipMemcpyHostToDevice, stream));
+      if (!hp.wide_tasks.empty())
+        HIP_OR_FAIL(hipMemcpyAsync(base + np->off_wide, hp.wide_tasks.data(), hp.wide_tasks.size() * sizeof(int32_t),
+                                   hipMemcpyHostToDevice, stream));
       dev->resident = np->serial;
     }
     const int32_t P = items[0].A->nranks;
@@ -939,10 +940,9 @@ extern "C" costa_status costa_transform_batched_noalloc(costa_dtype dtype, int32
     const ItemParam* ipar = reinterpret_cast<const ItemParam*>(dev->table.data() + ptr_bytes);
     void* const* d_bufs = reinterpret_cast<void* const*>(base + np->off_table);
     const ItemParam* d_items = reinterpret_cast<const ItemParam*>(base + np->off_table + ptr_bytes);
-    const int32_t* d_tasks = reinterpret_cast<const int32_t*>(base + np->off_tasks);
-    const int32_t* d_wide = reinterpret_cast<const int32_t*>(base + np->off_wide);
-    const DeviceTables tabs{reinterpret_cast<const Piece*>(base), d_tasks, d_tasks + hp.tasks.size(), d_wide,
-                            d_wide + hp.wide_tasks.size()};
+    const DeviceTables tabs{reinterpret_cast<const Piece*>(base),
+                            reinterpret_cast<const int32_t*>(base + np->off_tasks),
+                            reinterpret_cast<const int32_t*>(base + np->off_wide)};
     // no timing events on this path (creating one may allocate)
     return launch_plan(S, dtype, hp, tabs, ipar, n, reads_a, aligned, d_bufs, d_items, stream, false);
   });

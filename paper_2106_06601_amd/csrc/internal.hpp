@@ -124,14 +124,12 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 //   src_off + x*src_ld + y   (flag TRANSPOSE set: contiguous along y).
 // PIECE_WIDE: a non-transposed rectangle whose offsets, strides and width
 //   allow 16-byte vectors.
-// PIECE_GROUP_NEXT: the next rectangle of the launch continues this one's
-//   segment (its units follow this one's in the tasks that cover them).
+// PIECE_GROUP_NEXT: the next rectangle of the launch is moved by the same
+//   workgroup (a run of small rectangles shares one workgroup).
 // A transposed rectangle is moved in LDS tiles of tile_x x tile_y elements
 // (tile_x along the destination's contiguous direction; choose_tile below),
 // packed into `aux` with tile_pack.
-// PIECE_TILE_COLS: the tiles of a transposed rectangle are numbered down its
-//   tile columns (y first) instead of along its tile rows (x first).
-enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_TILE_COLS = 4, PIECE_GROUP_NEXT = 16 };
+enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_GROUP_NEXT = 16 };
 
 struct alignas(16) Piece {
   int64_t src_off;
@@ -147,24 +145,22 @@ struct alignas(16) Piece {
   int32_t task0;    // first workgroup of its launch that moves it
   int32_t aux;      // transposed rectangles: tile_pack(tile_x, tile_y); row walks in a
                     // launch without tiles: its first task in the launch's wide task table
-                    // (task0 and the wide task are for inspection; the kernels read the
-                    // task tables)
 };
 static_assert(sizeof(Piece) == 64, "Piece must be 64 bytes");
 
 // Work of one workgroup (kThreadsPerTask lanes): one LDS tile of a
-// transposed rectangle, or kThreadsPerTask units (16-byte vectors, or single
-// elements when the rectangle is not PIECE_WIDE) of a segment of row walks
-// (rectangles whose units are numbered one after another, see plan.cpp).  A
-// launch of row walks also has a wide task table whose tasks are
-// kWideTaskUnits units; launches that copy use it, two units per lane.
+// transposed rectangle, kThreadsPerTask units (16-byte vectors, or single
+// elements when the rectangle is not PIECE_WIDE) of a rectangle walked along
+// its rows, or a run of small rectangles moved at once.  A launch of row
+// walks also has a wide task table whose tasks are kWideTaskUnits units (a
+// run still one task); launches that copy use it, two units per lane.
 constexpr int32_t kThreadsPerTask = 256;
 #ifndef COSTA_COPY_UNITS
 #define COSTA_COPY_UNITS 2  // units per lane in launches of row walks that copy
 #endif
 constexpr int32_t kWideTaskUnits = (COSTA_COPY_UNITS > 1 ? COSTA_COPY_UNITS : 2) * kThreadsPerTask;
-constexpr int32_t kGroupUnitsMax = 128;  // without flat tasks: rectangles of at most this many units
-constexpr int32_t kGroupPiecesMax = 8;   // (at most this many) may share a workgroup
+constexpr int32_t kGroupUnitsMax = 128;  // rectangles of at most this many units may share a workgroup
+constexpr int32_t kGroupPiecesMax = 8;
 
 // Elements per 16-byte unit of a PIECE_WIDE rectangle.
 constexpr int32_t wide_elems(int32_t es) { return es >= 16 ? 1 : 16 / es; }
@@ -252,7 +248,7 @@ struct LaunchRange {
   int64_t wide_begin = 0, nwide = 0;  // wide task table (launches without tiles; 0 tasks otherwise)
   int64_t elems = 0;
   bool has_transpose = false;
-  int32_t xcd_ranges = 0;  // 1: each XCD takes one contiguous range of the launch's tasks; K >= 2: runs of K
+  int32_t xcd_ranges = 0;  // 1: each XCD takes one contiguous range of the launch's tasks
   std::vector<int64_t> item_elems;  // elements of each pair in this launch
 };
 
@@ -274,18 +270,15 @@ struct LaunchSpec {
   int32_t conj;
   bool has_transpose;
 };
-// pieces: the plan's rectangles (global indices); tasks / offs: the launch's
-// ntasks entries (the rectangle a task starts in, and its tile or first unit
-// there), wide / wide_offs: its wide task table (nwide entries, 0 in
-// launches with tiles).
+// pieces: the plan's rectangles (global indices); tasks: the launch's
+// ntasks entries, wide: its wide task table (nwide entries, 0 in launches
+// with tiles).
 // xcd_ranges: 0 runs task b in workgroup b (workgroups are dispatched
 // round-robin over the 8 XCDs); 1 hands each XCD one contiguous range of the
-// tasks of each launch slice; K >= 2 hands each XCD runs of K consecutive
-// tasks.
+// tasks of each launch slice.
 hipError_t launch_mover(MoverKind kind, costa_dtype dtype, const LaunchSpec& spec, const Piece* pieces,
-                        const int32_t* tasks, const int32_t* offs, int64_t ntasks, const int32_t* wide,
-                        const int32_t* wide_offs, int64_t nwide, void* const* bufs, const ItemParam* items,
-                        int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream);
+                        const int32_t* tasks, int64_t ntasks, const int32_t* wide, int64_t nwide, void* const* bufs,
+                        const ItemParam* items, int32_t allow_wide, int32_t xcd_ranges, hipStream_t stream);
 
 struct VolumeArgs {
   const Interval* rows;

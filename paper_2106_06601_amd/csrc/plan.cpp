@@ -302,14 +302,6 @@ void finish_piece(Piece& p, int elem_size) {
 #ifndef COSTA_XCD_RANGES
 #define COSTA_XCD_RANGES 1
 #endif
-// Runs of K consecutive tasks per XCD (0: off) for launches of tiles and for
-// launches of row walks that the per-XCD ranges do not take.
-#ifndef COSTA_TILE_KRUN
-#define COSTA_TILE_KRUN 0
-#endif
-#ifndef COSTA_WALK_KRUN
-#define COSTA_WALK_KRUN 0
-#endif
 
 // Whether every run of the rectangle (its rows in the source and in the
 // destination) starts and ends on a 128-byte line.
@@ -322,130 +314,10 @@ bool line_aligned(const Piece& p, int es) {
          (sstep == 1 || al(p.src_ld));
 }
 
-// Row walks of a launch are cut into segments: runs of consecutive
-// rectangles of one pair and one unit size whose units are numbered one after
-// another (PIECE_GROUP_NEXT on every rectangle but a segment's last); a task
-// takes the next T units of its segment, across rectangle ends, so that no
-// lane of a workgroup sits idle but at a segment's end.  A segment ends where
-// the pair or the unit size changes, before a rectangle that would make one
-// wide task (kWideTaskUnits units) span more than kFlatPiecesMax rectangles
-// (each lane walks the rectangles of its task one by one), and before its
-// units would pass 2^30.  With COSTA_FLAT_BIG_UNITS > 0, a rectangle of more
-// units than that is a segment of its own.  COSTA_FLAT_TASKS=0 keeps one
-// rectangle per segment
-// but for runs of small rectangles (at most kGroupUnitsMax units each and
-// kThreadsPerTask together, at most kGroupPiecesMax of them).
-#ifndef COSTA_FLAT_TASKS
-#define COSTA_FLAT_TASKS 1
-#endif
-#ifndef COSTA_FLAT_BIG_UNITS
-#define COSTA_FLAT_BIG_UNITS 2048  // 0: no limit
-#endif
-constexpr int32_t kFlatPiecesMax = 16;
-
-int64_t units_of(const Piece& p, int es) {
-  const int64_t ne = (int64_t)p.nx * p.ny;
-  return (p.flags & PIECE_WIDE) ? ne / wide_elems(es) : ne;
-}
-
-// starts[k] = 1 where row walk k begins a segment (tiles: always 1).
-std::vector<char> segment_starts(const std::vector<Piece>& ps, int es) {
-  std::vector<char> starts(ps.size(), 1);
-  int64_t seg = 0;          // units of the open segment
-  int64_t window = -1;      // last wide task of the open segment
-  int32_t in_window = 0;    // rectangles that task touches so far
-  int32_t small = 0;        // rectangles of an open run of small ones (COSTA_FLAT_TASKS=0)
-  for (size_t k = 0; k < ps.size(); ++k) {
-    const Piece& p = ps[k];
-    if (p.flags & PIECE_TRANSPOSE) {
-      seg = 0;
-      window = -1;
-      small = 0;
-      continue;
-    }
-    const int64_t u = units_of(p, es);
-    const Piece* q = k > 0 ? &ps[k - 1] : nullptr;
-    bool cont = q && !(q->flags & PIECE_TRANSPOSE) && q->item == p.item &&
-                (q->flags & PIECE_WIDE) == (p.flags & PIECE_WIDE);
-    if (COSTA_FLAT_TASKS) {
-      if (cont && seg / kWideTaskUnits == window && in_window + 1 > kFlatPiecesMax) cont = false;
-      if (cont && seg + u > ((int64_t)1 << 30)) cont = false;
-      if (COSTA_FLAT_BIG_UNITS > 0 && (u > COSTA_FLAT_BIG_UNITS || units_of(*q, es) > COSTA_FLAT_BIG_UNITS))
-        cont = false;
-    } else {
-      cont = cont && small > 0 && u <= kGroupUnitsMax && seg + u <= kThreadsPerTask && small < kGroupPiecesMax;
-    }
-    if (!cont) {
-      seg = 0;
-      window = -1;
-      small = 0;
-    }
-    starts[k] = cont ? 0 : 1;
-    const int64_t w0 = seg / kWideTaskUnits, w1 = (seg + u - 1) / kWideTaskUnits;
-    in_window = w0 == window ? in_window + 1 : 1;
-    if (w1 != w0) in_window = 1;
-    window = w1;
-    seg += u;
-    small = u <= kGroupUnitsMax ? small + 1 : 0;
-    if (!COSTA_FLAT_TASKS && small == 0) seg = kThreadsPerTask + 1;  // a large rectangle starts no run
-  }
-  return starts;
-}
-
-// The task table of a launch for tasks of T units (row walks): for each task
-// the rectangle it starts in and the unit of that rectangle it starts at;
-// tiles: one task per tile, with the tile's index.  first[k] / count[k]: the
-// first task that moves rectangle k and how many do.
-void task_table(const std::vector<Piece>& ps, const std::vector<char>& starts, int es, int64_t T, int32_t base,
-                std::vector<int32_t>& tasks, std::vector<int32_t>& offs, std::vector<int64_t>& first,
-                std::vector<int64_t>& count) {
-  const size_t t0 = tasks.size();
-  first.assign(ps.size(), 0);
-  count.assign(ps.size(), 0);
-  size_t k = 0;
-  while (k < ps.size()) {
-    const Piece& p = ps[k];
-    const int64_t tb = (int64_t)(tasks.size() - t0);
-    if (p.flags & PIECE_TRANSPOSE) {
-      const int32_t tx = tile_x_of(p.aux), ty = tile_y_of(p.aux);
-      const int64_t n = (int64_t)((p.nx + tx - 1) / tx) * ((p.ny + ty - 1) / ty);
-      for (int64_t c = 0; c < n; ++c) {
-        tasks.push_back(base + (int32_t)k);
-        offs.push_back((int32_t)c);
-      }
-      first[k] = tb;
-      count[k] = n;
-      ++k;
-      continue;
-    }
-    // one segment: rectangles k .. e-1, units numbered from 0
-    size_t e = k + 1;
-    while (e < ps.size() && !starts[e]) ++e;
-    int64_t cum = 0;
-    size_t r = k;          // rectangle holding unit g
-    int64_t r_start = 0;   // its first unit
-    for (size_t m = k; m < e; ++m) {
-      const int64_t u = units_of(ps[m], es);
-      first[m] = tb + cum / T;
-      count[m] = (cum + u - 1) / T - cum / T + 1;
-      cum += u;
-    }
-    for (int64_t g = 0; g < cum; g += T) {
-      while (g >= r_start + units_of(ps[r], es)) {
-        r_start += units_of(ps[r], es);
-        ++r;
-      }
-      tasks.push_back(base + (int32_t)r);
-      offs.push_back((int32_t)(g - r_start));
-    }
-    k = e;
-  }
-}
-
 // Appends one launch: its rectangles and the workgroups that move them, in
-// rectangle order.  A transposed rectangle gets one workgroup per LDS tile;
-// row walks get tasks of kThreadsPerTask units over their segments, and a
-// launch of row walks also a wide task table of kWideTaskUnits units.
+// rectangle order.  A transposed rectangle gets one workgroup per LDS tile
+// (tiles along x first); a row walk one per kThreadsPerTask units; runs of
+// small row walks of the same pair and vector width share one workgroup.
 LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nitems) {
   LaunchRange lr;
   lr.item_elems.assign(nitems, 0);
@@ -455,34 +327,77 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   if (hp.pieces.size() + ps.size() > (size_t)INT32_MAX)
     throw LimitExceeded("more than 2^31-1 rectangles in one plan");
   const int32_t base = (int32_t)hp.pieces.size();
-  for (Piece& p : ps) {
+  int64_t b = 0;
+  // the open run of small row walks
+  int64_t g_task = -1;
+  int64_t g_units = 0;
+  int32_t g_count = 0;
+  size_t g_last = 0;
+  bool g_wide = false;
+  int32_t g_item = 0;
+  for (size_t k = 0; k < ps.size(); ++k) {
+    Piece& p = ps[k];
     const int64_t ne = (int64_t)p.nx * p.ny;
     lr.elems += ne;
     lr.item_elems[p.item] += ne;
-    if (p.flags & PIECE_TRANSPOSE) lr.has_transpose = true;
+    const int32_t pi = base + (int32_t)k;
+    if (p.flags & PIECE_TRANSPOSE) {
+      lr.has_transpose = true;
+      g_task = -1;
+      const int32_t tx = tile_x_of(p.aux), ty = tile_y_of(p.aux);
+      const int64_t n = (int64_t)((p.nx + tx - 1) / tx) * ((p.ny + ty - 1) / ty);
+      p.task0 = (int32_t)b;
+      hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+      b += n;
+      continue;
+    }
+    const bool wide = p.flags & PIECE_WIDE;
+    const int64_t units = wide ? ne / wide_elems(es) : ne;
+    if (units <= kGroupUnitsMax && g_task >= 0 && wide == g_wide && p.item == g_item &&
+        g_units + units <= kThreadsPerTask && g_count < kGroupPiecesMax) {
+      ps[g_last].flags |= PIECE_GROUP_NEXT;
+      p.task0 = (int32_t)g_task;
+      g_units += units;
+      ++g_count;
+      g_last = k;
+      continue;
+    }
+    const int64_t n = (units + kThreadsPerTask - 1) / kThreadsPerTask;
+    p.task0 = (int32_t)b;
+    hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+    b += n;
+    if (units <= kGroupUnitsMax) {
+      g_task = b - 1;
+      g_units = units;
+      g_count = 1;
+      g_last = k;
+      g_wide = wide;
+      g_item = p.item;
+    } else {
+      g_task = -1;
+    }
   }
-  const std::vector<char> starts = segment_starts(ps, es);
-  for (size_t k = 0; k + 1 < ps.size(); ++k)
-    if (!starts[k + 1]) ps[k].flags |= PIECE_GROUP_NEXT;
-  std::vector<int64_t> first, count;
-  task_table(ps, starts, es, kThreadsPerTask, base, hp.tasks, hp.task_offs, first, count);
-  lr.ntasks = (int64_t)hp.tasks.size() - lr.task_begin;
-  if (lr.ntasks > INT32_MAX) throw LimitExceeded("more than 2^31-1 workgroups in one launch");
-  for (size_t k = 0; k < ps.size(); ++k) {
-    ps[k].task0 = (int32_t)first[k];
-    hp.piece_ntasks.push_back(count[k]);
-  }
-  // the wide task table of a launch of row walks (the launches that copy run on it)
+  if (b > INT32_MAX) throw LimitExceeded("more than 2^31-1 workgroups in one launch");
+  lr.ntasks = b;
+  // the wide task table of a launch of row walks: kWideTaskUnits units per
+  // task, a run of small rectangles still one task
   lr.wide_begin = (int64_t)hp.wide_tasks.size();
   if (!lr.has_transpose) {
-    task_table(ps, starts, es, kWideTaskUnits, base, hp.wide_tasks, hp.wide_offs, first, count);
-    lr.nwide = (int64_t)hp.wide_tasks.size() - lr.wide_begin;
+    int64_t b2 = 0;
     for (size_t k = 0; k < ps.size(); ++k) {
-      ps[k].aux = (int32_t)first[k];
-      hp.piece_wide_ntasks.push_back(count[k]);
+      Piece& p = ps[k];
+      if (k > 0 && (ps[k - 1].flags & PIECE_GROUP_NEXT)) {
+        p.aux = ps[k - 1].aux;
+        continue;
+      }
+      const int64_t ne = (int64_t)p.nx * p.ny;
+      const int64_t units = (p.flags & PIECE_WIDE) ? ne / wide_elems(es) : ne;
+      const int64_t n = (p.flags & PIECE_GROUP_NEXT) ? 1 : (units + kWideTaskUnits - 1) / kWideTaskUnits;
+      p.aux = (int32_t)b2;
+      hp.wide_tasks.insert(hp.wide_tasks.end(), (size_t)n, base + (int32_t)k);
+      b2 += n;
     }
-  } else {
-    hp.piece_wide_ntasks.insert(hp.piece_wide_ntasks.end(), ps.size(), 0);
+    lr.nwide = b2;
   }
   int64_t aligned = 0, transposed = 0;
   for (const Piece& p : ps) {
@@ -491,20 +406,6 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   }
   const bool one_kind = transposed == 0 || transposed == lr.elems;
   lr.xcd_ranges = COSTA_XCD_RANGES && one_kind && lr.elems > 0 && 10 * aligned >= 9 * lr.elems ? 1 : 0;
-  if (lr.xcd_ranges == 0 && lr.elems > 0) {
-    if (transposed == lr.elems && COSTA_TILE_KRUN >= 2) {
-      // tiles whose source runs start and end inside lines: runs of tiles
-      // down the tile columns on one XCD, so that the lines two tiles of a
-      // column share are fetched once into that XCD's L2
-      lr.xcd_ranges = COSTA_TILE_KRUN;
-      for (Piece& p : ps) p.flags |= PIECE_TILE_COLS;
-    } else if (transposed == 0 && COSTA_WALK_KRUN >= 2) {
-      // row walks whose rows start and end inside lines: runs of
-      // neighbouring tasks (rectangles side by side in the destination) on
-      // one XCD
-      lr.xcd_ranges = COSTA_WALK_KRUN;
-    }
-  }
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
 }

@@ -23,11 +23,8 @@ struct PlanConfig {
 
 struct HostPlan {
   std::vector<Piece> pieces;    // every launch's rectangles, concatenated
-  std::vector<int32_t> tasks;   // every launch's workgroups: index of the rectangle each starts in
-  std::vector<int32_t> task_offs;   // ... and where in it: its tile (tiles) or unit (row walks)
+  std::vector<int32_t> tasks;   // every launch's workgroups: index of the rectangle each starts with
   std::vector<int32_t> wide_tasks;  // the wide task tables of the launches without tiles
-  std::vector<int32_t> wide_offs;
-  std::vector<int64_t> piece_ntasks, piece_wide_ntasks;  // workgroups of each table that move each rectangle
   std::vector<LaunchRange> direct;  // empty when the direct rectangles join the last unpack
   std::vector<Wave> waves;
   int64_t workspace_bytes = 0;  // max message bytes of a wave

@@ -23,25 +23,19 @@ PACK, UNPACK, DIRECT = 0, 1, 2
 # MAXX[es] wide and its tile_x rows of tile_y | 1 elements fit the LDS array
 # of CAP[es] elements; a rectangle that fits is one tile, wider ones use as
 # few tile columns as MAXX allows, and cut tiles are not far below the LDS
-# array).  Row walks form segments -- runs of rectangles chained by flag 16,
-# each of one pair and one unit size (16-byte vectors when flag 2 is set,
-# else elements) -- whose units are numbered one after another; a workgroup
-# takes the next LANES units of a segment (WIDE_UNITS in the wide table),
-# and no wide task spans more than FLAT_PIECES rectangles.
+# array); a row walk by one
+# workgroup per 256 units (16-byte vectors when flag 2 is set, else
+# elements); a run of small row walks (each but the last flagged 16) by one
+# workgroup for all of them.
 CAP = {4: 4224, 8: 2176, 16: 3328}
 MAXX = {4: 128, 8: 128, 16: 256}
-LANES, WIDE_UNITS, FLAT_PIECES = 256, 512, 16
-
-
-def _units(p, es):
-    n = int(p["nx"]) * int(p["ny"])
-    return n // (16 // es) if int(p["flags"]) & 2 and es < 16 else n
+LANES, GROUP_UNITS, GROUP_PIECES, WIDE_UNITS = 256, 128, 8, 512
 
 
 def check_tasks(pieces, es):
     """Every launch's workgroups are handed out in rectangle order without gaps
-    or overlaps: one per tile, or tasks of LANES (WIDE_UNITS) consecutive
-    units of a segment; each rectangle reports the tasks that touch it."""
+    or overlaps, each rectangle gets the number its tiles or units need, and
+    runs of small rectangles fit one workgroup."""
     launches = {}
     for i, p in enumerate(pieces):
         launches.setdefault((int(p["kind"]), int(p["launch"])), []).append(p)
@@ -52,11 +46,21 @@ def check_tasks(pieces, es):
         T = {bool(int(p["flags"]) & 1) for p in ps}
         assert kind == PACK and T == {False} or len(T) == 1, "a launch holds tiles or row walks, not both"
     for ps in launches.values():
-        if int(ps[0]["flags"]) & 1:
-            nxt = 0
-            for p in ps:
-                nx, ny, fl = int(p["nx"]), int(p["ny"]), int(p["flags"])
-                assert int(p["group"]) == nxt, "workgroups of a launch are not handed out in order"
+        nxt = 0
+        run = None  # (units so far, rectangles so far, item, vector width) of an open run
+        for p in ps:
+            nx, ny, fl = int(p["nx"]), int(p["ny"]), int(p["flags"])
+            if run is not None:  # continues the run of the previous rectangle
+                assert not fl & 1 and int(p["group"]) == nxt - 1 and int(p["ntasks"]) == 1
+                units = nx * ny // (16 // es if fl & 2 and es < 16 else 1)
+                assert units <= GROUP_UNITS and int(p["item"]) == run[2] and (fl & 2) == run[3]
+                run = (run[0] + units, run[1] + 1, run[2], run[3])
+                assert run[0] <= LANES and run[1] <= GROUP_PIECES
+                if not fl & 16:
+                    run = None
+                continue
+            assert int(p["group"]) == nxt, "workgroups of a launch are not handed out in order"
+            if fl & 1:
                 tx, ty = int(p["tile_x"]), int(p["tile_y"])
                 assert 1 <= tx <= min(nx, MAXX[es]) and 1 <= ty <= ny and tx * (ty | 1) <= CAP[es]
                 if nx <= MAXX[es] and nx * (ny | 1) <= CAP[es] - MAXX[es]:
@@ -65,37 +69,34 @@ def check_tasks(pieces, es):
                     assert -(-nx // tx) == -(-nx // MAXX[es]), "more tile columns than needed"
                     assert ty == ny or 2 * tx * (ty + 2) > CAP[es] - MAXX[es], "tiles far below the LDS array"
                 need = -(-nx // tx) * -(-ny // ty)
-                assert not fl & 16 and int(p["ntasks"]) == need, f"{p} needs {need} workgroups"
-                assert int(p["wide_group"]) == -1 and int(p["wide_ntasks"]) == 0
-                nxt += need
+                assert not fl & 16
+            else:
+                units = nx * ny // (16 // es if fl & 2 and es < 16 else 1)
+                need = -(-units // LANES)
+                if fl & 16:
+                    assert units <= GROUP_UNITS and need == 1
+                    run = (units, 1, int(p["item"]), fl & 2)
+            assert int(p["ntasks"]) == need, f"{p} needs {need} workgroups"
+            nxt += need
+        assert run is None, "a run of small rectangles ends with the launch's last rectangle flagged"
+        # the wide task table of a launch of row walks: tasks of WIDE_UNITS
+        # units, a run of small rectangles one task; none in launches with tiles
+        if any(int(p["flags"]) & 1 for p in ps):
+            assert all(int(p["wide_group"]) == -1 and int(p["wide_ntasks"]) == 0 for p in ps)
             continue
-        # segments of row walks
-        segs, cur = [], []
+        nxt, in_run = 0, False
         for p in ps:
-            cur.append(p)
-            if not int(p["flags"]) & 16:
-                segs.append(cur)
-                cur = []
-        assert not cur, "the launch's last rectangle continues a segment"
-        for seg in segs:
-            assert len({int(p["item"]) for p in seg}) == 1, "a segment mixes pairs"
-            assert len({int(p["flags"]) & 2 for p in seg}) == 1, "a segment mixes unit sizes"
-        for T, gkey, nkey in ((LANES, "group", "ntasks"), (WIDE_UNITS, "wide_group", "wide_ntasks")):
-            nxt = 0
-            for seg in segs:
-                cum = 0
-                spans = {}
-                for p in seg:
-                    u = _units(p, es)
-                    assert u >= 1
-                    assert int(p[gkey]) == nxt + cum // T, f"{gkey} of {p}"
-                    assert int(p[nkey]) == (cum + u - 1) // T - cum // T + 1, f"{nkey} of {p}"
-                    for t in range(cum // T, (cum + u - 1) // T + 1):
-                        spans[t] = spans.get(t, 0) + 1
-                    cum += u
-                if T == WIDE_UNITS:
-                    assert max(spans.values()) <= FLAT_PIECES, "a wide task spans too many rectangles"
-                nxt += -(-cum // T)
+            nx, ny, fl = int(p["nx"]), int(p["ny"]), int(p["flags"])
+            if in_run:
+                assert int(p["wide_group"]) == nxt - 1 and int(p["wide_ntasks"]) == 1
+                in_run = bool(fl & 16)
+                continue
+            assert int(p["wide_group"]) == nxt, "wide tasks of a launch are not handed out in order"
+            units = nx * ny // (16 // es if fl & 2 and es < 16 else 1)
+            need = 1 if fl & 16 else -(-units // WIDE_UNITS)
+            assert int(p["wide_ntasks"]) == need
+            in_run = bool(fl & 16)
+            nxt += need
 
 
 def _descs(w):
