@@ -284,6 +284,11 @@ LDS_WORKLOADS = ["reshuffle_transpose_1k", "cosma_complex_16k", "rpa_batched_tal
 PMC_READ = "TCC_BUBBLE_sum TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_32B_sum"
 PMC_WRITE = "WRITE_SIZE TCC_EA0_RDREQ_DRAM_32B_sum TCC_EA0_WRREQ_WRITE_DRAM_32B_sum"
 PMC_LDS = "SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS SQ_WAVES SQ_WAVE_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE"
+STALL_WORKLOADS = ["cosma_complex_16k", "blocksize_change_16k", "pztranc_8k"]
+PMC_STALLS = ["SQ_WAVES SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_LDS SQ_INST_LEVEL_VMEM SQ_INSTS_VMEM "
+              "SQ_ACTIVE_INST_VMEM",
+              "TCC_EA0_RDREQ_DRAM_CREDIT_STALL_sum TCC_EA0_WRREQ_DRAM_CREDIT_STALL_sum TCC_BUSY_sum GRBM_GUI_ACTIVE",
+              "TA_BUSY_avr TA_ADDR_STALLED_BY_TC_CYCLES_sum GRBM_GUI_ACTIVE"]
 _MODES = {0: "copy", 1: "scale", 2: "axpby", 3: "per pair"}
 _TEMPLATE_NOTE = ("Kernel template arguments: <scalar, complex, kind (0 pack, 1 unpack-transform, 2 direct), "
                   "mode (0 copy, 1 scale, 2 axpby, 3 per pair), conjugate, LDS tiles>.")
@@ -306,6 +311,9 @@ def profile_commands(name: str, what: str) -> list:
                 f"--copy-probe 1024",
                 f"rocprofv3 --pmc {PMC_WRITE} -f csv -d <out>/pmcB_{name} -o run -- {b} --steps 2 --warmup 1 "
                 f"--copy-probe 1024"]
+    if what == "stalls":
+        return [f"rocprofv3 --pmc {c} -f csv -d <out>/stall{k}_{name} -o run -- {b} --steps 2 --warmup 1"
+                for k, c in enumerate(PMC_STALLS)]
     return [f"rocprofv3 --pmc {PMC_LDS} -f csv -d <out>/lds_{name} -o run -- {b} --steps 2 --warmup 1"]
 
 
@@ -567,6 +575,43 @@ def summarize_profiles(src: str, out_dir: str = None) -> None:
                  "(about 8x the kernel's cycles); resident waves per CU = 4 x SQ_WAVE_CYCLES / (GRBM_GUI_ACTIVE / 8) "
                  "/ 256 CUs.", _TEMPLATE_NOTE, "", *sections, stamp, ""]
         path = os.path.join(out_dir, "counters_lds_occupancy.md")
+        with open(path, "w") as fh:
+            fh.write("\n".join(lines))
+        wrote.append(path)
+    # where the mover kernels wait: occupancy, time a vector memory
+    # instruction stays outstanding, the address unit's stalls on the L1,
+    # the L2's DRAM-credit stalls
+    rows = []
+    cmds = []
+    for name in STALL_WORKLOADS:
+        dirs = [os.path.join(src, f"stall{k}_{name}") for k in range(len(PMC_STALLS))]
+        if not all(os.path.isdir(d) for d in dirs):
+            continue
+        cmds += profile_commands(name, "stalls")
+        M = {}
+        for d in dirs:
+            for c, v in _pmc_values(d).items():
+                M.setdefault(c, _per_kernel_mean(v))
+        for k in sorted(M["SQ_WAVES"]):
+            g = M["GRBM_GUI_ACTIVE"][k][1]
+            occ = 4 * M["SQ_WAVE_CYCLES"][k][1] / (g / 8) / 256 if g else 0.0
+            lvl = M["SQ_INST_LEVEL_VMEM"][k][1] / max(1.0, M["SQ_INSTS_VMEM"][k][1])
+            ta = M["TA_ADDR_STALLED_BY_TC_CYCLES_sum"][k][1] / g if g else 0.0
+            cr = (M["TCC_EA0_RDREQ_DRAM_CREDIT_STALL_sum"][k][1] + M["TCC_EA0_WRREQ_DRAM_CREDIT_STALL_sum"][k][1]) / g \
+                if g else 0.0
+            rows.append(f"| {name} | `{k}` | {_role(k)} | {occ:.1f} | {lvl:.1f} | {ta:.2f} | {cr:.3f} |")
+    if rows:
+        lines = ["# Where the mover kernels wait", "",
+                 "Commands (from /tmp with TMPDIR=/tmp; one rocprofv3 run per counter set):", "", "```", *cmds, "```",
+                 "", "Per dispatch, averaged over the dispatches of each kernel (the GRBM_GUI_ACTIVE of each run "
+                     "normalises its own counters).  Resident waves per CU = 4 x SQ_WAVE_CYCLES / (GRBM_GUI_ACTIVE / "
+                     "8 XCDs) / 256 CUs (SQ_WAVE_CYCLES counts quad-cycles; a CU holds 32 waves).  VMEM level = "
+                     "SQ_INST_LEVEL_VMEM / SQ_INSTS_VMEM (how long a vector memory instruction stays "
+                     "outstanding, relative).  TA address stalls on the vector L1 and the L2's DRAM-credit stalls "
+                     "(reads + writes) per GRBM_GUI_ACTIVE cycle.", _TEMPLATE_NOTE, "",
+                 "| workload | kernel | role | resident waves per CU | VMEM level | TA stalled by TC | "
+                 "L2 DRAM-credit stalls |", "|---|---|---|---|---|---|---|", *rows, "", stamp, ""]
+        path = os.path.join(out_dir, "counters_stalls_tiles_vs_walks.md")
         with open(path, "w") as fh:
             fh.write("\n".join(lines))
         wrote.append(path)
