@@ -204,6 +204,13 @@ void to_pair(costa_dtype dt, const void* p, double out[2]) {
   else { out[0] = ((const float*)p)[0]; out[1] = ((const float*)p)[1]; }
 }
 
+// Timing events only measure: they skip the system-scope release (an L2
+// write-back between the kernels they bracket), which the call's own ordering
+// does not need.
+#ifndef COSTA_TIMING_EVENT_FLAGS
+#define COSTA_TIMING_EVENT_FLAGS hipEventDisableSystemFence
+#endif
+
 hipEvent_t get_event(State& S) {
   if (!S.event_pool.empty()) {
     hipEvent_t e = S.event_pool.back();
@@ -211,7 +218,7 @@ hipEvent_t get_event(State& S) {
     return e;
   }
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, COSTA_TIMING_EVENT_FLAGS) != hipSuccess) return nullptr;
   return e;
 }
 
