@@ -111,6 +111,8 @@ std::string plan_key(int device, int es, const std::vector<ItemDesc>& items, con
     put(&d.B->id, sizeof d.B->id);
     int32_t t = d.op == COSTA_OP_N ? 0 : 1;  // T and C move the same data
     put(&t, sizeof t);
+    const char r = d.reads_a ? 1 : 0;  // stacks on A's side form only for pairs that do not read A
+    put(&r, sizeof r);
   }
   size_t ns = sigma.size();
   put(&ns, sizeof ns);
@@ -127,6 +129,8 @@ PlanConfig make_config(int es) {
 }
 
 // Validates a batch; fills `items` and `sig`.  No device calls.
+bool is_zero(costa_dtype dt, const void* p);
+
 costa_status validate(costa_dtype dtype, int32_t n, const costa_transform_desc* desc, const int32_t* sigma,
                       bool need_buffers, std::vector<ItemDesc>& items, std::vector<int32_t>& sig) {
   if (elem_size(dtype) == 0) return fail(COSTA_ERROR_INVALID_VALUE, "unknown dtype");
@@ -154,7 +158,8 @@ costa_status validate(costa_dtype dtype, int32_t n, const costa_transform_desc* 
       if (!d.alpha || !d.beta) return fail(COSTA_ERROR_INVALID_VALUE, "null alpha or beta");
       if (!d.A_local || !d.B_local) return fail(COSTA_ERROR_INVALID_VALUE, "null buffer array");
     }
-    items.push_back(ItemDesc{A, B, d.op});
+    // a missing beta (plan queries) counts as one that reads A
+    items.push_back(ItemDesc{A, B, d.op, !(d.beta && is_zero(dtype, d.beta))});
   }
   sig.clear();
   if (sigma && P > 0) {

@@ -126,10 +126,25 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 //   allow 16-byte vectors.
 // PIECE_GROUP_NEXT: the next rectangle of the launch is moved by the same
 //   workgroup (a run of small rectangles shares one workgroup).
+// PIECE_STACK: one of a stack of row walks -- consecutive rectangles of a
+//   launch, of one pair, vector width and height ny, that follow one another
+//   along x on one side (the source, or the destination with
+//   PIECE_STACK_DST): the same buffer and stride there, each starting where
+//   the previous one ends.  The stack is moved as one band of the summed
+//   width (stack_tasks below); its first rectangle holds the number of
+//   rectangles in flags bits 16-31, and every rectangle of the stack has the
+//   stack's first task in task0 and aux.
 // A transposed rectangle is moved in LDS tiles of tile_x x tile_y elements
 // (tile_x along the destination's contiguous direction; choose_tile below),
 // packed into `aux` with tile_pack.
-enum : int32_t { PIECE_TRANSPOSE = 1, PIECE_WIDE = 2, PIECE_GROUP_NEXT = 16 };
+enum : int32_t {
+  PIECE_TRANSPOSE = 1,
+  PIECE_WIDE = 2,
+  PIECE_GROUP_NEXT = 16,
+  PIECE_STACK = 32,
+  PIECE_STACK_DST = 64
+};
+constexpr int32_t stack_size_of(int32_t flags) { return (int32_t)((uint32_t)flags >> 16); }
 
 struct alignas(16) Piece {
   int64_t src_off;
@@ -161,6 +176,38 @@ constexpr int32_t kThreadsPerTask = 256;
 constexpr int32_t kWideTaskUnits = (COSTA_COPY_UNITS > 1 ? COSTA_COPY_UNITS : 2) * kThreadsPerTask;
 constexpr int32_t kGroupUnitsMax = 128;  // rectangles of at most this many units may share a workgroup
 constexpr int32_t kGroupPiecesMax = 8;
+
+// Stacks (PIECE_STACK): rectangles whose rows are COSTA_STACK_MIN_RUN to
+// COSTA_STACK_MAX_RUN bytes long stack, up to kStackPiecesMax of them.  A
+// stack of height ny and summed width hu units (16-byte vectors when
+// PIECE_WIDE, else elements) is cut into wave tasks of 64 units of x by
+// kStackRows rows of y: wave task t covers units [64 * (t % wb), +64) and
+// rows [kStackRows * (t / wb), +kStackRows), wb = ceil(hu / 64), and
+// workgroup task c runs wave tasks 4c .. 4c + 3 (stack_tasks of them).
+// COSTA_STACK_MAX_RUN 0 turns stacks off.
+#ifndef COSTA_STACK_MIN_RUN
+#define COSTA_STACK_MIN_RUN 128
+#endif
+#ifndef COSTA_STACK_MAX_RUN
+#define COSTA_STACK_MAX_RUN 512
+#endif
+#ifndef COSTA_STACK_ROWS
+#define COSTA_STACK_ROWS 4
+#endif
+#ifndef COSTA_STACK_MIN_UNITS
+#define COSTA_STACK_MIN_UNITS 256  // narrower stacks, and stacks whose last wave would be mostly idle, do not form
+#endif
+constexpr int32_t kStackPiecesMax = 4096;
+constexpr int32_t kStackRows = COSTA_STACK_ROWS;
+constexpr int32_t kStackWave = 64;
+constexpr int64_t kStackWaveTasksMax = (1 << 23) - 1;  // the kernel divides wave tasks in fp32
+inline int64_t stack_wave_tasks(int64_t hu, int64_t ny) {
+  return ((hu + kStackWave - 1) / kStackWave) * ((ny + kStackRows - 1) / kStackRows);
+}
+inline int64_t stack_tasks(int64_t hu, int64_t ny) {
+  const int64_t per = kThreadsPerTask / kStackWave;
+  return (stack_wave_tasks(hu, ny) + per - 1) / per;
+}
 
 // Elements per 16-byte unit of a PIECE_WIDE rectangle.
 constexpr int32_t wide_elems(int32_t es) { return es >= 16 ? 1 : 16 / es; }

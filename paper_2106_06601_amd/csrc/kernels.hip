@@ -370,6 +370,133 @@ __device__ __forceinline__ void move_walk_lanes(const Piece* __restrict__ pieces
   }
 }
 
+// Stack walk (PIECE_STACK): the rectangles of a stack follow one another
+// along x on one side, so the stack is walked as one band of hu units per y,
+// in wave tasks of 64 units by kStackRows rows: wave v of task c takes wave
+// task t = 4c + v, units [64 * (t % wb), +64) of x -- one per lane, the same
+// for every row -- and rows [kStackRows * (t / wb), +kStackRows) of y.  The
+// wave finds once which rectangle holds each lane's unit (a binary search for
+// the last rectangle that starts at or before its first unit, then a scan
+// over those that start before its last), then moves its rows with up to
+// kStackRowsInFlight loads in flight per lane.  Every 64-lane access is
+// contiguous on the stacked side, wherever the rectangles' edges fall in a
+// 128-byte line.
+#ifndef COSTA_STACK_ROWS_IN_FLIGHT
+#define COSTA_STACK_ROWS_IN_FLIGHT 4
+#endif
+constexpr int kStackRowsInFlight = COSTA_STACK_ROWS_IN_FLIGHT;
+
+template <typename S, bool CPLX, int MODE, bool CONJ>
+__device__ __forceinline__ void move_stack(const Piece* __restrict__ pieces, int32_t pi, int32_t c,
+                                           void* const* __restrict__ bufs, int32_t allow_wide, S ar, S ai, S br,
+                                           S bi) {
+  using TT = TypeTraits<S, CPLX>;
+  using E = Vec<S, TT::NS>;
+  constexpr int W = TT::WIDE_NEL;
+  constexpr int YU = kStackRowsInFlight;
+  static_assert(MODE != MODE_AXPBY, "stacks hold no rectangles of pairs that read A");
+  const Piece& h = pieces[pi];
+  const int32_t np = stack_size_of(h.flags);
+  const bool on_dst = (h.flags & PIECE_STACK_DST) != 0;
+  const bool wide = (h.flags & PIECE_WIDE) != 0;
+  const int32_t epu = wide ? W : 1;  // elements per unit
+  const Piece& last = pieces[pi + np - 1];
+  const int64_t base = on_dst ? h.dst_off : h.src_off;
+  const int32_t hu = (int32_t)(((on_dst ? last.dst_off : last.src_off) + last.nx - base) / epu);
+  const int32_t wb = (hu + kStackWave - 1) / kStackWave;
+  const int32_t nt = wb * ((h.ny + kStackRows - 1) / kStackRows);
+  // this wave's task (wave-uniform)
+  const int32_t t = c * (kThreads / kStackWave) + __builtin_amdgcn_readfirstlane((int32_t)threadIdx.x / kStackWave);
+  if (t >= nt) return;  // past the stack's last wave task (no barrier follows)
+  int32_t chunk, band;
+  divmod(t, wb, chunk, band);
+  const int32_t w0 = band * kStackWave;
+  const int32_t xu = w0 + (int32_t)(threadIdx.x % kStackWave);
+  const int64_t x = (int64_t)xu * epu;  // this lane's element offset along the stack
+  const int64_t xw0 = (int64_t)w0 * epu;
+  const int64_t xw1 = (int64_t)min(w0 + kStackWave, hu) * epu;
+  // the last rectangle that starts at or before the wave's first unit
+  int32_t lo = 0, hi = np - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    const Piece& m = pieces[pi + mid];
+    if ((on_dst ? m.dst_off : m.src_off) - base <= xw0) lo = mid;
+    else hi = mid - 1;
+  }
+  int64_t soff = 0, doff = 0, sld = 0, dld = 0;
+  int32_t sbuf = 0, dbuf = 0;
+  for (int32_t k = lo; k < np; ++k) {
+    const Piece& p = pieces[pi + k];
+    const int64_t s0 = (on_dst ? p.dst_off : p.src_off) - base;
+    if (s0 >= xw1) break;
+    if (x >= s0 && x < s0 + p.nx) {
+      soff = p.src_off + (x - s0);
+      doff = p.dst_off + (x - s0);
+      sld = p.src_ld;
+      dld = p.dst_ld;
+      sbuf = p.src_buf;
+      dbuf = p.dst_buf;
+    }
+  }
+  if (xu >= hu) return;
+  const int32_t y0 = chunk * kStackRows;
+  const int32_t y1 = min(y0 + kStackRows, h.ny);
+  const S* sb = reinterpret_cast<const S*>(bufs[sbuf]) + (soff + (int64_t)y0 * sld) * TT::NS;
+  S* db = reinterpret_cast<S*>(bufs[dbuf]) + (doff + (int64_t)y0 * dld) * TT::NS;
+  const int64_t ss = sld * TT::NS, ds = dld * TT::NS;  // row strides in scalars
+  int32_t y = y0;
+  if (W > 1 && wide && allow_wide) {
+    using U = Vec<S, TT::NS * W>;
+    for (; y + YU <= y1; y += YU) {
+      U bv[YU];
+#pragma unroll
+      for (int k = 0; k < YU; ++k) bv[k] = load<TT::NT_WALK>(reinterpret_cast<const U*>(sb + k * ss));
+#pragma unroll
+      for (int k = 0; k < YU; ++k)
+        store(reinterpret_cast<U*>(db + k * ds), combine<S, TT::NS * W, CPLX, MODE, CONJ>(bv[k], bv[k], ar, ai, br, bi));
+      sb += YU * ss;
+      db += YU * ds;
+    }
+    for (; y < y1; ++y) {
+      const U bv = load<TT::NT_WALK>(reinterpret_cast<const U*>(sb));
+      store(reinterpret_cast<U*>(db), combine<S, TT::NS * W, CPLX, MODE, CONJ>(bv, bv, ar, ai, br, bi));
+      sb += ss;
+      db += ds;
+    }
+  } else {
+    // one element at a time (epu of them: a PIECE_WIDE stack in a call whose
+    // buffers are not 16-byte aligned)
+    const E* se = reinterpret_cast<const E*>(sb);
+    E* de = reinterpret_cast<E*>(db);
+    for (; y + YU <= y1; y += YU) {
+      E bv[YU][W];
+#pragma unroll
+      for (int k = 0; k < YU; ++k)
+#pragma unroll
+        for (int j = 0; j < W; ++j)
+          if (j < epu) bv[k][j] = load<TT::NT_WALK>(se + k * sld + j);
+#pragma unroll
+      for (int k = 0; k < YU; ++k)
+#pragma unroll
+        for (int j = 0; j < W; ++j)
+          if (j < epu)
+            store(de + k * dld + j, combine<S, TT::NS, CPLX, MODE, CONJ>(bv[k][j], bv[k][j], ar, ai, br, bi));
+      se += YU * sld;
+      de += YU * dld;
+    }
+    for (; y < y1; ++y) {
+#pragma unroll
+      for (int j = 0; j < W; ++j)
+        if (j < epu) {
+          const E bv = load<TT::NT_WALK>(se + j);
+          store(de + j, combine<S, TT::NS, CPLX, MODE, CONJ>(bv, bv, ar, ai, br, bi));
+        }
+      se += sld;
+      de += dld;
+    }
+  }
+}
+
 // One LDS tile of a rectangle whose source runs along y while the
 // destination runs along x: tile c (tiles numbered along x first) of
 // tile_x x tile_y elements, cut at the rectangle's edges to w x h.  Loads
@@ -460,6 +587,12 @@ __device__ __forceinline__ void move_task(const Piece* __restrict__ pieces, int3
       move_tile<S, CPLX, MODE, CONJ>(pieces, pi, c, bufs, lds, ar, ai, br, bi);
       return;
     }
+  } else if constexpr (MODE != MODE_AXPBY) {
+    // stacks outside the pack hold only rectangles of pairs that do not read A
+    if (flags & PIECE_STACK) {
+      move_stack<S, CPLX, MODE, CONJ>(pieces, pi, c, bufs, allow_wide, ar, ai, br, bi);
+      return;
+    }
   }
   if constexpr (TypeTraits<S, CPLX>::ES >= 16)
     move_walk_lanes<S, CPLX, MODE, CONJ, UL>(pieces, pi, c, bufs, allow_wide, ar, ai, br, bi);
@@ -491,6 +624,10 @@ __device__ __forceinline__ void mover_body(const Piece* __restrict__ pieces, con
   const int32_t pi = tasks[b];
   const int32_t c = b - (UL == 1 ? pieces[pi].task0 : pieces[pi].aux);
   if constexpr (KIND == KIND_PACK) {
+    if (pieces[pi].flags & PIECE_STACK) {
+      move_stack<S, CPLX, MODE_COPY, false>(pieces, pi, c, bufs, allow_wide, S(0), S(0), S(0), S(0));
+      return;
+    }
     if constexpr (TT::ES >= 16)
       move_walk_lanes<S, CPLX, MODE_COPY, false, UL>(pieces, pi, c, bufs, allow_wide, S(0), S(0), S(0), S(0));
     else

@@ -314,11 +314,75 @@ bool line_aligned(const Piece& p, int es) {
          (sstep == 1 || al(p.src_ld));
 }
 
+// Whether rectangle `q` continues rectangle `p` along x on the source
+// (side 0) or the destination (side 1): the same buffer and stride there, and
+// q starting where p ends.
+bool continues(const Piece& p, const Piece& q, int side) {
+  if (side == 0)
+    return q.src_buf == p.src_buf && (p.ny == 1 || q.src_ld == p.src_ld) && q.src_off == p.src_off + p.nx;
+  return q.dst_buf == p.dst_buf && (p.ny == 1 || q.dst_ld == p.dst_ld) && q.dst_off == p.dst_off + p.nx;
+}
+
+// Marks the stacks of a launch of row walks (PIECE_STACK): maximal runs of
+// consecutive rectangles of short rows that continue one another along x on
+// one side.  Returns, per rectangle, the length of the stack it starts (0 when
+// it starts none).  Rectangles cut from one block by the other layout's
+// splits lie one after another in a local column on one side; moved as one
+// band, each 64-lane access covers contiguous bytes there, and rows that end
+// inside a 128-byte line are written whole by one wave.  Measured on MI355X:
+// the ScaLAPACK-shaped copy with misaligned columns (32-row into 128-row
+// blocks, 16 x 16 ranks) +7% per step; the scaled transpose's unpack with
+// beta = 0 +4 to +7%, with beta != 0 -5% -- outside the pack (a copy), stacks
+// form only from rectangles of pairs that do not read A (reads_a), and the
+// kernel has no stack walk that reads A.
+std::vector<int32_t> mark_stacks(std::vector<Piece>& ps, int es, bool is_pack, const std::vector<char>& reads_a) {
+  std::vector<int32_t> len(ps.size(), 0);
+  if (COSTA_STACK_MAX_RUN <= 0) return len;
+  for (const Piece& p : ps)
+    if (p.flags & PIECE_TRANSPOSE) return len;
+  auto short_rows = [&](const Piece& p) {
+    return (int64_t)p.nx * es >= COSTA_STACK_MIN_RUN && (int64_t)p.nx * es <= COSTA_STACK_MAX_RUN;
+  };
+  size_t k = 0;
+  while (k < ps.size()) {
+    const Piece& h = ps[k];
+    size_t e = k + 1;
+    int side = -1;
+    int64_t width = h.nx;
+    const int64_t epu = (h.flags & PIECE_WIDE) ? wide_elems(es) : 1;
+    if (short_rows(h) && (is_pack || !reads_a[h.item])) {
+      while (e < ps.size() && e - k < (size_t)kStackPiecesMax) {
+        const Piece& q = ps[e];
+        if (!short_rows(q) || q.item != h.item || q.ny != h.ny || (q.flags & PIECE_WIDE) != (h.flags & PIECE_WIDE) ||
+            stack_wave_tasks((width + q.nx) / epu, h.ny) > kStackWaveTasksMax)
+          break;
+        if (side < 0) side = continues(ps[e - 1], q, 0) ? 0 : continues(ps[e - 1], q, 1) ? 1 : -1;
+        if (side < 0 || !continues(ps[e - 1], q, side)) break;
+        width += q.nx;
+        ++e;
+      }
+    }
+    // a stack narrower than a few waves leaves lanes of its last wave of
+    // every row idle: keep the rectangles' own walks there (measured on
+    // MI355X: stacks 50-300 units wide, the scaled transpose, 20% slower)
+    const int64_t hu = width / epu;
+    const int64_t lanes = (hu + kStackWave - 1) / kStackWave * kStackWave;
+    if (e - k >= 2 && hu >= COSTA_STACK_MIN_UNITS && 10 * hu >= 9 * lanes) {
+      len[k] = (int32_t)(e - k);
+      for (size_t j = k; j < e; ++j) ps[j].flags |= PIECE_STACK | (side == 1 ? PIECE_STACK_DST : 0);
+      ps[k].flags |= (int32_t)((uint32_t)(e - k) << 16);
+    }
+    k = e;
+  }
+  return len;
+}
+
 // Appends one launch: its rectangles and the workgroups that move them, in
 // rectangle order.  A transposed rectangle gets one workgroup per LDS tile
 // (tiles along x first); a row walk one per kThreadsPerTask units; runs of
-// small row walks of the same pair and vector width share one workgroup.
-LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nitems) {
+// small row walks of the same pair and vector width share one workgroup; a
+// stack the workgroups of its bands (stack_tasks).
+LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nitems, bool is_pack) {
   LaunchRange lr;
   lr.item_elems.assign(nitems, 0);
   lr.piece_begin = (int64_t)hp.pieces.size();
@@ -327,6 +391,14 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   if (hp.pieces.size() + ps.size() > (size_t)INT32_MAX)
     throw LimitExceeded("more than 2^31-1 rectangles in one plan");
   const int32_t base = (int32_t)hp.pieces.size();
+  const std::vector<int32_t> stack_len = mark_stacks(ps, es, is_pack, hp.item_reads_a);
+  // tasks of the stack each rectangle starts (0 for the others)
+  auto stack_ntasks = [&](size_t k) -> int64_t {
+    const Piece& h = ps[k];
+    const Piece& l = ps[k + stack_len[k] - 1];
+    const int64_t width = (h.flags & PIECE_STACK_DST) ? l.dst_off + l.nx - h.dst_off : l.src_off + l.nx - h.src_off;
+    return stack_tasks(width / ((h.flags & PIECE_WIDE) ? wide_elems(es) : 1), h.ny);
+  };
   int64_t b = 0;
   // the open run of small row walks
   int64_t g_task = -1;
@@ -341,6 +413,18 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     lr.elems += ne;
     lr.item_elems[p.item] += ne;
     const int32_t pi = base + (int32_t)k;
+    if (p.flags & PIECE_STACK) {
+      g_task = -1;
+      if (stack_len[k] == 0) {  // a later rectangle of the stack
+        p.task0 = ps[k - 1].task0;
+        continue;
+      }
+      const int64_t n = stack_ntasks(k);
+      p.task0 = (int32_t)b;
+      hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+      b += n;
+      continue;
+    }
     if (p.flags & PIECE_TRANSPOSE) {
       lr.has_transpose = true;
       g_task = -1;
@@ -386,8 +470,15 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     int64_t b2 = 0;
     for (size_t k = 0; k < ps.size(); ++k) {
       Piece& p = ps[k];
-      if (k > 0 && (ps[k - 1].flags & PIECE_GROUP_NEXT)) {
+      if (k > 0 && ((ps[k - 1].flags & PIECE_GROUP_NEXT) || ((p.flags & PIECE_STACK) && stack_len[k] == 0))) {
         p.aux = ps[k - 1].aux;
+        continue;
+      }
+      if (p.flags & PIECE_STACK) {  // the same tasks as in the task table
+        const int64_t n = stack_ntasks(k);
+        p.aux = (int32_t)b2;
+        hp.wide_tasks.insert(hp.wide_tasks.end(), (size_t)n, base + (int32_t)k);
+        b2 += n;
         continue;
       }
       const int64_t ne = (int64_t)p.nx * p.ny;
@@ -400,12 +491,18 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     lr.nwide = b2;
   }
   int64_t aligned = 0, transposed = 0;
+#ifndef COSTA_XCD_STACKS
+#define COSTA_XCD_STACKS 0
+#endif
   for (const Piece& p : ps) {
-    if (line_aligned(p, es)) aligned += (int64_t)p.nx * p.ny;
+    if (line_aligned(p, es) || (COSTA_XCD_STACKS && (p.flags & PIECE_STACK))) aligned += (int64_t)p.nx * p.ny;
     if (p.flags & PIECE_TRANSPOSE) transposed += (int64_t)p.nx * p.ny;
   }
   const bool one_kind = transposed == 0 || transposed == lr.elems;
-  lr.xcd_ranges = COSTA_XCD_RANGES && one_kind && lr.elems > 0 && 10 * aligned >= 9 * lr.elems ? 1 : 0;
+#ifndef COSTA_XCD_ALIGNED_TENTHS
+#define COSTA_XCD_ALIGNED_TENTHS 9
+#endif
+  lr.xcd_ranges = COSTA_XCD_RANGES && one_kind && lr.elems > 0 && 10 * aligned >= COSTA_XCD_ALIGNED_TENTHS * lr.elems ? 1 : 0;
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
 }
@@ -433,10 +530,10 @@ std::vector<LaunchRange> add_launches(HostPlan& hp, std::vector<Piece>& ps, int 
     for (const Piece& p : ps) ((p.flags & PIECE_TRANSPOSE) ? tiles : walks).push_back(p);
   }
   if (tiles.empty() || walks.empty()) {
-    out.push_back(add_launch(hp, ps, es, nitems));
+    out.push_back(add_launch(hp, ps, es, nitems, false));
   } else {
-    out.push_back(add_launch(hp, tiles, es, nitems));
-    out.push_back(add_launch(hp, walks, es, nitems));
+    out.push_back(add_launch(hp, tiles, es, nitems, false));
+    out.push_back(add_launch(hp, walks, es, nitems, false));
   }
   return out;
 }
@@ -472,6 +569,8 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
   hp.item_total.assign(n, 0);
   hp.item_local.assign(n, 0);
   hp.item_remote.assign(n, 0);
+  hp.item_reads_a.assign(n, 0);
+  for (int32_t k = 0; k < n; ++k) hp.item_reads_a[k] = items[k].reads_a ? 1 : 0;
   std::vector<Cand> local, remote;
   for (int32_t k = 0; k < n; ++k) {
     hp.item_total[k] = items[k].A->nrows * items[k].A->ncols;
@@ -580,7 +679,7 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     sort_by_key(unpack, dst_key);
     Wave w;
     w.msg_bytes = off;
-    w.pack = add_launch(hp, pack, es, n);
+    w.pack = add_launch(hp, pack, es, n, true);
     w.unpack = add_launches(hp, unpack, es, n);
     hp.workspace_bytes = std::max(hp.workspace_bytes, off);
     hp.waves.push_back(w);

@@ -13,6 +13,7 @@ struct ItemDesc {
   const Layout* A;
   const Layout* B;
   costa_op op;
+  bool reads_a;  // beta != 0: the pair's unpack and direct rectangles read A
 };
 
 struct PlanConfig {
@@ -30,6 +31,7 @@ struct HostPlan {
   int64_t workspace_bytes = 0;  // max message bytes of a wave
   // per pair: elements on each path
   std::vector<int64_t> item_total, item_local, item_remote;
+  std::vector<char> item_reads_a;
   int64_t overlay_blocks = 0;
   int32_t pieces_pack = 0, pieces_unpack = 0, pieces_direct = 0;
   double plan_ms = 0.0;

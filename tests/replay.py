@@ -84,3 +84,36 @@ def short_walk_cases():
                                                    BC(2400, 2400, 64, 64, 4, 4, "col", "col"), "T", 1.0, 0.0)],
                        False, seed=55),
     ]
+
+
+def stack_cases():
+    """Layouts whose row walks stack (rectangles with rows of 128-512 bytes
+    that follow one another along a local column, at least 256 units wide):
+    ScaLAPACK descriptors on 2 x 2 grids, 32-row source blocks into 128-row
+    target blocks with a different first process, padded leading dimensions
+    (columns alternately off the 128-byte lines) -- stacks on the source side
+    (pack) and on the destination side (unpack and the direct rectangles with
+    it, for pairs that do not read A); 16-byte units and single elements (odd
+    padding), all four element types, copy and scale (and axpby, whose
+    rectangles stack in the pack only), stacks whose last wave is partly idle
+    (1000 local rows) and row counts that are not a multiple of the rows per
+    wave task (blocks of 26 columns)."""
+    SL = synth.ScaLapack
+
+    def pair(m, n, pad_a, pad_b, mb=32):
+        B = SL(m, n, mb, mb, 0, 0, -(-(-(-m // mb)) // 2) * mb + pad_b, 2, 2)
+        A = SL(m, n, 128, 128, 1, 0, -(-(-(-m // 128)) // 2) * 128 + pad_a, 2, 2)
+        return A, B
+
+    out = []
+    A, B = pair(2048, 90, 8, 8)
+    out.append(synth.Workload("stack0", "f64", [synth.Item(A, B, "N", 1.0, 0.0)], False, seed=61))
+    A, B = pair(2000, 96, 8, 8)
+    out.append(synth.Workload("stack1", "f64", [synth.Item(A, B, "N", 2.0, 0.5)], False, seed=62))
+    A, B = pair(2048, 64, 1, 3)
+    out.append(synth.Workload("stack2", "f32", [synth.Item(A, B, "N", -1.5, 0.0)], False, seed=63))
+    A, B = pair(2048, 58, 4, 4, mb=16)
+    out.append(synth.Workload("stack3", "c128", [synth.Item(A, B, "N", 0.5 - 0.25j, 0.0)], False, seed=64))
+    A, B = pair(2048, 70, 4, 4)
+    out.append(synth.Workload("stack4", "c64", [synth.Item(A, B, "N", 1.0, 0.0)], False, seed=65))
+    return out

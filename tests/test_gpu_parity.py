@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from replay import many_rank_cases, short_walk_cases
+from replay import many_rank_cases, short_walk_cases, stack_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -311,6 +311,20 @@ def test_short_row_walks_full_compare(k):
     it = w.items[0]
     _say(f"short walks {k}: {w.dtype} {it.A.nrows}x{it.A.ncols} op={it.op} sigma={sigma}")
     case = Case(w, sigma=sigma)
+    case.run()
+    case.check_full()
+
+
+@pytest.mark.parametrize("k", range(5))
+def test_stacked_walks_full_compare(k):
+    """Row walks moved as stacks (rectangles that follow one another along a
+    local column, on the source or the destination side; 16-byte units and
+    single elements, four element types, copy, scale and axpby, a partly idle
+    last wave, row counts off the wave task's rows), every element compared."""
+    w = stack_cases()[k]
+    it = w.items[0]
+    _say(f"stacked walks {k}: {w.dtype} {it.A.nrows}x{it.A.ncols} alpha={it.alpha} beta={it.beta}")
+    case = Case(w)
     case.run()
     case.check_full()
 

@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from replay import _combine, _index, many_rank_cases, short_walk_cases
+from replay import _combine, _index, many_rank_cases, short_walk_cases, stack_cases
 
 C = pytest.importorskip("paper_2106_06601_amd")
 
@@ -27,9 +27,49 @@ PACK, UNPACK, DIRECT = 0, 1, 2
 # workgroup per 256 units (16-byte vectors when flag 2 is set, else
 # elements); a run of small row walks (each but the last flagged 16) by one
 # workgroup for all of them.
+# A stack (flag 32; 64: stacked on the destination side, else the source)
+# is a run of row walks of one pair, vector width and height, each with rows
+# of STACK_RUN[0] to STACK_RUN[1] bytes, that follow one another along x on
+# that side; its first rectangle holds the stack's length in flags bits
+# 16-31.  It is cut into wave tasks of 64 units of x by STACK_ROWS rows, and
+# moved by ceil(wave tasks / 4) workgroups, in both task tables.
 CAP = {4: 4224, 8: 2176, 16: 3328}
 MAXX = {4: 128, 8: 128, 16: 256}
 LANES, GROUP_UNITS, GROUP_PIECES, WIDE_UNITS = 256, 128, 8, 512
+STACK_RUN, STACK_ROWS = (128, 512), 4
+
+
+def _stacks(ps, es):
+    """{index of a stack's first rectangle: (length, workgroups)} of one
+    launch, after checking the stack contract."""
+    out = {}
+    k = 0
+    while k < len(ps):
+        fl = int(ps[k]["flags"])
+        if not fl & 32:
+            assert fl >> 16 == 0
+            k += 1
+            continue
+        n = fl >> 16
+        assert n >= 2 and k + n <= len(ps), "a stack starts with its length"
+        side = "dst" if fl & 64 else "src"
+        h = ps[k]
+        for j in range(k, k + n):
+            q = ps[j]
+            qf = int(q["flags"])
+            assert qf & 32 and (qf & 64) == (fl & 64) and (j == k or qf >> 16 == 0)
+            assert not qf & (1 | 16) and (qf & 2) == (fl & 2)
+            assert int(q["item"]) == int(h["item"]) and int(q["ny"]) == int(h["ny"])
+            assert STACK_RUN[0] <= int(q["nx"]) * es <= STACK_RUN[1]
+            if j > k:
+                p = ps[j - 1]
+                assert int(q[side + "_buf"]) == int(p[side + "_buf"])
+                assert int(q[side + "_off"]) == int(p[side + "_off"]) + int(p["nx"]), "stacked rectangles are contiguous"
+                assert int(h["ny"]) == 1 or int(q[side + "_ld"]) == int(p[side + "_ld"])
+        width = sum(int(ps[j]["nx"]) for j in range(k, k + n)) // (16 // es if fl & 2 and es < 16 else 1)
+        out[k] = (n, -(-(-(-width // 64) * -(-int(h["ny"]) // STACK_ROWS)) // (LANES // 64)))
+        k += n
+    return out
 
 
 def check_tasks(pieces, es):
@@ -46,9 +86,23 @@ def check_tasks(pieces, es):
         T = {bool(int(p["flags"]) & 1) for p in ps}
         assert kind == PACK and T == {False} or len(T) == 1, "a launch holds tiles or row walks, not both"
     for ps in launches.values():
+        stacks = _stacks(ps, es)
+        assert not stacks or not any(int(p["flags"]) & 1 for p in ps), "stacks only in launches of row walks"
         nxt = 0
         run = None  # (units so far, rectangles so far, item, vector width) of an open run
-        for p in ps:
+        skip = 0
+        for i, p in enumerate(ps):
+            if skip:
+                skip -= 1
+                continue
+            if i in stacks:
+                n, need = stacks[i]
+                assert run is None
+                for q in ps[i:i + n]:
+                    assert int(q["group"]) == nxt and int(q["ntasks"]) == need
+                nxt += need
+                skip = n - 1
+                continue
             nx, ny, fl = int(p["nx"]), int(p["ny"]), int(p["flags"])
             if run is not None:  # continues the run of the previous rectangle
                 assert not fl & 1 and int(p["group"]) == nxt - 1 and int(p["ntasks"]) == 1
@@ -84,8 +138,18 @@ def check_tasks(pieces, es):
         if any(int(p["flags"]) & 1 for p in ps):
             assert all(int(p["wide_group"]) == -1 and int(p["wide_ntasks"]) == 0 for p in ps)
             continue
-        nxt, in_run = 0, False
-        for p in ps:
+        nxt, in_run, skip = 0, False, 0
+        for i, p in enumerate(ps):
+            if skip:
+                skip -= 1
+                continue
+            if i in stacks:
+                n, need = stacks[i]
+                for q in ps[i:i + n]:
+                    assert int(q["wide_group"]) == nxt and int(q["wide_ntasks"]) == need
+                nxt += need
+                skip = n - 1
+                continue
             nx, ny, fl = int(p["nx"]), int(p["ny"]), int(p["flags"])
             if in_run:
                 assert int(p["wide_group"]) == nxt - 1 and int(p["wide_ntasks"]) == 1
@@ -108,7 +172,25 @@ def _descs(w):
     return descs, keep
 
 
-def replay(w, sigma=None, limit=None):
+def _written_mask(it, sigma):
+    """Per rank of A, the local elements that belong to the matrix (the
+    oracle's transform of ones, marking what it writes; padding rows of a
+    ScaLAPACK leading dimension stay 0)."""
+    OA, OB = oracle.OLayout(it.A), oracle.OLayout(it.B)
+    P = it.A.nranks
+    sg = list(range(P)) if sigma is None else list(sigma)
+    inv = [0] * P
+    for t, r in enumerate(sg):
+        inv[r] = t
+    marks = [np.zeros(OA.local_elems(inv[r]), np.float64) for r in range(P)]
+    ones = [np.ones(OB.local_elems(s), np.float64) for s in range(P)]
+    oracle.transform("f64", "N" if it.op == "N" else "T", 1.0, 0.0, OA, marks, OB, ones, sigma)
+    return [m.astype(np.int32) for m in marks]
+
+
+def replay(w, sigma=None, limit=None, padded=False):
+    """padded: A's local buffers hold elements outside the matrix (padded
+    leading dimensions), which must stay unwritten."""
     descs, keep = _descs(w)
     if limit:
         C.costa_set_workspace_limit(limit)
@@ -171,8 +253,13 @@ def replay(w, sigma=None, limit=None):
             ha.append(a)
         hb = [bufs[n * P + k * P + s] for s in range(P)]
         oracle.transform(w.dtype, it.op, it.alpha, it.beta, OA, ha, OB, hb, sigma)
+        want = _written_mask(it, sigma) if padded else None
         for r in range(P):
-            assert np.all(hits[k * P + r] == 1), "an element of A is not written exactly once"
+            if padded:
+                assert np.array_equal(hits[k * P + r], want[r]), "an element of A is not written exactly once"
+                assert want[r].any() or want[r].size == 0
+            else:
+                assert np.all(hits[k * P + r] == 1), "an element of A is not written exactly once"
             u = np.uint64 if w.dtype in ("f64", "c128") else np.uint32
             assert np.array_equal(bufs[k * P + r].view(u), ha[r].view(u)), f"pair {k} rank {r} differs"
     return pieces, stats
@@ -295,3 +382,96 @@ def test_full_size_plans_stay_in_bounds(name):
     assert ((ny == 1) | (x["dst_ld"] >= nx)).all()
     written = (nx * ny)[x["kind"] != PACK].sum()
     assert written == st["total_elems"]
+
+
+def stack_walk_cover(ps, es):
+    """The elements that the workgroups of each stack move, computed with the
+    kernel's index arithmetic: wave v of task c takes wave task t = 4c + v
+    (none past the stack's last), units [64 * (t % wb), +64) of x and rows
+    [STACK_ROWS * (t // wb), +STACK_ROWS); the wave finds the last rectangle
+    starting at or before its first unit by binary search, then scans forward
+    while rectangles start before its end; each lane keeps the rectangle that
+    holds its unit.  Returns {rectangle index: times each of its (y, x)
+    elements is moved}."""
+    cover = {}
+    stacks = _stacks(ps, es)
+    for k, (n, ntasks) in stacks.items():
+        fl = int(ps[k]["flags"])
+        side = "dst" if fl & 64 else "src"
+        epu = 16 // es if fl & 2 and es < 16 else 1
+        base = int(ps[k][side + "_off"])
+        s0 = np.array([int(ps[j][side + "_off"]) - base for j in range(k, k + n)], np.int64)
+        nxs = np.array([int(ps[j]["nx"]) for j in range(k, k + n)], np.int64)
+        ny = int(ps[k]["ny"])
+        hu = int((s0[-1] + nxs[-1]) // epu)
+        wb = -(-hu // 64)
+        nt = wb * -(-ny // STACK_ROWS)
+        for j in range(n):
+            cover[k + j] = np.zeros((ny, int(nxs[j])), np.int32)
+        for c in range(ntasks):
+            for v in range(LANES // 64):
+                t = c * (LANES // 64) + v
+                if t >= nt:
+                    continue
+                chunk, band = divmod(t, wb)
+                y0, y1 = chunk * STACK_ROWS, min(chunk * STACK_ROWS + STACK_ROWS, ny)
+                w0 = band * 64
+                xw0, xw1 = w0 * epu, min(w0 + 64, hu) * epu
+                lo, hi = 0, n - 1
+                while lo < hi:
+                    mid = (lo + hi + 1) >> 1
+                    if s0[mid] <= xw0:
+                        lo = mid
+                    else:
+                        hi = mid - 1
+                xu = w0 + np.arange(64)
+                x = xu * epu
+                sel = np.full(64, -1)
+                q = lo
+                while q < n and s0[q] < xw1:
+                    sel[(x >= s0[q]) & (x < s0[q] + nxs[q])] = q
+                    q += 1
+                for lane in np.nonzero(xu < hu)[0]:
+                    q = sel[lane]
+                    assert q >= 0, "a lane of the stack finds no rectangle"
+                    xo = int(x[lane] - s0[q])
+                    cover[k + q][y0:y1, xo:xo + epu] += 1
+    return cover
+
+
+@pytest.mark.parametrize("case", list(range(5)) + ["short_walks", "scaled_transpose_20k"])
+def test_stack_walks_move_each_element_once(case):
+    """The stack walk's lane arithmetic, replayed on the CPU over plans with
+    stacks (and over cases whose walks do not stack): every element of every
+    stacked rectangle is moved by exactly one lane of one workgroup."""
+    if isinstance(case, int):
+        ws = [stack_cases()[case]]
+    elif case == "short_walks":
+        ws = short_walk_cases()
+    else:
+        ws = [synth.workload(case, scale="small")]
+    nstacked = 0
+    for w in ws:
+        descs, keep = _descs(w)
+        x = C.costa_plan_export(w.dtype, descs, None)
+        es = synth.ITEMSIZE[w.dtype]
+        check_tasks(x, es)
+        launches = {}
+        for i in range(len(x)):
+            launches.setdefault((int(x[i]["kind"]), int(x[i]["launch"])), []).append(x[i])
+        for (kind, _), ps in launches.items():
+            cover = stack_walk_cover(ps, es)
+            nstacked += len(cover)
+            if kind != PACK:  # outside the pack, stacks hold only pairs that do not read A
+                assert all(complex(w.items[int(ps[k]["item"])].beta) == 0 for k in cover)
+            for k, cv in cover.items():
+                assert (cv == 1).all(), f"rectangle {k} of a stack: elements moved {cv.min()}..{cv.max()} times"
+    if isinstance(case, int):
+        assert nstacked > 0, "the case has no stacks"
+
+
+@pytest.mark.parametrize("k", range(5))
+def test_replay_stacked_walks(k):
+    """Layouts whose walks stack, replayed rectangle by rectangle: in bounds,
+    every element of A written once, equal to the oracle."""
+    replay(stack_cases()[k], padded=True)
