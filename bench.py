@@ -278,7 +278,7 @@ PROFILE_WORKLOADS = ["reshuffle_transpose_1k", "blocksize_change_16k", "scaled_t
                      "rpa_batched_tall_skinny"]
 PROFILE_CALLS = ["pdgemr2d_16k", "pdgemr2d_scatter_16k", "pdtran_16k", "pztranc_8k"]
 TRAFFIC_WORKLOADS = ["blocksize_change_16k", "scaled_transpose_20k", "cosma_complex_16k", "rpa_batched_tall_skinny",
-                     "pztranc_8k"]
+                     "pdgemr2d_16k", "pdtran_16k", "pztranc_8k"]
 LDS_WORKLOADS = ["reshuffle_transpose_1k", "cosma_complex_16k", "rpa_batched_tall_skinny", "pdtran_16k",
                  "pztranc_8k"]
 PMC_READ = "TCC_BUBBLE_sum TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_32B_sum"
