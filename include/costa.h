@@ -414,7 +414,9 @@ typedef struct {
   int64_t bytes[COSTA_KERNEL_KINDS];    /* summed algorithmic bytes */
 } costa_timing;
 
-/* on != 0: bracket every later launch with HIP events.  Resets the counters. */
+/* on != 0: bracket every later launch with HIP events (2048 of them are
+ * created here, on the current device, so that the timed calls do not create
+ * them).  Resets the counters. */
 costa_status costa_timing_enable(int on);
 /* Waits for the recorded events, adds up their durations, returns the totals
  * since costa_timing_enable and keeps counting. */

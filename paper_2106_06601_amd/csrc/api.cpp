@@ -216,6 +216,8 @@ void to_pair(costa_dtype dt, const void* p, double out[2]) {
 #define COSTA_TIMING_EVENT_FLAGS hipEventDisableSystemFence
 #endif
 
+constexpr size_t kTimingEventsUpFront = 2048;
+
 hipEvent_t get_event(State& S) {
   if (!S.event_pool.empty()) {
     hipEvent_t e = S.event_pool.back();
@@ -967,6 +969,18 @@ extern "C" costa_status costa_timing_enable(int on) {
     costa_status st = collect_timing(S);
     S.timing = on != 0;
     S.totals = costa_timing{};
+    // create the events up front (hipEventCreate can take tens of
+    // microseconds; created lazily, they would land in the timed calls)
+    if (st == COSTA_SUCCESS && S.timing && S.event_pool.size() < kTimingEventsUpFront) {
+      int dev = 0;
+      if (hipGetDevice(&dev) == hipSuccess) {
+        while (S.event_pool.size() < kTimingEventsUpFront) {
+          hipEvent_t e = nullptr;
+          if (hipEventCreateWithFlags(&e, COSTA_TIMING_EVENT_FLAGS) != hipSuccess) break;
+          S.event_pool.push_back(e);
+        }
+      }
+    }
     return st;
   });
 }

@@ -16,8 +16,11 @@
 // workgroup.
 #include <algorithm>
 #include <chrono>
+#include <cstdlib>
+#include <exception>
 #include <new>
 #include <numeric>
+#include <thread>
 #include <tuple>
 
 #include "plan.hpp"
@@ -51,9 +54,49 @@ std::vector<Interval> overlay(const std::vector<int64_t>& sa, const std::vector<
 
 namespace {
 
+// Host threads of the planner: COSTA_PLAN_THREADS if set (1 plans on the
+// calling thread alone), else the hardware's threads, at most 16.  The plan
+// is the same whatever the count: work is split into ranges whose results
+// are joined in order, and sorts order unique keys.
+int plan_threads() {
+  if (const char* e = std::getenv("COSTA_PLAN_THREADS")) {
+    const int v = std::atoi(e);
+    if (v >= 1) return std::min(v, 64);
+  }
+  const unsigned h = std::thread::hardware_concurrency();
+  return (int)std::max(1u, std::min(h, 16u));
+}
+
+// fn(t) for t in [0, n) on up to `threads` threads (the calling one
+// included); an exception in any is rethrown here after all have joined.
+template <typename Fn>
+void parallel_for(int64_t n, int threads, Fn&& fn) {
+  const int64_t nt = std::min<int64_t>(n, threads);
+  if (nt <= 1) {
+    for (int64_t t = 0; t < n; ++t) fn(t);
+    return;
+  }
+  std::vector<std::exception_ptr> err((size_t)nt);
+  auto worker = [&](int64_t w) {
+    try {
+      for (int64_t t = w; t < n; t += nt) fn(t);
+    } catch (...) {
+      err[(size_t)w] = std::current_exception();
+    }
+  };
+  std::vector<std::thread> pool;
+  pool.reserve((size_t)nt - 1);
+  for (int64_t w = 1; w < nt; ++w) pool.emplace_back(worker, w);
+  worker(0);
+  for (std::thread& th : pool) th.join();
+  for (const std::exception_ptr& e : err)
+    if (e) std::rethrow_exception(e);
+}
+
 struct Cand {
   Piece p;
   int32_t kx0, kx1;  // x-interval range [kx0, kx1)
+  int32_t ly_start;  // y-interval index of its first strip
   int32_t ly_end;    // y-interval index following the last strip merged
   int32_t s, r;      // sender rank, receiving physical rank
 };
@@ -63,7 +106,6 @@ inline bool same_kind(const Piece& a, const Piece& b) {
          a.dst_ld == b.dst_ld;
 }
 
-// All overlay rectangles of one pair, merged; appended to `local` / `remote`.
 // Owner, leading dimension and local offset of a layout's blocks, with the
 // per-block-row and per-block-column parts of a block-cyclic layout (process
 // row or column and local start; ScaLAPACK INDXG2P / INDXG2L) taken once per
@@ -102,9 +144,15 @@ struct BlockMap {
   }
 };
 
+// All overlay rectangles of one pair, merged; appended to `local` / `remote`.
+// The strips along y are cut into ranges planned on up to `threads` threads
+// (each range starts with no open rectangles); the ranges are then stitched
+// in order, merging a range's rectangles that start on its first strip into
+// the open rectangles of the ranges before it -- the merges a single pass
+// over the strips makes, so the rectangles are the same.
 void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vector<int32_t>& sigma,
                std::vector<Cand>& local, std::vector<Cand>& remote, int64_t& overlay_blocks, int64_t& n_local,
-               int64_t& n_remote) {
+               int64_t& n_remote, int threads) {
   const Layout& A = *d.A;
   const Layout& B = *d.B;
   const BlockMap MA(A), MB(B);
@@ -121,94 +169,148 @@ void plan_pair(int32_t item, int32_t nitems, const ItemDesc& d, const std::vecto
   const int32_t KX = (int32_t)X.size(), LY = (int32_t)Y.size();
   overlay_blocks += (int64_t)KX * LY;
 
-  std::vector<int32_t> open(KX, -1);  // candidate (index into `all`) that starts at kx0 and may grow along y
-  std::vector<Cand> all;
-  std::vector<Cand> strip;
-  for (int32_t ly = 0; ly < LY; ++ly) {
-    strip.clear();
-    const Interval& yi = Y[ly];
-    for (int32_t kx = 0; kx < KX; ++kx) {
-      const Interval& xi = X[kx];
-      const Interval& ri = a_col ? xi : yi;  // row interval of this overlay block
-      const Interval& ci = a_col ? yi : xi;  // column interval
-      // destination block and label
-      const int32_t t = MA.owner(ri.a, ci.a);
-      const int32_t r = sigma.empty() ? t : sigma[t];
-      const int64_t pi = ri.start - A.rsplit[ri.a], pj = ci.start - A.csplit[ci.a];
-      const int64_t lda = MA.ld(ri.a, ci.a);
-      const int64_t dst_off = MA.offset(ri.a, ci.a, lda) + (a_col ? pi + pj * lda : pi * lda + pj);
-      // source block: op(B) block (ri.b, ci.b) is B block (ci.b, ri.b) for T/C
-      const int32_t bi = tr ? ci.b : ri.b, bj = tr ? ri.b : ci.b;
-      const int32_t s = MB.owner(bi, bj);
-      const int64_t ldb = MB.ld(bi, bj);
-      // B element of A's (i, j): B(i, j) for N, B(j, i) for T/C
-      const int64_t qrow = tr ? ci.start - B.rsplit[bi] : ri.start - B.rsplit[bi];
-      const int64_t qcol = tr ? ri.start - B.csplit[bj] : ci.start - B.csplit[bj];
-      const int64_t s_brow = b_col ? 1 : ldb, s_bcol = b_col ? ldb : 1;  // strides of B's row / col index
-      const int64_t src_off = MB.offset(bi, bj, ldb) + qrow * s_brow + qcol * s_bcol;
-      const int64_t s_i = tr ? s_bcol : s_brow;  // stride along A's row index i
-      const int64_t s_j = tr ? s_brow : s_bcol;  // stride along A's column index j
-      const int64_t sx = a_col ? s_i : s_j, sy = a_col ? s_j : s_i;
+  // whether c (starting on strip ly) continues q along y
+  auto continues_y = [](const Cand& q, const Cand& c, int32_t ly) {
+    const int64_t step = (q.p.flags & PIECE_TRANSPOSE) ? 1 : q.p.src_ld;
+    return q.ly_end == ly && q.kx1 == c.kx1 && same_kind(q.p, c.p) &&
+           c.p.dst_off == q.p.dst_off + (int64_t)q.p.ny * q.p.dst_ld &&
+           c.p.src_off == q.p.src_off + (int64_t)q.p.ny * step && (int64_t)q.p.ny + c.p.ny <= INT32_MAX;
+  };
+  struct Range {
+    std::vector<Cand> all;
+    std::vector<int32_t> open;  // per kx0: candidate that may still grow along y
+    int64_t n_local = 0, n_remote = 0;
+  };
+  const int64_t cells = (int64_t)KX * LY;
+  const int nr = (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)threads, LY, cells / 65536 + 1}));
+  std::vector<Range> R((size_t)nr);
+  parallel_for(nr, nr, [&](int64_t ri_) {
+    Range& rg = R[(size_t)ri_];
+    const int32_t ly0 = (int32_t)((int64_t)LY * ri_ / nr), ly1 = (int32_t)((int64_t)LY * (ri_ + 1) / nr);
+    rg.open.assign(KX, -1);
+    std::vector<Cand> strip;
+    for (int32_t ly = ly0; ly < ly1; ++ly) {
+      strip.clear();
+      const Interval& yi = Y[ly];
+      for (int32_t kx = 0; kx < KX; ++kx) {
+        const Interval& xi = X[kx];
+        const Interval& ri = a_col ? xi : yi;  // row interval of this overlay block
+        const Interval& ci = a_col ? yi : xi;  // column interval
+        // destination block and label
+        const int32_t t = MA.owner(ri.a, ci.a);
+        const int32_t r = sigma.empty() ? t : sigma[t];
+        const int64_t pi = ri.start - A.rsplit[ri.a], pj = ci.start - A.csplit[ci.a];
+        const int64_t lda = MA.ld(ri.a, ci.a);
+        const int64_t dst_off = MA.offset(ri.a, ci.a, lda) + (a_col ? pi + pj * lda : pi * lda + pj);
+        // source block: op(B) block (ri.b, ci.b) is B block (ci.b, ri.b) for T/C
+        const int32_t bi = tr ? ci.b : ri.b, bj = tr ? ri.b : ci.b;
+        const int32_t s = MB.owner(bi, bj);
+        const int64_t ldb = MB.ld(bi, bj);
+        // B element of A's (i, j): B(i, j) for N, B(j, i) for T/C
+        const int64_t qrow = tr ? ci.start - B.rsplit[bi] : ri.start - B.rsplit[bi];
+        const int64_t qcol = tr ? ri.start - B.csplit[bj] : ci.start - B.csplit[bj];
+        const int64_t s_brow = b_col ? 1 : ldb, s_bcol = b_col ? ldb : 1;  // strides of B's row / col index
+        const int64_t src_off = MB.offset(bi, bj, ldb) + qrow * s_brow + qcol * s_bcol;
+        const int64_t s_i = tr ? s_bcol : s_brow;  // stride along A's row index i
+        const int64_t s_j = tr ? s_brow : s_bcol;  // stride along A's column index j
+        const int64_t sx = a_col ? s_i : s_j, sy = a_col ? s_j : s_i;
 
-      Cand c;
-      Piece& p = c.p;
-      p.dst_off = dst_off;
-      p.dst_ld = lda;
-      p.src_off = src_off;
-      p.nx = (int32_t)xi.len;
-      p.ny = (int32_t)yi.len;
-      if (sx == 1 || p.nx == 1) {
-        p.flags = 0;
-        p.src_ld = sy;
-      } else {
-        p.flags = PIECE_TRANSPOSE;  // sy == 1 here: one of the strides is always 1
-        p.src_ld = sx;
-      }
-      p.dst_buf = item * P + r;
-      p.src_buf = nitems * P + item * P + s;
-      p.item = item;
-      p.task0 = 0;
-      p.aux = 0;
-      c.kx0 = kx;
-      c.kx1 = kx + 1;
-      c.ly_end = ly + 1;
-      c.s = s;
-      c.r = r;
-      const int64_t ne = (int64_t)p.nx * p.ny;
-      if (s == r) n_local += ne;
-      else n_remote += ne;
-      // merge along x with the previous rectangle of this strip
-      if (!strip.empty()) {
-        Piece& q = strip.back().p;
-        const int64_t step = (q.flags & PIECE_TRANSPOSE) ? q.src_ld : 1;
-        if (same_kind(q, p) && q.ny == p.ny && p.dst_off == q.dst_off + q.nx &&
-            p.src_off == q.src_off + (int64_t)q.nx * step && (int64_t)q.nx + p.nx <= INT32_MAX) {
-          q.nx += p.nx;
-          strip.back().kx1 = kx + 1;
-          continue;
+        Cand c;
+        Piece& p = c.p;
+        p.dst_off = dst_off;
+        p.dst_ld = lda;
+        p.src_off = src_off;
+        p.nx = (int32_t)xi.len;
+        p.ny = (int32_t)yi.len;
+        if (sx == 1 || p.nx == 1) {
+          p.flags = 0;
+          p.src_ld = sy;
+        } else {
+          p.flags = PIECE_TRANSPOSE;  // sy == 1 here: one of the strides is always 1
+          p.src_ld = sx;
         }
+        p.dst_buf = item * P + r;
+        p.src_buf = nitems * P + item * P + s;
+        p.item = item;
+        p.task0 = 0;
+        p.aux = 0;
+        c.kx0 = kx;
+        c.kx1 = kx + 1;
+        c.ly_start = ly;
+        c.ly_end = ly + 1;
+        c.s = s;
+        c.r = r;
+        const int64_t ne = (int64_t)p.nx * p.ny;
+        if (s == r) rg.n_local += ne;
+        else rg.n_remote += ne;
+        // merge along x with the previous rectangle of this strip
+        if (!strip.empty()) {
+          Piece& q = strip.back().p;
+          const int64_t step = (q.flags & PIECE_TRANSPOSE) ? q.src_ld : 1;
+          if (same_kind(q, p) && q.ny == p.ny && p.dst_off == q.dst_off + q.nx &&
+              p.src_off == q.src_off + (int64_t)q.nx * step && (int64_t)q.nx + p.nx <= INT32_MAX) {
+            q.nx += p.nx;
+            strip.back().kx1 = kx + 1;
+            continue;
+          }
+        }
+        strip.push_back(c);
       }
-      strip.push_back(c);
-    }
-    // merge along y with the rectangle of the previous strip with the same x range
-    for (Cand& c : strip) {
-      int32_t o = open[c.kx0];
-      if (o >= 0) {
-        Cand& q = all[o];
-        const int64_t step = (q.p.flags & PIECE_TRANSPOSE) ? 1 : q.p.src_ld;
-        if (q.ly_end == ly && q.kx1 == c.kx1 && same_kind(q.p, c.p) &&
-            c.p.dst_off == q.p.dst_off + (int64_t)q.p.ny * q.p.dst_ld &&
-            c.p.src_off == q.p.src_off + (int64_t)q.p.ny * step && (int64_t)q.p.ny + c.p.ny <= INT32_MAX) {
+      // merge along y with the rectangle of the previous strip with the same x range
+      for (Cand& c : strip) {
+        const int32_t o = rg.open[c.kx0];
+        if (o >= 0 && continues_y(rg.all[o], c, ly)) {
+          Cand& q = rg.all[o];
           q.p.ny += c.p.ny;
           q.ly_end = ly + 1;
           continue;
         }
+        rg.open[c.kx0] = (int32_t)rg.all.size();
+        rg.all.push_back(c);
       }
-      open[c.kx0] = (int32_t)all.size();
-      all.push_back(c);
     }
+  });
+  // stitch the ranges in order: a rectangle on a range's first strip that
+  // continues an open rectangle of the ranges before is merged into it
+  std::vector<std::pair<int32_t, int32_t>> open((size_t)KX, {-1, -1});  // (range, index)
+  std::vector<std::vector<char>> dead((size_t)nr);
+  for (int r = 0; r < nr; ++r) {
+    Range& rg = R[(size_t)r];
+    n_local += rg.n_local;
+    n_remote += rg.n_remote;
+    dead[(size_t)r].assign(rg.all.size(), 0);
+    const int32_t ly0 = (int32_t)((int64_t)LY * r / nr);
+    std::vector<std::pair<int32_t, int32_t>> moved(rg.all.size());
+    for (size_t j = 0; j < rg.all.size(); ++j) {
+      Cand& c = rg.all[j];
+      moved[j] = {r, (int32_t)j};
+      if (r == 0 || c.ly_start != ly0) continue;
+      const std::pair<int32_t, int32_t> o = open[(size_t)c.kx0];
+      if (o.first < 0) continue;
+      Cand& q = R[(size_t)o.first].all[(size_t)o.second];
+      if (continues_y(q, c, ly0)) {
+        q.p.ny += c.p.ny;
+        q.ly_end = c.ly_end;
+        moved[j] = o;
+        dead[(size_t)r][j] = 1;
+      }
+    }
+    for (int32_t kx = 0; kx < KX; ++kx)
+      if (rg.open[kx] >= 0) open[(size_t)kx] = moved[(size_t)rg.open[kx]];
   }
-  for (Cand& c : all) (c.s == c.r ? local : remote).push_back(c);
+  size_t nl = local.size(), nrem = remote.size();
+  for (int r = 0; r < nr; ++r)
+    for (size_t j = 0; j < R[(size_t)r].all.size(); ++j)
+      if (!dead[(size_t)r][j]) (R[(size_t)r].all[j].s == R[(size_t)r].all[j].r ? nl : nrem) += 1;
+  local.reserve(nl);
+  remote.reserve(nrem);
+  for (int r = 0; r < nr; ++r) {
+    for (size_t j = 0; j < R[(size_t)r].all.size(); ++j) {
+      const Cand& c = R[(size_t)r].all[j];
+      if (!dead[(size_t)r][j]) (c.s == c.r ? local : remote).push_back(c);
+    }
+    std::vector<Cand>().swap(R[(size_t)r].all);
+  }
 }
 
 // Cuts of a rectangle larger than max_elems elements: (x0, y0, nx, ny) of
@@ -377,6 +479,22 @@ std::vector<int32_t> mark_stacks(std::vector<Piece>& ps, int es, bool is_pack, c
   return len;
 }
 
+// Appends n tasks to a task table: task t of the launch moves the rectangle
+// of the last segment (first task, rectangle) that starts at or before t.
+void fill_tasks(std::vector<int32_t>& table, const std::vector<std::pair<int64_t, int32_t>>& seg, int64_t n) {
+  const size_t at = table.size();
+  table.resize(at + (size_t)n);
+  int32_t* out = table.data() + at;
+  const int threads = n >= (1 << 20) ? plan_threads() : 1;
+  parallel_for(threads, threads, [&](int64_t t) {
+    const size_t s0 = seg.size() * (size_t)t / (size_t)threads, s1 = seg.size() * (size_t)(t + 1) / (size_t)threads;
+    for (size_t j = s0; j < s1; ++j) {
+      const int64_t end = j + 1 < seg.size() ? seg[j + 1].first : n;
+      std::fill(out + seg[j].first, out + end, seg[j].second);
+    }
+  });
+}
+
 // Appends one launch: its rectangles and the workgroups that move them, in
 // rectangle order.  A transposed rectangle gets one workgroup per LDS tile
 // (tiles along x first); a row walk one per kThreadsPerTask units; runs of
@@ -400,6 +518,10 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     return stack_tasks(width / ((h.flags & PIECE_WIDE) ? wide_elems(es) : 1), h.ny);
   };
   int64_t b = 0;
+  // (first task, rectangle) of every rectangle that starts tasks; the tables
+  // are filled from these once their sizes are known
+  std::vector<std::pair<int64_t, int32_t>> seg;
+  seg.reserve(ps.size());
   // the open run of small row walks
   int64_t g_task = -1;
   int64_t g_units = 0;
@@ -421,7 +543,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
       }
       const int64_t n = stack_ntasks(k);
       p.task0 = (int32_t)b;
-      hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+      seg.emplace_back(b, pi);
       b += n;
       continue;
     }
@@ -431,7 +553,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
       const int32_t tx = tile_x_of(p.aux), ty = tile_y_of(p.aux);
       const int64_t n = (int64_t)((p.nx + tx - 1) / tx) * ((p.ny + ty - 1) / ty);
       p.task0 = (int32_t)b;
-      hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+      seg.emplace_back(b, pi);
       b += n;
       continue;
     }
@@ -448,7 +570,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     }
     const int64_t n = (units + kThreadsPerTask - 1) / kThreadsPerTask;
     p.task0 = (int32_t)b;
-    hp.tasks.insert(hp.tasks.end(), (size_t)n, pi);
+    seg.emplace_back(b, pi);
     b += n;
     if (units <= kGroupUnitsMax) {
       g_task = b - 1;
@@ -463,11 +585,13 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   }
   if (b > INT32_MAX) throw LimitExceeded("more than 2^31-1 workgroups in one launch");
   lr.ntasks = b;
+  fill_tasks(hp.tasks, seg, b);
   // the wide task table of a launch of row walks: kWideTaskUnits units per
   // task, a run of small rectangles still one task
   lr.wide_begin = (int64_t)hp.wide_tasks.size();
   if (!lr.has_transpose) {
     int64_t b2 = 0;
+    seg.clear();
     for (size_t k = 0; k < ps.size(); ++k) {
       Piece& p = ps[k];
       if (k > 0 && ((ps[k - 1].flags & PIECE_GROUP_NEXT) || ((p.flags & PIECE_STACK) && stack_len[k] == 0))) {
@@ -477,7 +601,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
       if (p.flags & PIECE_STACK) {  // the same tasks as in the task table
         const int64_t n = stack_ntasks(k);
         p.aux = (int32_t)b2;
-        hp.wide_tasks.insert(hp.wide_tasks.end(), (size_t)n, base + (int32_t)k);
+        seg.emplace_back(b2, base + (int32_t)k);
         b2 += n;
         continue;
       }
@@ -485,10 +609,11 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
       const int64_t units = (p.flags & PIECE_WIDE) ? ne / wide_elems(es) : ne;
       const int64_t n = (p.flags & PIECE_GROUP_NEXT) ? 1 : (units + kWideTaskUnits - 1) / kWideTaskUnits;
       p.aux = (int32_t)b2;
-      hp.wide_tasks.insert(hp.wide_tasks.end(), (size_t)n, base + (int32_t)k);
+      seg.emplace_back(b2, base + (int32_t)k);
       b2 += n;
     }
     lr.nwide = b2;
+    fill_tasks(hp.wide_tasks, seg, b2);
   }
   int64_t aligned = 0, transposed = 0;
 #ifndef COSTA_XCD_STACKS
@@ -546,12 +671,31 @@ template <typename T, typename KeyFn>
 void sort_by_key(std::vector<T>& v, KeyFn key) {
   using K = decltype(key(v[0]));
   if (v.size() > (size_t)UINT32_MAX) throw LimitExceeded("more than 2^32-1 rectangles to order");
-  std::vector<std::pair<K, uint32_t>> ix(v.size());
-  for (size_t i = 0; i < v.size(); ++i) ix[i] = {key(v[i]), (uint32_t)i};
-  std::sort(ix.begin(), ix.end());
-  std::vector<T> out;
-  out.reserve(v.size());
-  for (const auto& e : ix) out.push_back(std::move(v[e.second]));
+  const size_t n = v.size();
+  std::vector<std::pair<K, uint32_t>> ix(n);
+  // sorted runs on several threads, merged pairwise (the keys are unique, so
+  // the order is the one a single sort gives)
+  const int threads = n >= (1u << 16) ? plan_threads() : 1;
+  int64_t runs = 1;
+  while (runs < threads) runs *= 2;
+  std::vector<size_t> bound((size_t)runs + 1);
+  for (int64_t r = 0; r <= runs; ++r) bound[(size_t)r] = n * (size_t)r / (size_t)runs;
+  parallel_for(runs, threads, [&](int64_t r) {
+    for (size_t i = bound[(size_t)r]; i < bound[(size_t)r + 1]; ++i) ix[i] = {key(v[i]), (uint32_t)i};
+    std::sort(ix.begin() + (ptrdiff_t)bound[(size_t)r], ix.begin() + (ptrdiff_t)bound[(size_t)r + 1]);
+  });
+  for (int64_t width = 1; width < runs; width *= 2) {
+    parallel_for(runs / (2 * width), threads, [&](int64_t m) {
+      const size_t lo = bound[(size_t)(2 * width * m)], mid = bound[(size_t)(2 * width * m + width)],
+                   hi = bound[(size_t)(2 * width * m + 2 * width)];
+      std::inplace_merge(ix.begin() + (ptrdiff_t)lo, ix.begin() + (ptrdiff_t)mid, ix.begin() + (ptrdiff_t)hi);
+    });
+  }
+  std::vector<T> out(n);
+  parallel_for(threads, threads, [&](int64_t r) {
+    for (size_t i = n * (size_t)r / (size_t)threads; i < n * (size_t)(r + 1) / (size_t)threads; ++i)
+      out[i] = std::move(v[ix[i].second]);
+  });
   v.swap(out);
 }
 
@@ -572,9 +716,31 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
   hp.item_reads_a.assign(n, 0);
   for (int32_t k = 0; k < n; ++k) hp.item_reads_a[k] = items[k].reads_a ? 1 : 0;
   std::vector<Cand> local, remote;
-  for (int32_t k = 0; k < n; ++k) {
-    hp.item_total[k] = items[k].A->nrows * items[k].A->ncols;
-    plan_pair(k, n, items[k], sigma, local, remote, hp.overlay_blocks, hp.item_local[k], hp.item_remote[k]);
+  {
+    // the pairs on several threads, joined in pair order
+    std::vector<std::vector<Cand>> loc((size_t)n), rem((size_t)n);
+    std::vector<int64_t> blocks((size_t)n, 0);
+    const int threads = plan_threads();
+    const int inner = std::max(1, threads / std::max(1, n));  // threads per pair
+    parallel_for(n, threads, [&](int64_t k) {
+      hp.item_total[k] = items[k].A->nrows * items[k].A->ncols;
+      plan_pair((int32_t)k, n, items[k], sigma, loc[k], rem[k], blocks[k], hp.item_local[k], hp.item_remote[k],
+                inner);
+    });
+    size_t nl = 0, nr = 0;
+    for (int32_t k = 0; k < n; ++k) {
+      nl += loc[k].size();
+      nr += rem[k].size();
+      hp.overlay_blocks += blocks[k];
+    }
+    local.reserve(nl);
+    remote.reserve(nr);
+    for (int32_t k = 0; k < n; ++k) {
+      local.insert(local.end(), loc[k].begin(), loc[k].end());
+      remote.insert(remote.end(), rem[k].begin(), rem[k].end());
+      std::vector<Cand>().swap(loc[k]);
+      std::vector<Cand>().swap(rem[k]);
+    }
   }
   split_pieces(local, cfg.max_piece_elems);
   split_pieces(remote, cfg.max_piece_elems);
@@ -624,6 +790,17 @@ void build_plan(const std::vector<ItemDesc>& items, const std::vector<int32_t>& 
     sort_by_key(remote, [](const Cand& c) { return std::make_tuple(c.r, c.s, c.p.src_buf, c.p.src_off); });
   }
 
+  // room for the task tables and rectangles of every launch (an upper bound
+  // of the tasks: one per 256 elements, plus the rounding of each
+  // rectangle), so that appending launches does not move the tables
+  {
+    int64_t est = 0;
+    for (const Cand& c : remote) est += 2 * ((int64_t)c.p.nx * c.p.ny / kThreadsPerTask + 2);
+    for (const Piece& p : direct) est += (int64_t)p.nx * p.ny / kThreadsPerTask + 2;
+    hp.tasks.reserve((size_t)est);
+    hp.wide_tasks.reserve((size_t)est);
+    hp.pieces.reserve(2 * remote.size() + direct.size());
+  }
   const int32_t msg_buf = 2 * n * (items.empty() ? 0 : items[0].A->nranks);
   size_t k = 0;
   while (k < remote.size()) {

@@ -475,3 +475,36 @@ def test_replay_stacked_walks(k):
     """Layouts whose walks stack, replayed rectangle by rectangle: in bounds,
     every element of A written once, equal to the oracle."""
     replay(stack_cases()[k], padded=True)
+
+
+@pytest.mark.parametrize("name", ["scaled_transpose_20k", "rpa_batched_tall_skinny", "pdgemr2d_16k"])
+def test_plans_do_not_depend_on_planner_threads(name, monkeypatch):
+    """The planner's threads (pairs, ranges of strips, sorts and task tables
+    split over up to 16) give the plan of a single thread, rectangle for
+    rectangle and task for task (full sizes, where every split engages)."""
+    import os
+    if name in synth.WORKLOADS:
+        w = synth.workload(name)
+        descs, keep = _descs(w)
+        dt = w.dtype
+    else:
+        call = synth.scalapack_call(name)
+        SA = C.layout_from_spec(call.A).submatrix(call.ia - 1, call.ja - 1, call.m, call.n)
+        SC = C.layout_from_spec(call.C).submatrix(call.ic - 1, call.jc - 1, call.m, call.n)
+        descs = [dict(op="N", alpha=1.0, beta=0.0, A=SC, B=SA)]
+        dt = call.dtype
+    limit = 18 << 30 if name == "rpa_batched_tall_skinny" else 0  # several waves
+    out = {}
+    for threads in ("1", "8"):
+        monkeypatch.setenv("COSTA_PLAN_THREADS", threads)
+        C.costa_finalize()  # empty the plan cache
+        C.costa_set_workspace_limit(limit)
+        try:
+            out[threads] = (C.costa_plan_export(dt, descs, None), C.costa_plan_stats(dt, descs, None))
+        finally:
+            C.costa_set_workspace_limit(0)
+    (x1, s1), (x8, s8) = out["1"], out["8"]
+    assert len(x1) > 100000
+    assert np.array_equal(x1.view(np.uint8), x8.view(np.uint8))
+    for k in ("waves", "workspace_bytes", "pieces_pack", "pieces_unpack", "pieces_direct", "model_bytes"):
+        assert s1[k] == s8[k], k
