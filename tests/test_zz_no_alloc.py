@@ -12,6 +12,7 @@ import torch
 
 import synth
 from parity import Case, lib
+from replay import stack_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -28,7 +29,10 @@ class Twin:
     """A workload on the device with a second copy of A for the no-allocation call."""
 
     def __init__(self, name, size=None):
-        self.w = synth.workload(name, size) if size else synth.workload(name)
+        if isinstance(name, synth.Workload):
+            self.w = name
+        else:
+            self.w = synth.workload(name, size) if size else synth.workload(name)
         self.case = Case(self.w)
         self.A2 = [[a.clone() for a in ak] for ak in self.case.A]
 
@@ -74,9 +78,11 @@ def test_noalloc_matches_the_allocating_entry_point():
     # 2) a smaller input right after it: the scaled transpose (alpha = 2,
     #    beta = 0.5: A is read) at reduced size, then the 1024^2 transpose
     #    with relabeling and the tall-skinny batch (mixed ops) at reduced size
+    #    and two layouts whose row walks stack (fp64 and single-element
+    #    float units)
     for name, size in (("scaled_transpose_20k", "small"), ("reshuffle_transpose_1k", None),
-                       ("rpa_batched_tall_skinny", "small")):
-        _say(f"noalloc: {name} {size or 'full size'}")
+                       ("rpa_batched_tall_skinny", "small"), (stack_cases()[0], None), (stack_cases()[2], None)):
+        _say(f"noalloc: {getattr(name, 'name', name)} {size or 'full size'}")
         t = Twin(name, size)
         t.run_and_compare()
         t.run_and_compare()  # the same plan again: tables already resident
