@@ -233,8 +233,11 @@ costa_status costa_relabel_cost(int32_t P, const int64_t* V_host, double elem_by
  * Buffers must hold costa_layout_local_elems() elements; a rank that owns
  * nothing may pass NULL.  A and B must not overlap.  Asynchronous on
  * `stream`; every argument error is returned before anything is enqueued.
- * The first call for a (layouts, op, sigma, type) combination builds and
- * caches a plan (host planning plus one upload). */
+ * The first call for a (layouts, op, sigma, type, whether beta is zero)
+ * combination builds and caches a plan (host planning plus one upload).
+ * Planning runs on up to 16 host threads, or on COSTA_PLAN_THREADS of them
+ * when that environment variable is set (1: the calling thread only); the
+ * plan does not depend on the count. */
 costa_status costa_transform(costa_dtype dtype, costa_op op, const void* alpha, const void* beta,
                              costa_layout A, void* const* A_local, costa_layout B,
                              const void* const* B_local, const int32_t* sigma, hipStream_t stream);
