@@ -861,10 +861,30 @@ def copy_ceiling(dev, stream, mib: int = 1024, reps: int = 10):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    del src, dst
+    # the same copy through the library: an identity transform between two
+    # single-rank layouts of one block (all of it on the direct path, the
+    # row-walk kernel's plain copy)
+    import synth
+    import paper_2106_06601_amd as C
+    n = nbytes // 8
+    spec = synth.BlockCyclic(8192, n // 8192, 8192, n // 8192, 1, 1)
+    L = C.layout_from_spec(spec)
+    C.costa_transform("f64", "N", 1.0, 0.0, L, [dst], L, [src], None, stream)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        C.costa_transform("f64", "N", 1.0, 0.0, L, [dst], L, [src], None, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_costa = e0.elapsed_time(e1) / reps
+    del src, dst, L
+    C.costa_finalize()
     torch.cuda.empty_cache()
     return {"GB_s": round(2 * nbytes / (ms * 1e-3) / 1e9, 1), "bytes_per_copy": 2 * nbytes,
-            "kind": f"device copy of {mib} MiB (torch copy_), read + write bytes"}
+            "kind": f"device copy of {mib} MiB (torch copy_), read + write bytes",
+            "costa_GB_s": round(2 * nbytes / (ms_costa * 1e-3) / 1e9, 1),
+            "costa_kind": f"the same {mib} MiB through costa_transform (one rank, one block: the direct "
+                          "path's row-walk copy)"}
 
 
 def scalapack_bench(name: str, args) -> dict:
