@@ -5,11 +5,12 @@
 // values and write one, with at most a few flops (Section 5 eq:costa).  The
 // movers are therefore built from one-shot workgroups: each takes one task
 // from the plan's task table -- 256 or 512 consecutive 16-byte units (or
-// elements) of a rectangle walked along its rows, or one LDS tile of a
-// rectangle whose source and destination run in different directions --
-// moves it with coalesced 64-lane accesses and exits, so the workgroups in
-// flight sweep the buffers in task order.  A launch whose tasks are all
-// alike may hand each XCD (one L2) a contiguous range of them.
+// elements) of a rectangle walked along its rows, four wave tasks of a stack
+// of short rectangles that follow one another along a local column, or one
+// LDS tile of a rectangle whose source and destination run in different
+// directions -- moves it with coalesced 64-lane accesses and exits, so the
+// workgroups in flight sweep the buffers in task order.  A launch whose
+// tasks are all alike may hand each XCD (one L2) a contiguous range of them.
 #include <hip/hip_runtime.h>
 
 #include "internal.hpp"

@@ -12,8 +12,10 @@
 // destination storage (for instance the blocks of one process row of a 1 x P
 // grid) are merged into one rectangle.  Each launch's rectangles are then cut
 // into workgroup tasks of equal size (an LDS tile of a transposed rectangle,
-// or a few KiB of a row walk), and runs of small rectangles share one
-// workgroup.
+// or a few KiB of a row walk); runs of small rectangles share one workgroup,
+// and stacks of short rectangles that follow one another on one side move as
+// one band.  The planning itself runs on host threads (plan_threads) and
+// gives the same plan whatever their number.
 #include <algorithm>
 #include <chrono>
 #include <cstdlib>
@@ -404,6 +406,16 @@ void finish_piece(Piece& p, int elem_size) {
 #ifndef COSTA_XCD_RANGES
 #define COSTA_XCD_RANGES 1
 #endif
+// Tenths of a launch's elements that must lie in line-aligned rectangles for
+// the ranges (0: every launch of one kind; measured: the scaled transpose
+// -8%, the complex case -4%, pdgemr2d's unpack +5% and its pack -1%).
+#ifndef COSTA_XCD_ALIGNED_TENTHS
+#define COSTA_XCD_ALIGNED_TENTHS 9
+#endif
+// 1: stacked rectangles count as aligned (measured: pdgemr2d -4%, pdtran -6%).
+#ifndef COSTA_XCD_STACKS
+#define COSTA_XCD_STACKS 0
+#endif
 
 // Whether every run of the rectangle (its rows in the source and in the
 // destination) starts and ends on a 128-byte line.
@@ -616,17 +628,11 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     fill_tasks(hp.wide_tasks, seg, b2);
   }
   int64_t aligned = 0, transposed = 0;
-#ifndef COSTA_XCD_STACKS
-#define COSTA_XCD_STACKS 0
-#endif
   for (const Piece& p : ps) {
     if (line_aligned(p, es) || (COSTA_XCD_STACKS && (p.flags & PIECE_STACK))) aligned += (int64_t)p.nx * p.ny;
     if (p.flags & PIECE_TRANSPOSE) transposed += (int64_t)p.nx * p.ny;
   }
   const bool one_kind = transposed == 0 || transposed == lr.elems;
-#ifndef COSTA_XCD_ALIGNED_TENTHS
-#define COSTA_XCD_ALIGNED_TENTHS 9
-#endif
   lr.xcd_ranges = COSTA_XCD_RANGES && one_kind && lr.elems > 0 && 10 * aligned >= COSTA_XCD_ALIGNED_TENTHS * lr.elems ? 1 : 0;
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
