@@ -297,7 +297,7 @@ _TEMPLATE_NOTE = ("Kernel template arguments: <scalar, complex, kind (0 pack, 1 
 def _bench_args(name: str) -> str:
     if name in PROFILE_CALLS:
         return f"--scalapack {name}"
-    return f"--workload {name} --no-cpu-baseline"
+    return f"--workload {name} --no-cpu-baseline --no-copy-ceiling"
 
 
 def profile_commands(name: str, what: str) -> list:
@@ -523,6 +523,8 @@ def summarize_profiles(src: str, out_dir: str = None) -> None:
                   "| kind | launches | FETCH+WRITE bytes per launch | ratio | DRAM read+write bytes per launch | "
                   "ratio | algorithmic bytes per launch |", "|---|---|---|---|---|---|---|"]
         for k, (n, sf, sw, sdr, sdw) in kinds.items():
+            if k not in dA["kernels"]:  # launches the timed steps do not make
+                continue
             hbm = round((sf / n * ff + sw / n * wf) * 1024)
             dram = round((sdr / n * drf + sdw / n * dwf) * 1024)
             alg = dA["kernels"][k]["bytes_per_launch"]
@@ -715,6 +717,9 @@ def main():
                     help="CPU-baseline time of a single workload (half of it per workload with 'all', 2 s for "
                          "the 1024^2 case)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy-ceiling", action="store_true",
+                    help="skip the 1 GiB copy probes after the workloads (profiling runs: their launches would "
+                         "join the kernel traces)")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1),
                     help="threads of the CPU baseline (default: up to 16, the host share of one GPU)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -766,7 +771,8 @@ def main():
     # context for the peak: a plain device copy, after every workload, so
     # that its 2 GiB of buffers are not allocated and freed between them
     head = recs[HEADLINE if HEADLINE in recs else names[0]]
-    head["copy_ceiling"] = copy_ceiling(torch.device("cuda:0"), torch.cuda.current_stream())
+    if not args.no_copy_ceiling:
+        head["copy_ceiling"] = copy_ceiling(torch.device("cuda:0"), torch.cuda.current_stream())
     out = {"metric": METRIC, "value": head["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": head["ms_per_step"], "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": head["dtype"], "data": "synthetic",
