@@ -78,6 +78,7 @@ struct TimingRec {
   costa_kernel_kind kind;
   hipEvent_t start, stop;
   int64_t bytes;
+  int device;  // the device the events belong to
 };
 
 struct State {
@@ -88,7 +89,7 @@ struct State {
   std::map<int, Workspace> ws;
   bool timing = false;
   std::vector<TimingRec> pending;
-  std::vector<hipEvent_t> event_pool;
+  std::map<int, std::vector<hipEvent_t>> event_pool;  // per device: events are recorded on that device's streams
   costa_timing totals{};
 };
 
@@ -218,15 +219,21 @@ void to_pair(costa_dtype dt, const void* p, double out[2]) {
 
 constexpr size_t kTimingEventsUpFront = 2048;
 
-hipEvent_t get_event(State& S) {
-  if (!S.event_pool.empty()) {
-    hipEvent_t e = S.event_pool.back();
-    S.event_pool.pop_back();
+// A timing event of the current device (from its pool, else a new one).
+hipEvent_t get_event(State& S, int device) {
+  std::vector<hipEvent_t>& pool = S.event_pool[device];
+  if (!pool.empty()) {
+    hipEvent_t e = pool.back();
+    pool.pop_back();
     return e;
   }
   hipEvent_t e = nullptr;
   if (hipEventCreateWithFlags(&e, COSTA_TIMING_EVENT_FLAGS) != hipSuccess) return nullptr;
   return e;
+}
+
+void put_event(State& S, int device, hipEvent_t e) {
+  if (e) S.event_pool[device].push_back(e);
 }
 
 costa_status collect_timing(State& S) {
@@ -237,8 +244,8 @@ costa_status collect_timing(State& S) {
     S.totals.ms[r.kind] += ms;
     S.totals.launches[r.kind] += 1;
     S.totals.bytes[r.kind] += r.bytes;
-    S.event_pool.push_back(r.start);
-    S.event_pool.push_back(r.stop);
+    put_event(S, r.device, r.start);
+    put_event(S, r.device, r.stop);
   }
   S.pending.clear();
   return COSTA_SUCCESS;
@@ -258,16 +265,18 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DeviceTab
                        int64_t bytes, hipStream_t stream, bool timed = true) {
   if (lr.ntasks == 0) return COSTA_SUCCESS;
   hipEvent_t e0 = nullptr, e1 = nullptr;
+  int device = 0;
   if (S.timing && timed) {
     if (S.pending.size() > 4096) {
       costa_status st = collect_timing(S);
       if (st != COSTA_SUCCESS) return st;
     }
-    e0 = get_event(S);
-    e1 = get_event(S);
+    HIP_OR_FAIL(hipGetDevice(&device));
+    e0 = get_event(S, device);
+    e1 = get_event(S, device);
     if (!e0 || !e1) {
-      if (e0) S.event_pool.push_back(e0);
-      if (e1) S.event_pool.push_back(e1);
+      put_event(S, device, e0);
+      put_event(S, device, e1);
       return fail(COSTA_ERROR_DEVICE, "hipEventCreate failed");
     }
     HIP_OR_FAIL(hipEventRecord(e0, stream));
@@ -281,7 +290,7 @@ costa_status run_range(State& S, MoverKind kind, costa_dtype dt, const DeviceTab
     costa_kernel_kind kk = kind == KIND_PACK ? COSTA_KERNEL_PACK
                            : kind == KIND_UNPACK ? COSTA_KERNEL_UNPACK
                                                  : COSTA_KERNEL_DIRECT;
-    S.pending.push_back(TimingRec{kk, e0, e1, bytes});
+    S.pending.push_back(TimingRec{kk, e0, e1, bytes, device});
   }
   return COSTA_SUCCESS;
 }
@@ -716,9 +725,10 @@ extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, 
     DevBuf d_rows, d_cols, d_oa, d_ob, d_v, d_hr, d_hc, d_ca, d_cb;
     std::vector<unsigned long long> zeros;
     hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (S.timing) {
-      e0 = get_event(S);
-      e1 = get_event(S);
+    int ev_device = 0;
+    if (S.timing && hipGetDevice(&ev_device) == hipSuccess) {
+      e0 = get_event(S, ev_device);
+      e1 = get_event(S, ev_device);
     }
     auto run = [&]() -> costa_status {
       HIP_OR_FAIL(d_v.alloc(sizeof(int64_t) * PP));
@@ -789,7 +799,8 @@ extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, 
       }
       if (e1) {
         HIP_OR_FAIL(hipEventRecord(e1, stream));
-        S.pending.push_back(TimingRec{COSTA_KERNEL_VOLUME, e0, e1, (int64_t)(rows.size() + cols.size()) * 24});
+        S.pending.push_back(
+            TimingRec{COSTA_KERNEL_VOLUME, e0, e1, (int64_t)(rows.size() + cols.size()) * 24, ev_device});
         e0 = e1 = nullptr;
       }
       HIP_OR_FAIL(hipMemcpyAsync(V_host, d_v.p, sizeof(int64_t) * PP, hipMemcpyDeviceToHost, stream));
@@ -798,8 +809,8 @@ extern "C" costa_status costa_volume_matrix(costa_layout A_h, costa_layout B_h, 
     };
     costa_status st = run();
     (void)hipStreamSynchronize(stream);  // device buffers are freed below
-    if (e0) S.event_pool.push_back(e0);
-    if (e1) S.event_pool.push_back(e1);
+    put_event(S, ev_device, e0);
+    put_event(S, ev_device, e1);
     return st;
   });
 }
@@ -971,14 +982,13 @@ extern "C" costa_status costa_timing_enable(int on) {
     S.totals = costa_timing{};
     // create the events up front (hipEventCreate can take tens of
     // microseconds; created lazily, they would land in the timed calls)
-    if (st == COSTA_SUCCESS && S.timing && S.event_pool.size() < kTimingEventsUpFront) {
-      int dev = 0;
-      if (hipGetDevice(&dev) == hipSuccess) {
-        while (S.event_pool.size() < kTimingEventsUpFront) {
-          hipEvent_t e = nullptr;
-          if (hipEventCreateWithFlags(&e, COSTA_TIMING_EVENT_FLAGS) != hipSuccess) break;
-          S.event_pool.push_back(e);
-        }
+    int dev = 0;
+    if (st == COSTA_SUCCESS && S.timing && hipGetDevice(&dev) == hipSuccess) {
+      std::vector<hipEvent_t>& pool = S.event_pool[dev];
+      while (pool.size() < kTimingEventsUpFront) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreateWithFlags(&e, COSTA_TIMING_EVENT_FLAGS) != hipSuccess) break;
+        pool.push_back(e);
       }
     }
     return st;
@@ -1021,7 +1031,8 @@ extern "C" costa_status costa_finalize(void) {
         if (kv.second.last_use) (void)hipEventDestroy(kv.second.last_use);
       }
       S.ws.clear();
-      for (hipEvent_t e : S.event_pool) (void)hipEventDestroy(e);
+      for (auto& kv : S.event_pool)
+        for (hipEvent_t e : kv.second) (void)hipEventDestroy(e);
       S.event_pool.clear();
       S.timing = false;
       S.totals = costa_timing{};
