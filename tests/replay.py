@@ -117,3 +117,26 @@ def stack_cases():
     A, B = pair(2048, 70, 4, 4)
     out.append(synth.Workload("stack4", "c64", [synth.Item(A, B, "N", 1.0, 0.0)], False, seed=65))
     return out
+
+
+def random_stack_case(seed):
+    """A random ScaLAPACK-descriptor pair whose row walks stack: 2 x 2 grids,
+    source blocks of 128-512 bytes of rows inside 128-row target blocks whose
+    first process row is the other one, random sizes and padded leading
+    dimensions (odd pads: single-element units), element type by seed, beta
+    0 for even seeds (stacks on both sides) and 0.5 for odd ones."""
+    rng = np.random.default_rng(1000 + seed)
+    SL = synth.ScaLapack
+    dtype = ["f64", "f32", "c128", "c64"][seed % 4]
+    es = synth.ITEMSIZE[dtype]
+    mb = int(rng.choice([128, 256, 512])) // es
+    m = int(rng.integers(1600, 2600))
+    n = int(rng.integers(8, 90))
+
+    def lld(mm, b):
+        return -(-(-(-mm // b)) // 2) * b + int(rng.integers(1, 9))
+    B = SL(m, n, mb, mb, 0, 0, lld(m, mb), 2, 2)
+    A = SL(m, n, 128, 128, 1, 0, lld(m, 128), 2, 2)
+    beta = 0.0 if seed % 2 == 0 else 0.5
+    return synth.Workload(f"rs{seed}", dtype, [synth.Item(A, B, "N", 1.0 if seed % 3 else 2.0, beta)], False,
+                          seed=300 + seed)

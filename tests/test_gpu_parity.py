@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from replay import many_rank_cases, short_walk_cases, stack_cases
+from replay import many_rank_cases, random_stack_case, short_walk_cases, stack_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -324,6 +324,19 @@ def test_stacked_walks_full_compare(k):
     w = stack_cases()[k]
     it = w.items[0]
     _say(f"stacked walks {k}: {w.dtype} {it.A.nrows}x{it.A.ncols} alpha={it.alpha} beta={it.beta}")
+    case = Case(w)
+    case.run()
+    case.check_full()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_stacked_layouts_full_compare(seed):
+    """Random ScaLAPACK-descriptor pairs whose walks stack (sizes, pads, first
+    processes, all four element types; beta 0 and 0.5), every element
+    compared."""
+    w = random_stack_case(seed)
+    it = w.items[0]
+    _say(f"random stacked layouts {seed}: {w.dtype} {it.A.nrows}x{it.A.ncols} beta={it.beta}")
     case = Case(w)
     case.run()
     case.check_full()

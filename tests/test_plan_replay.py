@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from replay import _combine, _index, many_rank_cases, short_walk_cases, stack_cases
+from replay import _combine, _index, many_rank_cases, random_stack_case, short_walk_cases, stack_cases
 
 C = pytest.importorskip("paper_2106_06601_amd")
 
@@ -508,3 +508,32 @@ def test_plans_do_not_depend_on_planner_threads(name, monkeypatch):
     assert np.array_equal(x1.view(np.uint8), x8.view(np.uint8))
     for k in ("waves", "workspace_bytes", "pieces_pack", "pieces_unpack", "pieces_direct", "model_bytes"):
         assert s1[k] == s8[k], k
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_stacked_layouts(seed):
+    """Random ScaLAPACK-descriptor pairs whose row walks stack: 2 x 2 grids,
+    source blocks of 128-512 bytes of rows inside 128-row target blocks
+    whose first process row is the other one, random sizes and padded
+    leading dimensions (odd pads: single-element units), every element
+    type, β = 0 (stacks on both sides) and β ≠ 0 (the pack's only):
+    the stacks' lane arithmetic moves each element once, and the plan
+    replayed rectangle by rectangle equals the oracle."""
+    w = random_stack_case(seed)
+    es = synth.ITEMSIZE[w.dtype]
+    beta = complex(w.items[0].beta)
+    descs, keep = _descs(w)
+    x = C.costa_plan_export(w.dtype, descs, None)
+    launches = {}
+    for i in range(len(x)):
+        launches.setdefault((int(x[i]["kind"]), int(x[i]["launch"])), []).append(x[i])
+    nstacked = 0
+    for (kind, _), ps in launches.items():
+        for k, cv in stack_walk_cover(ps, es).items():
+            nstacked += 1
+            assert (cv == 1).all()
+            if kind != PACK:
+                assert beta == 0
+    if beta == 0:
+        assert nstacked > 0, "the case has no stacks"
+    replay(w, padded=True)
