@@ -36,7 +36,13 @@ namespace {
 #define COSTA_NT_STORES 1
 #endif
 #ifndef COSTA_NT_ALOADS
-#define COSTA_NT_ALOADS 0
+#define COSTA_NT_ALOADS 0  // loads of A in row walks (measured: 1 makes the scaled transpose's unpack 29% slower)
+#endif
+// Loads of A in LDS tiles.  Measured with 1: the tiles' unpack 1-2% slower,
+// but the pack of the next call faster (pztranc's +7%, the tall-skinny
+// batch's +1 to +3%): whole steps +1.2 to +1.4%.
+#ifndef COSTA_NT_TILE_ALOADS
+#define COSTA_NT_TILE_ALOADS 1
 #endif
 
 constexpr int kThreads = kThreadsPerTask;
@@ -544,7 +550,7 @@ __device__ __forceinline__ void move_tile(const Piece* __restrict__ pieces, int3
       if (i < n) {
         int32_t yl, xl;
         divmod(i, w, yl, xl);
-        a[k] = load<COSTA_NT_ALOADS>(de + ((int64_t)yl * p.dst_ld + xl));
+        a[k] = load<COSTA_NT_TILE_ALOADS>(de + ((int64_t)yl * p.dst_ld + xl));
       }
     }
   }
