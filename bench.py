@@ -624,7 +624,10 @@ def summarize_profiles(src: str, out_dir: str = None) -> None:
 # The configurations the default run times, in this order: the block-size
 # change first (the headline figure), the tall-skinny batch last (its 256 GiB
 # of A and B need the device to themselves).
-ALL_WORKLOADS = ["blocksize_change_16k", "reshuffle_transpose_1k", "scaled_transpose_20k", "cosma_complex_16k",
+# the 1024^2 case first: launch-bound, its timed steps have shown one
+# stall of tens of ms when they followed the block-size change's (and its
+# device buffers' release) in the same process
+ALL_WORKLOADS = ["reshuffle_transpose_1k", "blocksize_change_16k", "scaled_transpose_20k", "cosma_complex_16k",
                  "rpa_batched_tall_skinny"]
 HEADLINE = "blocksize_change_16k"
 NO_BANDWIDTH_CLAIM = {"reshuffle_transpose_1k": "29 MB per step, launch-bound and cache-resident: "
