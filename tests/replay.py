@@ -140,3 +140,17 @@ def random_stack_case(seed):
     beta = 0.0 if seed % 2 == 0 else 0.5
     return synth.Workload(f"rs{seed}", dtype, [synth.Item(A, B, "N", 1.0 if seed % 3 else 2.0, beta)], False,
                           seed=300 + seed)
+
+
+def long_stack_case():
+    """Local columns of 70,000 rows cut into 16-row source blocks (128 bytes
+    of fp64), 3 columns: stacks longer than the 4096 rectangles a stack may
+    hold, so the planner cuts them."""
+    SL = synth.ScaLapack
+    m = 2 * 70000
+
+    def lld(mm, b):
+        return -(-(-(-mm // b)) // 2) * b + 3
+    B = SL(m, 3, 16, 16, 0, 0, lld(m, 16), 2, 1)
+    A = SL(m, 3, 128, 128, 1, 0, lld(m, 128), 2, 1)
+    return synth.Workload("long_stack", "f64", [synth.Item(A, B, "N", 1.0, 0.0)], False, seed=77)

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from replay import many_rank_cases, random_stack_case, short_walk_cases, stack_cases
+from replay import long_stack_case, many_rank_cases, random_stack_case, short_walk_cases, stack_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -337,6 +337,16 @@ def test_random_stacked_layouts_full_compare(seed):
     w = random_stack_case(seed)
     it = w.items[0]
     _say(f"random stacked layouts {seed}: {w.dtype} {it.A.nrows}x{it.A.ncols} beta={it.beta}")
+    case = Case(w)
+    case.run()
+    case.check_full()
+
+
+def test_stacks_longer_than_the_limit_full_compare():
+    """Stacks cut at 4096 rectangles (local columns of 70,000 rows in 16-row
+    source blocks), every element compared."""
+    w = long_stack_case()
+    _say("long stacks: fp64 140000x3")
     case = Case(w)
     case.run()
     case.check_full()

@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from replay import _combine, _index, many_rank_cases, random_stack_case, short_walk_cases, stack_cases
+from replay import _combine, _index, long_stack_case, many_rank_cases, random_stack_case, short_walk_cases, stack_cases
 
 C = pytest.importorskip("paper_2106_06601_amd")
 
@@ -536,4 +536,21 @@ def test_random_stacked_layouts(seed):
                 assert beta == 0
     if beta == 0:
         assert nstacked > 0, "the case has no stacks"
+    replay(w, padded=True)
+
+
+def test_stacks_longer_than_the_limit_are_cut():
+    """A local column of 4375 stackable rectangles: stacks of at most 4096,
+    each element moved once, the plan equal to the oracle."""
+    w = long_stack_case()
+    descs, keep = _descs(w)
+    x = C.costa_plan_export(w.dtype, descs, None)
+    sizes = x["flags"] >> 16
+    assert sizes.max() == 4096 and (sizes > 0).sum() >= 3
+    launches = {}
+    for i in range(len(x)):
+        launches.setdefault((int(x[i]["kind"]), int(x[i]["launch"])), []).append(x[i])
+    for ps in launches.values():
+        for k, cv in stack_walk_cover(ps, 8).items():
+            assert (cv == 1).all()
     replay(w, padded=True)
