@@ -597,7 +597,17 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
   }
   if (b > INT32_MAX) throw LimitExceeded("more than 2^31-1 workgroups in one launch");
   lr.ntasks = b;
-  fill_tasks(hp.tasks, seg, b);
+  // Which tables the kernels read (the units per lane of each launch): the
+  // pack always copies (the wide table, unless COSTA_COPY_UNITS is 1); an
+  // unpack or direct launch copies only in calls that read no A, and a plan
+  // built for pairs that read A serves only such calls (reads_a is part of
+  // the plan key), so its launches never read the wide table.  The first
+  // tasks and counts of both are kept whatever is filled.
+  bool plan_reads_a = false;
+  for (char r : hp.item_reads_a) plan_reads_a = plan_reads_a || r;
+  const bool need_narrow = !is_pack || COSTA_COPY_UNITS <= 1;
+  const bool need_wide = is_pack ? COSTA_COPY_UNITS > 1 : !plan_reads_a;
+  if (need_narrow) fill_tasks(hp.tasks, seg, b);
   // the wide task table of a launch of row walks: kWideTaskUnits units per
   // task, a run of small rectangles still one task
   lr.wide_begin = (int64_t)hp.wide_tasks.size();
@@ -625,7 +635,7 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
       b2 += n;
     }
     lr.nwide = b2;
-    fill_tasks(hp.wide_tasks, seg, b2);
+    if (need_wide) fill_tasks(hp.wide_tasks, seg, b2);
   }
   int64_t aligned = 0, transposed = 0;
   for (const Piece& p : ps) {
