@@ -22,6 +22,7 @@
 #include <exception>
 #include <new>
 #include <numeric>
+#include <system_error>
 #include <thread>
 #include <tuple>
 
@@ -88,7 +89,13 @@ void parallel_for(int64_t n, int threads, Fn&& fn) {
   };
   std::vector<std::thread> pool;
   pool.reserve((size_t)nt - 1);
-  for (int64_t w = 1; w < nt; ++w) pool.emplace_back(worker, w);
+  int64_t started = 1;
+  try {
+    for (; started < nt; ++started) pool.emplace_back(worker, started);
+  } catch (const std::system_error&) {
+    // no more threads: the calling thread takes the shares not started
+  }
+  for (int64_t w = started; w < nt; ++w) worker(w);
   worker(0);
   for (std::thread& th : pool) th.join();
   for (const std::exception_ptr& e : err)
