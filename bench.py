@@ -750,7 +750,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the transform's virtual ranks all live in "
-              "one GPU's HBM and this build has no multi-GPU exchange", file=sys.stderr)
+              "one GPU's HBM and the library has no multi-GPU exchange", file=sys.stderr)
         sys.exit(2)
 
     import torch

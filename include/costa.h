@@ -58,7 +58,7 @@ typedef enum {
   COSTA_ERROR_SHAPE_MISMATCH = 2, /* A is not the shape of op(B), or the process counts differ */
   COSTA_ERROR_OUT_OF_MEMORY = 3,  /* not even one wave of message buffers fits on the device */
   COSTA_ERROR_DEVICE = 4,         /* a HIP call failed */
-  COSTA_ERROR_NOT_SUPPORTED = 5   /* a valid request this build does not handle */
+  COSTA_ERROR_NOT_SUPPORTED = 5   /* a valid request the library does not handle */
 } costa_status;
 
 /* op of equation (eq:costa); for real types C equals T. */
