@@ -423,6 +423,16 @@ void finish_piece(Piece& p, int elem_size) {
 #ifndef COSTA_XCD_STACKS
 #define COSTA_XCD_STACKS 0
 #endif
+// Row strides (bytes) from which rows count as far apart: such row walks
+// cost more per task than walks of nearby rows, so a launch that holds both
+// is not of one kind for the XCD ranges (measured on MI355X: the tall-skinny
+// batch's pack, identity pairs with rows 32 KiB apart and transposed pairs
+// with rows 4 MiB apart, +6 to +8% without the ranges, its step +2.5%; the
+// transposed pairs alone -2 to -13% without them); it also decides the pack
+// order below.
+#ifndef COSTA_PACK_FAR_ROWS
+#define COSTA_PACK_FAR_ROWS (1 << 20)
+#endif
 
 // Whether every run of the rectangle (its rows in the source and in the
 // destination) starts and ends on a 128-byte line.
@@ -644,12 +654,14 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
     lr.nwide = b2;
     if (need_wide) fill_tasks(hp.wide_tasks, seg, b2);
   }
-  int64_t aligned = 0, transposed = 0;
+  int64_t aligned = 0, transposed = 0, far = 0, near = 0;
   for (const Piece& p : ps) {
-    if (line_aligned(p, es) || (COSTA_XCD_STACKS && (p.flags & PIECE_STACK))) aligned += (int64_t)p.nx * p.ny;
-    if (p.flags & PIECE_TRANSPOSE) transposed += (int64_t)p.nx * p.ny;
+    const int64_t ne = (int64_t)p.nx * p.ny;
+    if (line_aligned(p, es) || (COSTA_XCD_STACKS && (p.flags & PIECE_STACK))) aligned += ne;
+    if (p.flags & PIECE_TRANSPOSE) transposed += ne;
+    else if (p.ny > 1) (std::max(p.src_ld, p.dst_ld) * es >= COSTA_PACK_FAR_ROWS ? far : near) += ne;
   }
-  const bool one_kind = transposed == 0 || transposed == lr.elems;
+  const bool one_kind = (transposed == 0 || transposed == lr.elems) && (far == 0 || near == 0);
   lr.xcd_ranges = COSTA_XCD_RANGES && one_kind && lr.elems > 0 && 10 * aligned >= COSTA_XCD_ALIGNED_TENTHS * lr.elems ? 1 : 0;
   hp.pieces.insert(hp.pieces.end(), ps.begin(), ps.end());
   return lr;
@@ -657,9 +669,6 @@ LaunchRange add_launch(HostPlan& hp, std::vector<Piece>& ps, int es, int32_t nit
 
 #ifndef COSTA_PACK_BY_SOURCE
 #define COSTA_PACK_BY_SOURCE 1
-#endif
-#ifndef COSTA_PACK_FAR_ROWS
-#define COSTA_PACK_FAR_ROWS (1 << 20)
 #endif
 // Split an unpack or direct launch that holds both row walks and LDS tiles
 // into one launch of each kind (tiles first), so that each can take the
