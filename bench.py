@@ -21,6 +21,7 @@ identity op, alpha = 1, beta = 0, relabeling on.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -697,6 +698,7 @@ def run_workload(name: str, args, cpu_seconds: float) -> dict:
            "pct_of_hbm_peak": round(100 * m["value"] / HBM_PEAK_GBS, 2), "dtype": w.dtype,
            "config": describe(w),
            "ms_per_step_median": m["ms_per_step_median"], "ms_per_step_min": m["ms_per_step_min"],
+           "ms_per_step_max": m["ms_per_step_max"],
            "model_bytes_per_step": stats["model_bytes"],
            "bytes_without_staging_per_step": stats["model_bytes"] - 2 * stats["message_bytes"],
            "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
@@ -780,7 +782,8 @@ def main():
            "warmup": args.warmup, "ms_per_step": head["ms_per_step"], "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": head["dtype"], "data": "synthetic",
            "pct_of_hbm_peak": head["pct_of_hbm_peak"], "config": head["config"]}
-    for k in ("ms_per_step_median", "ms_per_step_min", "model_bytes_per_step", "bytes_without_staging_per_step",
+    for k in ("ms_per_step_median", "ms_per_step_min", "ms_per_step_max", "model_bytes_per_step",
+              "bytes_without_staging_per_step",
               "local_fraction", "waves", "plan_s", "kernels", "roofline", "copy_ceiling", "cpu_baseline"):
         if k in head:
             out[k] = head[k]
@@ -816,14 +819,24 @@ def measure(step, stats: dict, workload: str, args) -> dict:
 
     C.costa_timing_enable(True)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    ev[0].record(stream)
-    for i in range(args.steps):
-        step()
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    # no garbage collection inside the timed steps: a full collection of the
+    # objects earlier workloads left holds the host for tens of ms, long
+    # enough for the GPU to run out of queued steps
+    gc.collect()
+    gc_was_on = gc.isenabled()
+    gc.disable()
+    try:
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        ev[0].record(stream)
+        for i in range(args.steps):
+            step()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+    finally:
+        if gc_was_on:
+            gc.enable()
     kt = C.costa_timing_read()
     C.costa_timing_enable(False)
     gpu_ms = ev[0].elapsed_time(ev[-1])
@@ -848,7 +861,8 @@ def measure(step, stats: dict, workload: str, args) -> dict:
             "bytes_per_launch": dk["bytes_per_launch"], "ms_per_launch": dk["ms_per_launch"]}
     return {"value": round(value, 1), "ms_per_step": round(ms_per_step, 4), "kernels": per_kernel,
             "roofline": roof, "first_step_s": first_step_s,
-            "ms_per_step_median": round(per_step[len(per_step) // 2], 4), "ms_per_step_min": round(per_step[0], 4)}
+            "ms_per_step_median": round(per_step[len(per_step) // 2], 4), "ms_per_step_min": round(per_step[0], 4),
+            "ms_per_step_max": round(per_step[-1], 4)}
 
 
 def copy_ceiling(dev, stream, mib: int = 1024, reps: int = 10):
@@ -952,6 +966,7 @@ def scalapack_bench(name: str, args) -> dict:
                        "source": dsc(call.A) + f", submatrix at ({call.ia}, {call.ja})",
                        "target": dsc(call.C) + f", submatrix at ({call.ic}, {call.jc})"},
             "ms_per_step_median": m["ms_per_step_median"], "ms_per_step_min": m["ms_per_step_min"],
+            "ms_per_step_max": m["ms_per_step_max"],
             "model_bytes_per_step": stats["model_bytes"],
             "bytes_without_staging_per_step": stats["model_bytes"] - 2 * stats["message_bytes"],
             "local_fraction": round(stats["local_elems"] / stats["total_elems"], 6),
